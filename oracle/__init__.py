@@ -1,0 +1,190 @@
+"""CPU oracle for the Kareus schedule-search hot path -- TEST INFRASTRUCTURE ONLY.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may import this
+package.  It loads `liboracle.so`, built from `kareus_oracle.c` with gcc (no FMA
+contraction, no fast-math), and wraps it with numpy arrays.  It shares no code with
+the HIP library and never imports it.
+
+The C source cites, per function, the passage of the paper it follows.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "kareus_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+CFLAGS = ["-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared"]
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc; returns the library path."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB)
+        dp = ctypes.POINTER(ctypes.c_double)
+        ip = ctypes.POINTER(ctypes.c_int32)
+        lp = ctypes.POINTER(ctypes.c_int64)
+        i, d = ctypes.c_int, ctypes.c_double
+        lib.oracle_evaluate.argtypes = [i, i, i, i, i, d, dp, dp, dp, dp, dp, dp]
+        lib.oracle_pareto.argtypes = [ctypes.c_int64, dp, dp, ip, lp]
+        lib.oracle_compose.argtypes = [i, lp, dp, dp, i, d, dp, ip, ip, dp, ip]
+        lib.oracle_staircase.argtypes = [i, dp, d, d, ip, dp, dp, ip]
+        lib.oracle_extract.argtypes = [i, i, lp, dp, dp, ip, ip, ctypes.c_int32, ip, dp, dp]
+        for fn in ("oracle_evaluate", "oracle_pareto", "oracle_compose", "oracle_staircase",
+                   "oracle_extract"):
+            getattr(lib, fn).restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _p(a: np.ndarray, ct):
+    return a.ctypes.data_as(ctypes.POINTER(ct))
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def evaluate_partition(space, t, pw, tc, pc, part: int = 0):
+    """Time and energy of every candidate of partition `part`: (T, E) float64[n_cand]."""
+    lib = _load()
+    tp, pwp = _f64(t[part]), _f64(pw[part])
+    tcp, pcp = _f64(tc[part]), _f64(pc[part])
+    n = space.n_cand
+    T = np.empty(n)
+    E = np.empty(n)
+    rc = lib.oracle_evaluate(space.n_kernels, space.n_comm, space.n_freq, space.n_sm,
+                             space.n_pos, float(space.p_static), _p(tp, ctypes.c_double),
+                             _p(pwp, ctypes.c_double), _p(tcp, ctypes.c_double),
+                             _p(pcp, ctypes.c_double), _p(T, ctypes.c_double),
+                             _p(E, ctypes.c_double))
+    if rc != 0:
+        raise OracleError("oracle_evaluate failed: %d" % rc)
+    return T, E
+
+
+def pareto(T, E):
+    """Indices of the non-dominated points, in ascending time."""
+    lib = _load()
+    T, E = _f64(T), _f64(E)
+    out = np.empty(max(len(T), 1), dtype=np.int32)
+    n_out = ctypes.c_int64(0)
+    rc = lib.oracle_pareto(len(T), _p(T, ctypes.c_double), _p(E, ctypes.c_double),
+                           _p(out, ctypes.c_int32), ctypes.byref(n_out))
+    if rc != 0:
+        raise OracleError("oracle_pareto failed: %d" % rc)
+    return out[: n_out.value].copy()
+
+
+def evaluate_and_filter(space, t, pw, tc, pc, parts: Optional[range] = None):
+    """Per partition: (frontier candidate indices, T, E)."""
+    res = []
+    for p in (parts if parts is not None else range(space.n_parts)):
+        T, E = evaluate_partition(space, t, pw, tc, pc, p)
+        idx = pareto(T, E)
+        res.append((idx, T[idx], E[idx]))
+    return res
+
+
+class Composed:
+    def __init__(self, F, bp, pt_bin, delta, tmin_sum, L):
+        self.F, self.bp, self.pt_bin = F, bp, pt_bin
+        self.delta, self.tmin_sum, self.L = delta, tmin_sum, L
+
+
+def compose(off, T, E, n_bins: int, delta: float = 0.0) -> Composed:
+    lib = _load()
+    off = np.ascontiguousarray(off, dtype=np.int64)
+    T, E = _f64(T), _f64(E)
+    P = len(off) - 1
+    F = np.empty(n_bins)
+    bp = np.empty((P, n_bins), dtype=np.int32)
+    pt = np.empty(max(int(off[-1]), 1), dtype=np.int32)
+    info = np.empty(2)
+    L = ctypes.c_int32(0)
+    rc = lib.oracle_compose(P, _p(off, ctypes.c_int64), _p(T, ctypes.c_double),
+                            _p(E, ctypes.c_double), n_bins, float(delta),
+                            _p(F, ctypes.c_double), _p(bp, ctypes.c_int32),
+                            _p(pt, ctypes.c_int32), _p(info, ctypes.c_double), ctypes.byref(L))
+    if rc != 0:
+        raise OracleError("oracle_compose failed: %d" % rc)
+    return Composed(F, bp, pt[: int(off[-1])], float(info[0]), float(info[1]), int(L.value))
+
+
+def staircase(F, delta: float, tmin_sum: float):
+    """(bins int32, T_lo float64, E float64) of the non-dominated composite bins."""
+    lib = _load()
+    F = _f64(F)
+    B = len(F)
+    bins = np.empty(B, dtype=np.int32)
+    tlo = np.empty(B)
+    e = np.empty(B)
+    n = ctypes.c_int32(0)
+    lib.oracle_staircase(B, _p(F, ctypes.c_double), float(delta), float(tmin_sum),
+                         _p(bins, ctypes.c_int32), _p(tlo, ctypes.c_double),
+                         _p(e, ctypes.c_double), ctypes.byref(n))
+    k = n.value
+    return bins[:k].copy(), tlo[:k].copy(), e[:k].copy()
+
+
+def extract(off, T, E, comp: Composed, bin_: int):
+    """(choice int32[P], T_sum, E_sum) behind composite bin `bin_`."""
+    lib = _load()
+    off = np.ascontiguousarray(off, dtype=np.int64)
+    T, E = _f64(T), _f64(E)
+    P = len(off) - 1
+    B = comp.bp.shape[1]
+    choice = np.empty(P, dtype=np.int32)
+    ts = ctypes.c_double(0.0)
+    es = ctypes.c_double(0.0)
+    bp = np.ascontiguousarray(comp.bp, dtype=np.int32)
+    pt = np.ascontiguousarray(comp.pt_bin, dtype=np.int32)
+    rc = lib.oracle_extract(P, B, _p(off, ctypes.c_int64), _p(T, ctypes.c_double),
+                            _p(E, ctypes.c_double), _p(bp, ctypes.c_int32),
+                            _p(pt, ctypes.c_int32), int(bin_), _p(choice, ctypes.c_int32),
+                            ctypes.byref(ts), ctypes.byref(es))
+    if rc != 0:
+        raise OracleError("oracle_extract failed for bin %d: %d" % (bin_, rc))
+    return choice, ts.value, es.value
+
+
+def decode(space, idx: int):
+    """Candidate index -> (f, positions tuple, SM-choice tuple), the oracle's order."""
+    S = space.n_sm
+    if space.n_comm == 1:
+        s = idx % S
+        rest = idx // S
+        return rest // space.n_pos, (rest % space.n_pos,), (s,)
+    s2 = idx % S
+    s1 = (idx // S) % S
+    rest = idx // (S * S)
+    f, pp = divmod(rest, space.n_pairs)
+    for p1 in range(space.n_pos):
+        width = space.n_pos - p1
+        if pp < width:
+            return f, (p1, p1 + pp), (s1, s2)
+        pp -= width
+    raise ValueError(idx)

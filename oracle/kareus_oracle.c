@@ -1,0 +1,458 @@
+/*
+ * Kareus schedule-search hot path: CPU ORACLE.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may call, link or load this
+ * file; only the tests, the smoke check and the benchmark's CPU-baseline leg use it.
+ * It is plain, slow and single-threaded on purpose, and shares no code, header, table
+ * or helper with the HIP library.  Build: gcc -O2 -ffp-contract=off -fPIC -shared.
+ *
+ * What it computes (Kareus, "Joint Reduction of Dynamic and Static Energy in Large
+ * Model Training"):
+ *   oracle_evaluate   time and energy of every candidate execution schedule of one
+ *                     partition (Sections 4.1-4.2; energy model of Sections 2.1, 2.3,
+ *                     4.3.2 and 4.5).  The paper gives no closed-form cost model
+ *                     (Section 4.3.1 says time and energy come from profiling), so
+ *                     this follows a fluid SM-share reading written out below.
+ *   oracle_pareto     GetFrontier: the non-dominated (time, energy) set (Algorithm 1's
+ *                     return value; Algorithm 2's last step).
+ *   oracle_compose    partition frontiers -> summed (time, energy) over every choice
+ *                     of one point per partition, pruned to a frontier (Section 4.4,
+ *                     Algorithm 2), done as a min-plus recurrence over a discretised
+ *                     time axis.
+ *   oracle_staircase  the non-dominated points of the composed array.
+ *   oracle_extract    the per-partition choice behind a composed point (schedule
+ *                     selection for a target latency, Section 5.1).
+ *
+ * Every floating-point line is one IEEE fp64 rounding in the written order; the file
+ * must be compiled without FMA contraction and without fast-math.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define OR_OK 0
+#define OR_EINVAL -1
+#define OR_ECAPACITY -3
+
+/* ------------------------------------------------------------------------------
+ * Cost model of one partition (Sections 3.2 and 4.2).
+ *
+ * A partition holds N compute kernels that run in order on the compute stream and M
+ * (1 or 2) communication kernels with no data dependence on them (Section 4.2).  A
+ * candidate fixes the GPU frequency f, and for each comm kernel m its launch
+ * position p_m and SM choice s_m (Section 4.1).
+ *
+ * Readings (the paper is silent; Sections 4.3.1 and Appendix B):
+ *  - launch position p means the comm kernel is launched together with compute
+ *    kernel p, i.e. when compute reaches the start of kernel p; p = N launches it
+ *    after the last compute kernel (fully exposed) (Section 3.2.2).
+ *  - SMs given to communication are taken from compute (Section 3.2.1): while comm m
+ *    runs, compute runs in SM state sigma_m = s_m + 1, whose per-kernel time and
+ *    power come from the tables; otherwise it runs in state 0 (all SMs).
+ *  - progress is fluid: a kernel interrupted by a state change keeps the finished
+ *    fraction of its work.
+ *  - comm kernels share one comm stream in FIFO order (Section 5.2: compute and comm
+ *    on separate streams, events for launch timing); comm m starts at the later of
+ *    its launch and the end of comm m-1, and runs for tc regardless of compute.
+ *  - energy = static power x partition time + dynamic energy of compute and comm
+ *    (Sections 2.1, 2.3 and 4.5); idle compute draws no dynamic power; the
+ *    partition ends when both compute and the last comm kernel have finished.
+ * ---------------------------------------------------------------------------- */
+
+typedef struct {
+    int N;            /* compute kernels */
+    int S1;           /* SM states = S + 1 */
+    const double *t;  /* [N][S1] kernel time in each state, this frequency */
+    const double *pw; /* [N][S1] kernel dynamic power in each state */
+    const double *A;  /* [S1][N+1] A[s][i] = sum_{j<i} t[j][s], left to right */
+    const double *B;  /* [S1][N+1] B[s][i] = sum_{j<i} pw[j][s]*t[j][s] */
+    int i;            /* kernel in progress (or next to start) */
+    double w;         /* unfinished fraction of kernel i (1.0 = not started) */
+    double Ec;        /* compute dynamic energy so far */
+} walk_state;
+
+#define TT(W, j, s) ((W)->t[(size_t)(j) * (W)->S1 + (s)])
+#define PW(W, j, s) ((W)->pw[(size_t)(j) * (W)->S1 + (s)])
+#define AA(W, s, j) ((W)->A[(size_t)(s) * ((W)->N + 1) + (j)])
+#define BB(W, s, j) ((W)->B[(size_t)(s) * ((W)->N + 1) + (j)])
+
+/* Run compute in SM state s for at most `budget` seconds or until it reaches the
+ * start of kernel `stop` (i <= stop <= N).  Sets *elapsed; returns 1 if `stop` was
+ * reached, 0 if the budget ran out first. */
+static int run_compute(walk_state *W, int s, double budget, int stop, double *elapsed)
+{
+    double used = 0.0;
+    if (W->w < 1.0) {
+        /* finish the interrupted kernel first */
+        double need = W->w * TT(W, W->i, s);
+        if (need <= budget) {
+            W->Ec = W->Ec + PW(W, W->i, s) * need;
+            used = need;
+            W->i = W->i + 1;
+            W->w = 1.0;
+        } else {
+            W->Ec = W->Ec + PW(W, W->i, s) * budget;
+            W->w = W->w - budget / TT(W, W->i, s);
+            if (W->w < 0.0) W->w = 0.0;
+            *elapsed = budget;
+            return 0;
+        }
+    }
+    double rb = budget - used;
+    /* whole kernels that fit: the largest j in [i, stop] with A[j] - A[i] <= rb */
+    int i0 = W->i;
+    int j = i0;
+    while (j < stop && (AA(W, s, j + 1) - AA(W, s, i0)) <= rb) j = j + 1;
+    W->Ec = W->Ec + (BB(W, s, j) - BB(W, s, i0));
+    if (j == stop) {
+        *elapsed = used + (AA(W, s, j) - AA(W, s, i0));
+        W->i = j;
+        return 1;
+    }
+    /* budget ends inside kernel j */
+    double r = rb - (AA(W, s, j) - AA(W, s, i0));
+    W->Ec = W->Ec + PW(W, j, s) * r;
+    W->w = 1.0 - r / TT(W, j, s);
+    if (W->w < 0.0) W->w = 0.0;
+    W->i = j;
+    *elapsed = budget;
+    return 0;
+}
+
+/* Time and energy of one candidate at one frequency.
+ * tcm, pcm: comm time and power of each comm kernel under its SM choice. */
+static void cost_one(walk_state *W, int M, const int *pos, const int *sigma,
+                     const double *tcm, const double *pcm, double p_static,
+                     double *T_out, double *E_out)
+{
+    double tau = 0.0, el = 0.0, T = 0.0;
+    int m, done = 0;
+    W->i = 0;
+    W->w = 1.0;
+    W->Ec = 0.0;
+    for (m = 0; m < M; m++) {
+        if (W->i < pos[m]) { /* compute has not yet reached the launch point */
+            run_compute(W, 0, INFINITY, pos[m], &el);
+            tau = tau + el;
+        }
+        double start = tau; /* FIFO: tau is also the end of comm m-1 */
+        if (run_compute(W, sigma[m], tcm[m], W->N, &el)) {
+            /* compute finished while comm m ran; later comm kernels follow it */
+            T = start + tcm[m];
+            for (int q = m + 1; q < M; q++) T = T + tcm[q];
+            done = 1;
+            break;
+        }
+        tau = start + tcm[m];
+    }
+    if (!done) {
+        run_compute(W, 0, INFINITY, W->N, &el);
+        T = tau + el;
+    }
+    double E = p_static * T;
+    E = E + W->Ec;
+    for (m = 0; m < M; m++) E = E + pcm[m] * tcm[m];
+    *T_out = T;
+    *E_out = E;
+}
+
+/* Candidate index (frequency slowest, SM choice fastest):
+ *   M = 1: idx = (f * n_pos + p) * S + s
+ *   M = 2: pairs p1 <= p2 ranked lexicographically as pp;
+ *          idx = (f * n_pp + pp) * S * S + s1 * S + s2
+ * One partition; t, pw: [F][N][S+1]; tc, pc: [F][M][S]; T_out, E_out: [n_cand]. */
+int oracle_evaluate(int N, int M, int F, int S, int n_pos, double p_static,
+                    const double *t, const double *pw, const double *tc, const double *pc,
+                    double *T_out, double *E_out)
+{
+    if (N < 1 || (M != 1 && M != 2) || F < 1 || S < 1 || n_pos < 1 || n_pos > N + 1)
+        return OR_EINVAL;
+    int S1 = S + 1;
+    double *A = (double *)malloc(sizeof(double) * (size_t)S1 * (N + 1));
+    double *B = (double *)malloc(sizeof(double) * (size_t)S1 * (N + 1));
+    if (!A || !B) { free(A); free(B); return OR_EINVAL; }
+    long long idx = 0;
+    for (int f = 0; f < F; f++) {
+        const double *tf = t + (size_t)f * N * S1;
+        const double *pwf = pw + (size_t)f * N * S1;
+        const double *tcf = tc + (size_t)f * M * S;
+        const double *pcf = pc + (size_t)f * M * S;
+        for (int s = 0; s < S1; s++) {
+            A[(size_t)s * (N + 1)] = 0.0;
+            B[(size_t)s * (N + 1)] = 0.0;
+            for (int i = 0; i < N; i++) {
+                double ti = tf[(size_t)i * S1 + s];
+                A[(size_t)s * (N + 1) + i + 1] = A[(size_t)s * (N + 1) + i] + ti;
+                B[(size_t)s * (N + 1) + i + 1] =
+                    B[(size_t)s * (N + 1) + i] + (pwf[(size_t)i * S1 + s] * ti);
+            }
+        }
+        walk_state W = {N, S1, tf, pwf, A, B, 0, 1.0, 0.0};
+        int pos[2], sig[2];
+        double tcm[2], pcm[2];
+        if (M == 1) {
+            for (int p = 0; p < n_pos; p++)
+                for (int s = 0; s < S; s++) {
+                    pos[0] = p;
+                    sig[0] = s + 1;
+                    tcm[0] = tcf[s];
+                    pcm[0] = pcf[s];
+                    cost_one(&W, 1, pos, sig, tcm, pcm, p_static, &T_out[idx], &E_out[idx]);
+                    idx++;
+                }
+        } else {
+            for (int p1 = 0; p1 < n_pos; p1++)
+                for (int p2 = p1; p2 < n_pos; p2++)
+                    for (int s1 = 0; s1 < S; s1++)
+                        for (int s2 = 0; s2 < S; s2++) {
+                            pos[0] = p1;
+                            pos[1] = p2;
+                            sig[0] = s1 + 1;
+                            sig[1] = s2 + 1;
+                            tcm[0] = tcf[s1];
+                            pcm[0] = pcf[s1];
+                            tcm[1] = tcf[S + s2];
+                            pcm[1] = pcf[S + s2];
+                            cost_one(&W, 2, pos, sig, tcm, pcm, p_static, &T_out[idx],
+                                     &E_out[idx]);
+                            idx++;
+                        }
+        }
+    }
+    free(A);
+    free(B);
+    return OR_OK;
+}
+
+/* ------------------------------------------------------------------------------
+ * GetFrontier (Algorithm 1's return value, Algorithm 2's last step).
+ * A point is kept iff no other point is at least as good in both time and energy
+ * and strictly better in one; of exact (time, energy) duplicates the smallest index
+ * is kept.  Done as: sort by (T, E, index), keep a point iff its energy is strictly
+ * below every energy before it.  Output is in ascending time.
+ * ---------------------------------------------------------------------------- */
+static const double *g_T, *g_E;
+
+static int cmp_tei(const void *a, const void *b)
+{
+    int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+    if (g_T[x] < g_T[y]) return -1;
+    if (g_T[x] > g_T[y]) return 1;
+    if (g_E[x] < g_E[y]) return -1;
+    if (g_E[x] > g_E[y]) return 1;
+    return (x > y) - (x < y);
+}
+
+int oracle_pareto(int64_t n, const double *T, const double *E, int32_t *out_idx, int64_t *n_out)
+{
+    if (n < 0) return OR_EINVAL;
+    int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+    if (!order) return OR_EINVAL;
+    for (int64_t k = 0; k < n; k++) order[k] = (int32_t)k;
+    g_T = T;
+    g_E = E;
+    qsort(order, (size_t)n, sizeof(int32_t), cmp_tei);
+    double best = INFINITY;
+    int64_t kept = 0;
+    for (int64_t k = 0; k < n; k++) {
+        int32_t c = order[k];
+        if (E[c] < best) {
+            out_idx[kept++] = c;
+            best = E[c];
+        }
+    }
+    *n_out = kept;
+    free(order);
+    return OR_OK;
+}
+
+/* ------------------------------------------------------------------------------
+ * Composition of partition frontiers (Section 4.4, Algorithm 2).
+ *
+ * The microbatch runs its partitions one after another, so one choice per partition
+ * gives time = sum of times and energy = sum of energies; the composed frontier is
+ * GetFrontier over every such combination.  Instead of enumerating the Cartesian
+ * product, time is discretised: with bin width delta, point j of partition k sits at
+ * offset off_k[j] = floor((T_k[j] - tmin_k) / delta), and
+ *     F_1[b] = e_1[b],   F_k[b] = min_{b2} F_{k-1}[b - b2] + e_k[b2]
+ * where e_k[b2] is the least energy among partition k's points at offset b2.  F_P[b]
+ * is the least total energy of any combination whose offsets add up to b, i.e. whose
+ * time lies in [tmin_sum + b*delta, tmin_sum + (b+P)*delta).
+ *
+ * Readings: delta = (sum_k (tmax_k - tmin_k)) / (B - 1) (1.0 if that sum is 0), or
+ * the caller's delta > 0; with an automatic delta it is nudged up one ulp at a time
+ * until 1 + sum_k floor(range_k / delta) <= B.  Ties in e_k go to the smallest point
+ * index; ties in the min-plus go to the smallest b2.
+ *
+ * off [P+1] point offsets; T, E [off[P]] points; F_out [B]; bp_out [P][B] point
+ * index chosen for partition k at composite bin b (-1 = unreachable); pt_bin_out
+ * [off[P]] the offset of every point; info_out[0] = delta, info_out[1] = tmin_sum;
+ * L_out = number of bins reachable (1 + sum_k M_k).
+ * ---------------------------------------------------------------------------- */
+int oracle_compose(int P, const int64_t *off, const double *T, const double *E, int B,
+                   double delta_in, double *F_out, int32_t *bp_out, int32_t *pt_bin_out,
+                   double *info_out, int32_t *L_out)
+{
+    if (P < 1 || B < 2) return OR_EINVAL;
+    for (int k = 0; k < P; k++)
+        if (off[k + 1] <= off[k]) return OR_EINVAL;
+    double *tmin = (double *)malloc(sizeof(double) * P);
+    double *range = (double *)malloc(sizeof(double) * P);
+    int64_t *Mk = (int64_t *)malloc(sizeof(int64_t) * P);
+    double *e = (double *)malloc(sizeof(double) * (size_t)B);
+    int32_t *arg = (int32_t *)malloc(sizeof(int32_t) * (size_t)B);
+    double *Fprev = (double *)malloc(sizeof(double) * (size_t)B);
+    double *Fcur = (double *)malloc(sizeof(double) * (size_t)B);
+    int rc = OR_OK;
+    if (!tmin || !range || !Mk || !e || !arg || !Fprev || !Fcur) { rc = OR_EINVAL; goto done; }
+
+    /* 1. per-partition time range */
+    for (int k = 0; k < P; k++) {
+        double lo = T[off[k]], hi = T[off[k]];
+        for (int64_t j = off[k]; j < off[k + 1]; j++) {
+            if (T[j] < lo) lo = T[j];
+            if (T[j] > hi) hi = T[j];
+        }
+        tmin[k] = lo;
+        range[k] = hi - lo;
+    }
+    /* 2-3. bin width and per-partition bin counts */
+    double R = 0.0;
+    for (int k = 0; k < P; k++) R = R + range[k];
+    double delta;
+    if (delta_in > 0.0) delta = delta_in;
+    else if (R > 0.0) delta = R / (double)(B - 1);
+    else delta = 1.0;
+    for (;;) {
+        int64_t total = 1;
+        for (int k = 0; k < P; k++) {
+            Mk[k] = (int64_t)floor(range[k] / delta);
+            total += Mk[k];
+        }
+        if (total <= B) break;
+        if (delta_in > 0.0) { rc = OR_ECAPACITY; goto done; }
+        delta = nextafter(delta, INFINITY);
+    }
+    double tmin_sum = 0.0;
+    for (int k = 0; k < P; k++) tmin_sum = tmin_sum + tmin[k];
+
+    /* 4. offsets of every point */
+    for (int k = 0; k < P; k++)
+        for (int64_t j = off[k]; j < off[k + 1]; j++) {
+            int64_t o = (int64_t)floor((T[j] - tmin[k]) / delta);
+            if (o > Mk[k]) o = Mk[k];
+            pt_bin_out[j] = (int32_t)o;
+        }
+
+    for (int64_t x = 0; x < (int64_t)P * B; x++) bp_out[x] = -1;
+    int64_t L = 0;
+    for (int k = 0; k < P; k++) {
+        /* 5. least energy per offset of partition k (ties: smallest point index) */
+        for (int64_t b = 0; b <= Mk[k]; b++) {
+            e[b] = INFINITY;
+            arg[b] = -1;
+        }
+        for (int64_t j = off[k]; j < off[k + 1]; j++) {
+            int32_t b = pt_bin_out[j];
+            if (E[j] < e[b]) {
+                e[b] = E[j];
+                arg[b] = (int32_t)(j - off[k]);
+            }
+        }
+        int32_t *bpk = bp_out + (size_t)k * B;
+        if (k == 0) {
+            /* 6. F_1 = e_1 */
+            L = Mk[0] + 1;
+            for (int64_t b = 0; b < B; b++) Fcur[b] = INFINITY;
+            for (int64_t b = 0; b < L; b++) {
+                Fcur[b] = e[b];
+                bpk[b] = arg[b];
+            }
+        } else {
+            /* 7. min-plus step, plain double loop */
+            int64_t Lnew = L + Mk[k];
+            for (int64_t b = 0; b < B; b++) Fcur[b] = INFINITY;
+            for (int64_t b = 0; b < Lnew; b++) {
+                double best = INFINITY;
+                int32_t who = -1;
+                for (int64_t b2 = 0; b2 <= Mk[k]; b2++) {
+                    int64_t a = b - b2;
+                    if (a < 0 || a >= L) continue;
+                    if (!(Fprev[a] < INFINITY) || !(e[b2] < INFINITY)) continue;
+                    double v = Fprev[a] + e[b2];
+                    if (v < best) {
+                        best = v;
+                        who = arg[b2];
+                    }
+                }
+                Fcur[b] = best;
+                bpk[b] = who;
+            }
+            L = Lnew;
+        }
+        double *sw = Fprev;
+        Fprev = Fcur;
+        Fcur = sw;
+    }
+    memcpy(F_out, Fprev, sizeof(double) * (size_t)B);
+    info_out[0] = delta;
+    info_out[1] = tmin_sum;
+    *L_out = (int32_t)L;
+done:
+    free(tmin);
+    free(range);
+    free(Mk);
+    free(e);
+    free(arg);
+    free(Fprev);
+    free(Fcur);
+    return rc;
+}
+
+/* Non-dominated bins of the composed array: keep b iff F[b] is strictly below every
+ * F[b'] with b' < b.  The lower time edge of bin b is tmin_sum + b * delta. */
+int oracle_staircase(int B, const double *F, double delta, double tmin_sum,
+                     int32_t *bins_out, double *Tlo_out, double *E_out, int32_t *n_out)
+{
+    double best = INFINITY;
+    int32_t n = 0;
+    for (int b = 0; b < B; b++)
+        if (F[b] < best) {
+            best = F[b];
+            bins_out[n] = b;
+            Tlo_out[n] = tmin_sum + (double)b * delta;
+            E_out[n] = F[b];
+            n++;
+        }
+    *n_out = n;
+    return OR_OK;
+}
+
+/* The per-partition choice behind composite bin `bin`: walk the back-pointers from
+ * the last partition to the first, peeling off each chosen point's offset.  Writes
+ * the point index per partition, and the exact time and energy of that schedule,
+ * summed over partitions in order.  Returns OR_EINVAL if `bin` is unreachable. */
+int oracle_extract(int P, int B, const int64_t *off, const double *T, const double *E,
+                   const int32_t *bp, const int32_t *pt_bin, int32_t bin,
+                   int32_t *choice_out, double *T_out, double *E_out)
+{
+    if (bin < 0 || bin >= B) return OR_EINVAL;
+    int32_t b = bin;
+    for (int k = P - 1; k >= 0; k--) {
+        int32_t j = bp[(size_t)k * B + b];
+        if (j < 0) return OR_EINVAL;
+        choice_out[k] = j;
+        b = b - pt_bin[off[k] + j];
+        if (b < 0) return OR_EINVAL;
+    }
+    if (b != 0) return OR_EINVAL;
+    double Ts = 0.0, Es = 0.0;
+    for (int k = 0; k < P; k++) {
+        Ts = Ts + T[off[k] + choice_out[k]];
+        Es = Es + E[off[k] + choice_out[k]];
+    }
+    *T_out = Ts;
+    *E_out = Es;
+    return OR_OK;
+}
