@@ -1,0 +1,229 @@
+/*
+ * kareus.h -- C ABI of the MI355X (gfx950) schedule-search library
+ * (libkareus_mi355x.so).
+ *
+ * Kareus ("Joint Reduction of Dynamic and Static Energy in Large Model Training")
+ * plans a training iteration by searching, for every partition, over execution
+ * schedules -- the launch position of the communication kernel among the
+ * partition's compute kernels, the number of SMs given to communication, and the
+ * GPU frequency (Section 4.1) -- keeping each partition's time-energy frontier
+ * (Section 4.3, GetFrontier), composing the partition frontiers into the
+ * microbatch/iteration frontier (Section 4.4, Algorithm 2) and selecting the
+ * schedule behind a frontier point (Section 5.1).  This library runs that search
+ * over the whole candidate space with a closed cost model fed by per-kernel time and
+ * power tables, on one GPU.
+ *
+ * Conventions for every entry point
+ *  - Array arguments are DEVICE pointers unless marked "host".  The caller owns and
+ *    allocates every buffer; the library never allocates or frees device memory and
+ *    uses only the workspace the caller passes (size from the matching *_workspace
+ *    query).  Workspace contents need no initialisation and are not preserved.
+ *  - All work is enqueued on `stream` (a hipStream_t; NULL = the null stream) in
+ *    stream order; no entry point synchronises the device.  Results that depend on
+ *    device data (counts, status words) are valid once the stream has reached them.
+ *  - Return codes report argument errors found on the host and launch errors.  A
+ *    condition found on the device (an output capacity exceeded) is reported through
+ *    the device-side count/status outputs documented per call.  On any error the
+ *    outputs are unspecified but no memory outside the documented extents is written.
+ *  - fp64 everywhere; no FMA contraction; every rounding follows the documented
+ *    order, so results are reproducible bit for bit across runs and launch shapes.
+ *  - Inputs must be finite; times strictly positive, powers and comm times >= 0.
+ *    Non-finite inputs give unspecified (memory-safe) results.
+ */
+#ifndef KAREUS_H
+#define KAREUS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t kr_status;
+#define KR_OK 0
+#define KR_EINVAL (-1)       /* null pointer, size out of range, inconsistent shape */
+#define KR_ECAPACITY (-3)    /* workspace or output capacity too small (host-known) */
+#define KR_EHIP (-4)         /* a HIP runtime call or kernel launch failed */
+#define KR_EUNSUPPORTED (-5) /* shape beyond the kernels' on-chip limits */
+
+/*
+ * One batch of P partitions and its candidate axes (Sections 4.1-4.2).
+ *
+ * A partition is one communication kernel stream plus N compute kernels that run in
+ * order with no data dependence on it (Section 4.2).  M = 1 or 2 comm kernels run in
+ * FIFO order on one comm stream (Section 5.2); the two-kernel form covers the
+ * unfused consecutive collectives that Section 4.5 mentions.
+ *
+ * Candidate axes: frequency index f in [0, F); per comm kernel m a launch position
+ * p_m in [0, n_pos) -- the comm kernel is launched together with compute kernel p_m
+ * (Section 3.2.2), p_m = N meaning after the last one -- with p_1 <= p_2 when M = 2;
+ * and per comm kernel an SM choice s_m in [0, S).
+ *
+ * Candidate index within a partition (frequency slowest, SM choice fastest):
+ *   M = 1: idx = (f * n_pos + p) * S + s
+ *   M = 2: pairs (p1 <= p2) ranked lexicographically as pp in [0, n_pos(n_pos+1)/2);
+ *          idx = (f * n_pp + pp) * S * S + s1 * S + s2
+ */
+typedef struct kr_space {
+    int32_t n_parts;   /* P >= 1 */
+    int32_t n_kernels; /* N >= 1 compute kernels per partition */
+    int32_t n_comm;    /* M, 1 or 2 */
+    int32_t n_freq;    /* F >= 1 */
+    int32_t n_sm;      /* S >= 1 comm SM choices */
+    int32_t n_pos;     /* 1 <= n_pos <= N + 1 launch positions */
+    double p_static;   /* static power in W (Sections 2.1, 4.5) */
+} kr_space;
+
+/*
+ * Table layout (row-major fp64, device):
+ *   t [P][F][N][S+1]  compute kernel time (s); SM state 0 = no comm running (all SMs),
+ *                     state s+1 = comm holds SM choice s (Section 3.2.1)
+ *   pw[P][F][N][S+1]  compute kernel dynamic power (W) in that state
+ *   tc[P][F][M][S]    comm kernel time (s) with SM choice s
+ *   pc[P][F][M][S]    comm kernel dynamic power (W) with SM choice s
+ *
+ * Cost model (the paper obtains time and energy by profiling and gives no closed
+ * form, Section 4.3.1; this is the library's fluid reading of Sections 3.2 and 4.2):
+ * compute kernels progress at 1/t in the current SM state and draw pw; comm kernel m
+ * is launched when compute reaches the start of kernel p_m, starts when the comm
+ * stream is free, runs tc regardless of compute and draws pc; a kernel interrupted
+ * by a state change keeps its finished fraction.  Partition time T = the later of
+ * compute end and last comm end; energy E = p_static * T + compute dynamic energy +
+ * comm dynamic energy (Sections 2.1, 2.3, 4.5).
+ */
+
+/*
+ * kr_evaluate_partition -- time and energy of every candidate schedule
+ * (Section 4.1 decision variables; cost model above).
+ *   T_out, E_out  [P][C] with C = F * (n_pos * S) for M = 1, F * (n_pp * S * S) for
+ *                 M = 2, indexed by the candidate index above.
+ * Limits: the per-(partition, frequency) table slab staged on chip,
+ * 8 * (2N(S+1) + 2(N+1)(S+1) + 2MS) bytes plus 4 bytes per launch-position pair when
+ * M = 2, must fit in 64 KiB, else KR_EUNSUPPORTED.  No workspace.
+ */
+kr_status kr_evaluate_partition(const kr_space *space, const double *t, const double *pw,
+                                const double *tc, const double *pc, double *T_out,
+                                double *E_out, void *stream);
+
+/* Candidates per partition of `space` (0 if the space is invalid). */
+int64_t kr_candidates_per_partition(const kr_space *space);
+
+/*
+ * kr_pareto_filter -- GetFrontier per segment (Algorithm 1's return value,
+ * Algorithm 2's last step).
+ *
+ * Segment g holds points [seg_off[g], seg_off[g+1]) of T/E.  A point is kept iff no
+ * point of its segment is no worse in time and energy and better in one; among exact
+ * (T, E) duplicates the smallest index is kept.  The output per segment is a strict
+ * staircase in ascending T (T strictly increasing, E strictly decreasing).
+ *   n_total        host; = seg_off[n_seg]
+ *   T, E           [n_total] device; T > 0 and E >= 0, finite
+ *   seg_off        device [n_seg + 1]: non-decreasing, seg_off[0] = 0,
+ *                  seg_off[n_seg] = n_total (trusted: not checked on the host)
+ *   max_seg_len    host; an upper bound on every segment's length, < 2^31 (it sizes
+ *                  the merge passes; a segment longer than this gives a wrong result)
+ *   cap            host; capacity of out_idx/out_T/out_E
+ *   out_off        device [n_seg + 1]: out_off[g] = start of segment g's frontier;
+ *                  out_off[n_seg] = total frontier points, even if > cap
+ *   out_idx        device [cap] point index relative to its segment start
+ *   out_T, out_E   device [cap]
+ * If the total exceeds cap, only the first cap points are written; check
+ * out_off[n_seg] after the stream completes.
+ */
+kr_status kr_pareto_filter(int64_t n_total, const double *T, const double *E,
+                           const int64_t *seg_off, int32_t n_seg, int64_t max_seg_len,
+                           int64_t cap, int64_t *out_off, int32_t *out_idx, double *out_T,
+                           double *out_E, void *ws, size_t ws_bytes, void *stream);
+size_t kr_pareto_filter_workspace(int64_t n_total, int32_t n_seg, int64_t max_seg_len);
+
+/*
+ * kr_evaluate_and_filter -- kr_evaluate_partition followed by kr_pareto_filter with
+ * one segment per partition, fused: candidate T/E never reach device memory, only
+ * tile-local frontiers do.  Arguments as in the two calls; out_idx holds candidate
+ * indices.  Results are identical to the unfused pair.
+ */
+kr_status kr_evaluate_and_filter(const kr_space *space, const double *t, const double *pw,
+                                 const double *tc, const double *pc, int64_t cap,
+                                 int64_t *out_off, int32_t *out_idx, double *out_T,
+                                 double *out_E, void *ws, size_t ws_bytes, void *stream);
+size_t kr_evaluate_and_filter_workspace(const kr_space *space);
+
+/*
+ * kr_compose_frontiers -- compose partition frontiers into the frontier of their
+ * sequential execution (Section 4.4, Algorithm 2), by min-plus convolution over a
+ * discretised time axis, plus the non-dominated bins of the result.
+ *
+ * Partition k's points are [off[k], off[k+1]) of T/E (any finite set with E >= 0,
+ * not necessarily sorted or strict).  With bin width delta, point j of partition k sits
+ * at offset off_k[j] = floor((T[j] - tmin_k) / delta); e_k[b] = least E at offset b
+ * (ties: smallest point index).  F_1 = e_1 and
+ *   F_k[b] = min over b2 of F_{k-1}[b - b2] + e_k[b2]   (ties: smallest b2),
+ * so F_P[b] is the least energy of any one-point-per-partition choice whose offsets
+ * add up to b, i.e. whose time lies in [tmin_sum + b*delta, tmin_sum + (b+P)*delta).
+ * delta = (sum_k range_k) / (n_bins - 1) (1.0 if that sum is 0), nudged up one ulp at
+ * a time until 1 + sum_k floor(range_k / delta) <= n_bins; or the caller's delta > 0.
+ *
+ *   n_parts      host P >= 1; off device [P+1] (every partition non-empty)
+ *   n_bins       host B >= 2
+ *   F_out        device [B]       F_P (+inf where unreachable)
+ *   bp_out       device [P][B]    point index (relative to its partition) chosen for
+ *                                 partition k at composite bin b of F_k; -1 if none
+ *   pt_bin_out   device [off[P]]  offset of every point
+ *   info_out     device [2]       delta, tmin_sum
+ *   L_out        device [1]       reachable bins 1 + sum_k M_k
+ *   stair_bin, stair_Tlo, stair_E  device [B]: bins b with F_P[b] below every earlier
+ *                                 bin, their lower time edge tmin_sum + b*delta, F_P[b]
+ *   n_stair      device [1]       number of staircase bins
+ *   status_out   device [1]       KR_OK, or KR_ECAPACITY if the caller's delta needs
+ *                                 more than B bins, or KR_EINVAL for an empty partition
+ *                                 (then nothing else is meaningful)
+ */
+kr_status kr_compose_frontiers(int32_t n_parts, const int64_t *off, const double *T,
+                               const double *E, int32_t n_bins, double delta, double *F_out,
+                               int32_t *bp_out, int32_t *pt_bin_out, double *info_out,
+                               int32_t *L_out, int32_t *stair_bin, double *stair_Tlo,
+                               double *stair_E, int32_t *n_stair, int32_t *status_out,
+                               void *ws, size_t ws_bytes, void *stream);
+size_t kr_compose_frontiers_workspace(int32_t n_parts, int32_t n_bins);
+
+/*
+ * kr_extract_schedule -- the per-partition choice behind composed bins (schedule
+ * selection for a target latency, Section 5.1).  For each query bin, walk the
+ * back-pointers from the last partition to the first, peeling off each chosen
+ * point's offset.
+ *   bp, pt_bin, off, T, E   as produced / consumed by kr_compose_frontiers
+ *   bins          device [n_q] query bins
+ *   cand_idx      device [off[P]] or NULL: candidate index of every frontier point
+ *                 (out_idx of kr_evaluate_and_filter); when given, choice_cand_out
+ *                 receives the candidate index of each choice
+ *   choice_out    device [n_q][P] point index per partition
+ *   choice_cand_out device [n_q][P] or NULL
+ *   T_out, E_out  device [n_q] exact sums of the chosen points' T and E, in
+ *                 partition order (E equals F_P[bin] bit for bit)
+ *   ok_out        device [n_q] 1 if the bin was reachable and the walk consistent
+ */
+kr_status kr_extract_schedule(int32_t n_parts, int32_t n_bins, const int32_t *bp,
+                              const int32_t *pt_bin, const int64_t *off, const double *T,
+                              const double *E, const int32_t *bins, int32_t n_q,
+                              const int32_t *cand_idx, int32_t *choice_out,
+                              int32_t *choice_cand_out, double *T_out, double *E_out,
+                              int32_t *ok_out, void *stream);
+
+/*
+ * kr_decode_candidates -- candidate index -> (frequency index, launch positions, SM
+ * choices) under the index order above.
+ *   idx [n] device; f_out [n]; pos_out [n][M]; sm_out [n][M] (device)
+ */
+kr_status kr_decode_candidates(const kr_space *space, const int32_t *idx, int64_t n,
+                               int32_t *f_out, int32_t *pos_out, int32_t *sm_out,
+                               void *stream);
+
+/* Human-readable name of a status code. */
+const char *kr_status_string(kr_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KAREUS_H */

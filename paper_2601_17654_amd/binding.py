@@ -1,0 +1,300 @@
+"""Python binding of libkareus_mi355x.so (the C ABI in include/kareus.h).
+
+Argument marshalling only: every step runs in the library's HIP kernels.  PyTorch
+provides device memory and the current HIP stream.  The functions carry the C names
+without the `kr_` prefix.  Importing this module loads the library and fails loudly
+if it has not been built.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Optional
+
+import numpy as np
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkareus_mi355x.so")
+if not os.path.exists(_LIB_PATH):
+    raise ImportError("libkareus_mi355x.so is not built (run __graft_entry__.build() or "
+                      "python paper_2601_17654_amd/build.py)")
+_lib = ctypes.CDLL(_LIB_PATH)
+
+KR_OK, KR_EINVAL, KR_ECAPACITY, KR_EHIP, KR_EUNSUPPORTED = 0, -1, -3, -4, -5
+
+
+class KrSpace(ctypes.Structure):
+    _fields_ = [("n_parts", ctypes.c_int32), ("n_kernels", ctypes.c_int32),
+                ("n_comm", ctypes.c_int32), ("n_freq", ctypes.c_int32),
+                ("n_sm", ctypes.c_int32), ("n_pos", ctypes.c_int32),
+                ("p_static", ctypes.c_double)]
+
+
+_vp, _i32, _i64, _f64, _sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                              ctypes.c_double, ctypes.c_size_t)
+_SP = ctypes.POINTER(KrSpace)
+_SIGS = {
+    "kr_evaluate_partition": (_i32, [_SP, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "kr_candidates_per_partition": (_i64, [_SP]),
+    "kr_pareto_filter": (_i32, [_i64, _vp, _vp, _vp, _i32, _i64, _i64, _vp, _vp, _vp, _vp, _vp,
+                                _sz, _vp]),
+    "kr_pareto_filter_workspace": (_sz, [_i64, _i32, _i64]),
+    "kr_evaluate_and_filter": (_i32, [_SP, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _sz,
+                                      _vp]),
+    "kr_evaluate_and_filter_workspace": (_sz, [_SP]),
+    "kr_compose_frontiers": (_i32, [_i32, _vp, _vp, _vp, _i32, _f64, _vp, _vp, _vp, _vp, _vp, _vp,
+                                    _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "kr_compose_frontiers_workspace": (_sz, [_i32, _i32]),
+    "kr_extract_schedule": (_i32, [_i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
+                                   _vp, _vp, _vp, _vp]),
+    "kr_decode_candidates": (_i32, [_SP, _vp, _i64, _vp, _vp, _vp, _vp]),
+    "kr_status_string": (ctypes.c_char_p, [_i32]),
+}
+for _name, (_res, _args) in _SIGS.items():
+    _fn = getattr(_lib, _name)
+    _fn.restype = _res
+    _fn.argtypes = _args
+
+
+class KrError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__("%s: %s (%d)" % (fn, status_string(status), status))
+        self.status = status
+
+
+def status_string(status: int) -> str:
+    return _lib.kr_status_string(int(status)).decode()
+
+
+def _check(fn: str, status: int) -> None:
+    if status != KR_OK:
+        raise KrError(fn, status)
+
+
+def _space(space) -> KrSpace:
+    return KrSpace(space.n_parts, space.n_kernels, space.n_comm, space.n_freq, space.n_sm,
+                   space.n_pos, float(space.p_static))
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(x, dtype, name: str) -> torch.Tensor:
+    if not isinstance(x, torch.Tensor):
+        x = torch.as_tensor(np.ascontiguousarray(x))
+    if x.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, x.dtype))
+    if not x.is_cuda:
+        x = x.cuda()
+    return x.contiguous()
+
+
+_ws_cache = {}
+
+
+def _workspace(nbytes: int) -> torch.Tensor:
+    dev = torch.cuda.current_device()
+    buf = _ws_cache.get(dev)
+    if buf is None or buf.numel() < nbytes:
+        buf = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device="cuda")
+        _ws_cache[dev] = buf
+    return buf
+
+
+def candidates_per_partition(space) -> int:
+    return int(_lib.kr_candidates_per_partition(ctypes.byref(_space(space))))
+
+
+def evaluate_partition(space, t, pw, tc, pc, T_out=None, E_out=None):
+    """Time and energy of every candidate: (T, E), float64 [P][C] on the device."""
+    sp = _space(space)
+    C = candidates_per_partition(space)
+    t, pw = _dev(t, torch.float64, "t"), _dev(pw, torch.float64, "pw")
+    tc, pc = _dev(tc, torch.float64, "tc"), _dev(pc, torch.float64, "pc")
+    _check_tables(space, t, pw, tc, pc)
+    if T_out is None:
+        T_out = torch.empty((space.n_parts, C), dtype=torch.float64, device="cuda")
+    if E_out is None:
+        E_out = torch.empty((space.n_parts, C), dtype=torch.float64, device="cuda")
+    _check("kr_evaluate_partition",
+           _lib.kr_evaluate_partition(ctypes.byref(sp), _ptr(t), _ptr(pw), _ptr(tc), _ptr(pc),
+                                      _ptr(T_out), _ptr(E_out), _stream()))
+    return T_out, E_out
+
+
+def _check_tables(space, t, pw, tc, pc):
+    P, F, N, S, M = space.n_parts, space.n_freq, space.n_kernels, space.n_sm, space.n_comm
+    if tuple(t.shape) != (P, F, N, S + 1) or tuple(pw.shape) != (P, F, N, S + 1):
+        raise ValueError("t/pw must be [P][F][N][S+1] = %s" % ((P, F, N, S + 1),))
+    if tuple(tc.shape) != (P, F, M, S) or tuple(pc.shape) != (P, F, M, S):
+        raise ValueError("tc/pc must be [P][F][M][S] = %s" % ((P, F, M, S),))
+
+
+@dataclasses.dataclass
+class Frontier:
+    """Per-segment frontiers in CSR form (device tensors)."""
+    off: torch.Tensor   # int64 [n_seg + 1]
+    idx: torch.Tensor   # int32 [total]
+    T: torch.Tensor     # float64 [total]
+    E: torch.Tensor     # float64 [total]
+
+
+def _finish_frontier(off, idx, T, E, cap, sync):
+    if not sync:
+        return Frontier(off, idx, T, E), True
+    torch.cuda.current_stream().synchronize()
+    total = int(off[-1].item())
+    if total > cap:
+        return None, total
+    return Frontier(off, idx[:total], T[:total], E[:total]), True
+
+
+def pareto_filter(T, E, seg_off, max_seg_len: Optional[int] = None, cap: Optional[int] = None,
+                  sync: bool = True) -> Frontier:
+    """GetFrontier of every segment [seg_off[g], seg_off[g+1]) of (T, E)."""
+    seg_host = np.asarray(seg_off.cpu() if isinstance(seg_off, torch.Tensor) else seg_off,
+                          dtype=np.int64)
+    n_seg = len(seg_host) - 1
+    if n_seg < 0 or seg_host[0] != 0 or np.any(np.diff(seg_host) < 0):
+        raise ValueError("seg_off must start at 0 and be non-decreasing")
+    T = _dev(T, torch.float64, "T").reshape(-1)
+    E = _dev(E, torch.float64, "E").reshape(-1)
+    n_total = int(seg_host[-1])
+    if T.numel() != n_total or E.numel() != n_total:
+        raise ValueError("T/E must hold seg_off[-1] points")
+    if max_seg_len is None:
+        max_seg_len = int(np.diff(seg_host).max()) if n_seg > 0 else 0
+    seg_dev = torch.from_numpy(seg_host).cuda()
+    while True:
+        c = int(cap) if cap is not None else min(n_total, max(4096 * max(n_seg, 1), 1))
+        off = torch.empty(n_seg + 1, dtype=torch.int64, device="cuda")
+        idx = torch.empty(max(c, 1), dtype=torch.int32, device="cuda")
+        oT = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
+        oE = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
+        wsb = _lib.kr_pareto_filter_workspace(n_total, n_seg, max_seg_len)
+        ws = _workspace(wsb)
+        _check("kr_pareto_filter",
+               _lib.kr_pareto_filter(n_total, _ptr(T), _ptr(E), _ptr(seg_dev), n_seg, max_seg_len,
+                                     c, _ptr(off), _ptr(idx), _ptr(oT), _ptr(oE), _ptr(ws), wsb,
+                                     _stream()))
+        fr, ok = _finish_frontier(off, idx, oT, oE, c, sync)
+        if fr is not None:
+            return fr
+        cap = ok  # the exact size
+
+
+def evaluate_and_filter(space, t, pw, tc, pc, cap: Optional[int] = None,
+                        sync: bool = True) -> Frontier:
+    """Fused evaluation + GetFrontier, one segment per partition; idx = candidate index."""
+    sp = _space(space)
+    t, pw = _dev(t, torch.float64, "t"), _dev(pw, torch.float64, "pw")
+    tc, pc = _dev(tc, torch.float64, "tc"), _dev(pc, torch.float64, "pc")
+    _check_tables(space, t, pw, tc, pc)
+    C = candidates_per_partition(space)
+    wsb = _lib.kr_evaluate_and_filter_workspace(ctypes.byref(sp))
+    if wsb == 0:
+        raise KrError("kr_evaluate_and_filter_workspace", KR_EUNSUPPORTED)
+    while True:
+        c = int(cap) if cap is not None else min(space.n_parts * C, 4096 * space.n_parts)
+        off = torch.empty(space.n_parts + 1, dtype=torch.int64, device="cuda")
+        idx = torch.empty(max(c, 1), dtype=torch.int32, device="cuda")
+        oT = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
+        oE = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
+        ws = _workspace(wsb)
+        _check("kr_evaluate_and_filter",
+               _lib.kr_evaluate_and_filter(ctypes.byref(sp), _ptr(t), _ptr(pw), _ptr(tc), _ptr(pc),
+                                           c, _ptr(off), _ptr(idx), _ptr(oT), _ptr(oE), _ptr(ws),
+                                           wsb, _stream()))
+        fr, ok = _finish_frontier(off, idx, oT, oE, c, sync)
+        if fr is not None:
+            return fr
+        cap = ok
+
+
+@dataclasses.dataclass
+class Composed:
+    F: torch.Tensor          # float64 [B]
+    bp: torch.Tensor         # int32 [P][B]
+    pt_bin: torch.Tensor     # int32 [n_points]
+    info: torch.Tensor       # float64 [2]: delta, tmin_sum
+    L: torch.Tensor          # int32 [1]
+    stair_bin: torch.Tensor  # int32 [B]
+    stair_Tlo: torch.Tensor  # float64 [B]
+    stair_E: torch.Tensor    # float64 [B]
+    n_stair: torch.Tensor    # int32 [1]
+    status: torch.Tensor     # int32 [1]
+
+    def staircase(self):
+        n = int(self.n_stair.item())
+        return self.stair_bin[:n], self.stair_Tlo[:n], self.stair_E[:n]
+
+
+def compose_frontiers(off, T, E, n_bins: int, delta: float = 0.0, out: Optional[Composed] = None
+                      ) -> Composed:
+    """Min-plus composition of partition frontiers [off[k], off[k+1]) of (T, E)."""
+    off = _dev(off, torch.int64, "off")
+    T = _dev(T, torch.float64, "T").reshape(-1)
+    E = _dev(E, torch.float64, "E").reshape(-1)
+    P = off.numel() - 1
+    B = int(n_bins)
+    if out is None:
+        f64 = dict(dtype=torch.float64, device="cuda")
+        i32 = dict(dtype=torch.int32, device="cuda")
+        out = Composed(torch.empty(B, **f64), torch.empty((P, B), **i32),
+                       torch.empty(max(T.numel(), 1), **i32), torch.empty(2, **f64),
+                       torch.empty(1, **i32), torch.empty(B, **i32), torch.empty(B, **f64),
+                       torch.empty(B, **f64), torch.empty(1, **i32), torch.empty(1, **i32))
+    wsb = _lib.kr_compose_frontiers_workspace(P, B)
+    ws = _workspace(wsb)
+    _check("kr_compose_frontiers",
+           _lib.kr_compose_frontiers(P, _ptr(off), _ptr(T), _ptr(E), B, float(delta), _ptr(out.F),
+                                     _ptr(out.bp), _ptr(out.pt_bin), _ptr(out.info), _ptr(out.L),
+                                     _ptr(out.stair_bin), _ptr(out.stair_Tlo), _ptr(out.stair_E),
+                                     _ptr(out.n_stair), _ptr(out.status), _ptr(ws), wsb,
+                                     _stream()))
+    return out
+
+
+def extract_schedule(comp: Composed, off, T, E, bins, cand_idx=None):
+    """Per-partition choice behind each query bin.
+    Returns (choice [n_q][P], choice_cand [n_q][P] or None, T [n_q], E [n_q], ok [n_q])."""
+    off = _dev(off, torch.int64, "off")
+    T = _dev(T, torch.float64, "T").reshape(-1)
+    E = _dev(E, torch.float64, "E").reshape(-1)
+    bins = _dev(bins, torch.int32, "bins").reshape(-1)
+    P, B = comp.bp.shape
+    nq = bins.numel()
+    choice = torch.empty((nq, P), dtype=torch.int32, device="cuda")
+    cc = None
+    if cand_idx is not None:
+        cand_idx = _dev(cand_idx, torch.int32, "cand_idx")
+        cc = torch.empty((nq, P), dtype=torch.int32, device="cuda")
+    Ts = torch.empty(nq, dtype=torch.float64, device="cuda")
+    Es = torch.empty(nq, dtype=torch.float64, device="cuda")
+    ok = torch.empty(nq, dtype=torch.int32, device="cuda")
+    _check("kr_extract_schedule",
+           _lib.kr_extract_schedule(P, B, _ptr(comp.bp), _ptr(comp.pt_bin), _ptr(off), _ptr(T),
+                                    _ptr(E), _ptr(bins), nq, _ptr(cand_idx), _ptr(choice), _ptr(cc),
+                                    _ptr(Ts), _ptr(Es), _ptr(ok), _stream()))
+    return choice, cc, Ts, Es, ok
+
+
+def decode_candidates(space, idx):
+    """Candidate index -> (f [n], pos [n][M], sm [n][M]) on the device."""
+    sp = _space(space)
+    idx = _dev(idx, torch.int32, "idx").reshape(-1)
+    n = idx.numel()
+    f = torch.empty(n, dtype=torch.int32, device="cuda")
+    pos = torch.empty((n, space.n_comm), dtype=torch.int32, device="cuda")
+    sm = torch.empty((n, space.n_comm), dtype=torch.int32, device="cuda")
+    _check("kr_decode_candidates",
+           _lib.kr_decode_candidates(ctypes.byref(sp), _ptr(idx), n, _ptr(f), _ptr(pos), _ptr(sm),
+                                     _stream()))
+    return f, pos, sm

@@ -1,0 +1,87 @@
+"""The C ABI library loads and exports every symbol that include/kareus.h declares;
+host-side argument validation answers without touching a GPU."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kareus.h")
+LIB = os.path.join(ROOT, "paper_2601_17654_amd", "libkareus_mi355x.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kr_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        from paper_2601_17654_amd import build
+
+        build.build()
+    return ctypes.CDLL(LIB)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    lib.kr_status_string.restype = ctypes.c_char_p
+    assert lib.kr_status_string(0) == b"ok"
+    assert b"capacity" in lib.kr_status_string(-3)
+    assert b"unknown" in lib.kr_status_string(42)
+
+
+def test_host_validation_without_gpu():
+    from paper_2601_17654_amd import binding as b
+    from paper_2601_17654_amd import inputs as I
+
+    L = b._lib
+    sp = b._space(I.SPACES[0]["space"])
+    null = ctypes.c_void_p(0)
+    assert L.kr_evaluate_partition(ctypes.byref(sp), null, null, null, null, null, null,
+                                   null) == b.KR_EINVAL
+    bad = b.KrSpace(1, 4, 3, 1, 1, 5, 90.0)  # three comm kernels
+    assert L.kr_candidates_per_partition(ctypes.byref(bad)) == 0
+    bad = b.KrSpace(1, 4, 1, 1, 1, 6, 90.0)  # n_pos > N + 1
+    assert L.kr_candidates_per_partition(ctypes.byref(bad)) == 0
+    # a slab that cannot fit on chip is refused before any launch
+    huge = b.KrSpace(1, 400, 1, 1, 40, 401, 90.0)
+    one = ctypes.c_void_p(8)
+    assert L.kr_evaluate_partition(ctypes.byref(huge), one, one, one, one, one, one,
+                                   null) == b.KR_EUNSUPPORTED
+    assert L.kr_evaluate_and_filter_workspace(ctypes.byref(huge)) == 0
+    # workspace sizes grow with the problem
+    assert L.kr_pareto_filter_workspace(10, 1, 10) < L.kr_pareto_filter_workspace(10 ** 6, 8, 10 ** 6)
+    assert L.kr_compose_frontiers_workspace(4, 1024) < L.kr_compose_frontiers_workspace(512, 65536)
+    assert L.kr_compose_frontiers_workspace(0, 1024) == 0
+    # too small a workspace is refused on the host
+    assert L.kr_compose_frontiers(4, one, one, one, 1024, 0.0, one, one, one, one, one, one, one,
+                                  one, one, one, one, 16, null) == b.KR_ECAPACITY
+    assert L.kr_compose_frontiers(4, one, one, one, 1024, -1.0, one, one, one, one, one, one, one,
+                                  one, one, one, one, 1 << 30, null) == b.KR_EINVAL
+    assert b.candidates_per_partition(I.SPACES[2]["space"]) == 1148928
+
+
+def test_oracle_and_library_share_nothing():
+    """The oracle neither includes the library's header nor loads it, and the library's
+    sources never mention the oracle."""
+    src = open(os.path.join(ROOT, "oracle", "kareus_oracle.c")).read()
+    assert "kareus.h" not in src and "libkareus" not in src
+    py = open(os.path.join(ROOT, "oracle", "__init__.py")).read()
+    assert "paper_2601_17654_amd" not in py and "libkareus" not in py
+    csrc = os.path.join(ROOT, "paper_2601_17654_amd", "csrc")
+    for f in os.listdir(csrc):
+        assert "oracle" not in open(os.path.join(csrc, f)).read().lower(), f
+    for f in ("binding.py", "build.py", "__init__.py", "inputs.py"):
+        text = open(os.path.join(ROOT, "paper_2601_17654_amd", f)).read()
+        assert not re.search(r"^\s*(import|from)\s+oracle", text, flags=re.M), f

@@ -1,0 +1,348 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle, element by
+element, on the same seeded inputs.
+
+Bars: frontier index sets, chosen candidates, offsets and back-pointers bit-exact;
+T and E within 1e-9 relative (fp64); composed energies within 1e-6 relative.  With
+identical fp64 operation orders on both sides the values are expected to agree bit
+for bit, and the tests also report how many do not.
+"""
+
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2601_17654_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+RT_TE = 1e-9
+RT_MINPLUS = 1e-6
+
+
+@pytest.fixture(scope="module")
+def kr():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    from paper_2601_17654_amd import binding
+
+    return binding
+
+
+_cache = {}
+
+
+def workload(cfg, parts=None):
+    key = (cfg, None if parts is None else (parts.start, parts.stop))
+    if key not in _cache:
+        _cache[key] = I.config_workload(cfg, parts=parts)
+    return _cache[key]
+
+
+def dev_tables(w):
+    return [torch.from_numpy(getattr(w, k)).cuda() for k in ("t", "pw", "tc", "pc")]
+
+
+def assert_close(got, ref, rtol, what):
+    got = np.asarray(got)
+    ref = np.asarray(ref)
+    assert got.shape == ref.shape, what
+    np.testing.assert_allclose(got, ref, rtol=rtol, atol=0, err_msg=what)
+    diff = int(np.count_nonzero(got != ref))
+    if diff:
+        print("%s: %d of %d values not bit-identical (within rtol %g)" % (what, diff, got.size, rtol))
+
+
+def check_frontier(fr, part, ref, what):
+    """fr: binding.Frontier on host numpy; ref = (idx, T, E) of the oracle."""
+    off = fr.off.cpu().numpy()
+    lo, hi = int(off[part]), int(off[part + 1])
+    idx = fr.idx.cpu().numpy()[lo:hi]
+    np.testing.assert_array_equal(idx, ref[0], err_msg=what + " idx")
+    assert_close(fr.T.cpu().numpy()[lo:hi], ref[1], RT_TE, what + " T")
+    assert_close(fr.E.cpu().numpy()[lo:hi], ref[2], RT_TE, what + " E")
+
+
+def small_spaces():
+    rng = np.random.default_rng(77)
+    spaces = []
+    for i in range(10):
+        spaces.append(I.random_space(rng, n_comm=1 + (i % 2), max_kernels=8, max_sm=5,
+                                     max_freq=3, n_parts=3))
+    # edge shapes: one kernel, one position, one SM choice, one frequency; n_pos = N + 1
+    spaces.append(I.Space(2, 1, 1, 1, (8,), (1500.0,)))
+    spaces.append(I.Space(2, 1, 2, 2, (8, 16), (1500.0,)))
+    spaces.append(I.Space(2, 9, 1, 10, (1, 2, 3), (1005.0, 1980.0)))
+    spaces.append(I.Space(2, 9, 2, 10, (1, 32), (1005.0, 1980.0)))
+    return spaces
+
+
+@pytest.mark.parametrize("case", range(14))
+@pytest.mark.parametrize("tc_scale", [1.0, 1e-3, 1e3])
+def test_evaluate_small_spaces(kr, oracle_lib, case, tc_scale):
+    space = small_spaces()[case]
+    tab = I.make_tables(space, seed=case, comm_bytes=(4e6, 64e6))
+    tab["tc"] = tab["tc"] * tc_scale
+    d = [torch.from_numpy(tab[k]).cuda() for k in ("t", "pw", "tc", "pc")]
+    T, E = kr.evaluate_partition(space, *d)
+    fr = kr.evaluate_and_filter(space, *d)
+    T, E = T.cpu().numpy(), E.cpu().numpy()
+    for p in range(space.n_parts):
+        Tr, Er = oracle_lib.evaluate_partition(space, tab["t"], tab["pw"], tab["tc"], tab["pc"], p)
+        assert_close(T[p], Tr, RT_TE, "T case %d part %d" % (case, p))
+        assert_close(E[p], Er, RT_TE, "E case %d part %d" % (case, p))
+        ix = oracle_lib.pareto(Tr, Er)
+        check_frontier(fr, p, (ix, Tr[ix], Er[ix]), "frontier case %d part %d" % (case, p))
+
+
+@pytest.mark.parametrize("cfg", [0, 1])
+def test_evaluate_and_filter_full(kr, oracle_lib, cfg):
+    w = workload(cfg)
+    d = dev_tables(w)
+    T, E = kr.evaluate_partition(w.space, *d)
+    fr = kr.evaluate_and_filter(w.space, *d)
+    T, E = T.cpu().numpy(), E.cpu().numpy()
+    ref = oracle_lib.evaluate_and_filter(w.space, w.t, w.pw, w.tc, w.pc)
+    for p in range(w.space.n_parts):
+        Tr, Er = oracle_lib.evaluate_partition(w.space, w.t, w.pw, w.tc, w.pc, p)
+        assert_close(T[p], Tr, RT_TE, "cfg%d T part %d" % (cfg, p))
+        assert_close(E[p], Er, RT_TE, "cfg%d E part %d" % (cfg, p))
+        check_frontier(fr, p, ref[p], "cfg%d part %d" % (cfg, p))
+
+
+@pytest.mark.parametrize("cfg,parts", [(2, range(0, 2)), (2, range(255, 256)),
+                                       (3, range(0, 8)), (3, range(1020, 1024))])
+def test_evaluate_sampled_partitions(kr, oracle_lib, cfg, parts):
+    """Unfused evaluation on a sub-batch (the tables are those of the full batch)."""
+    w = workload(cfg, parts)
+    T, E = kr.evaluate_partition(w.space, *dev_tables(w))
+    T, E = T.cpu().numpy(), E.cpu().numpy()
+    for p in range(len(parts)):
+        Tr, Er = oracle_lib.evaluate_partition(w.space, w.t, w.pw, w.tc, w.pc, p)
+        assert_close(T[p], Tr, RT_TE, "cfg%d T part %d" % (cfg, parts.start + p))
+        assert_close(E[p], Er, RT_TE, "cfg%d E part %d" % (cfg, parts.start + p))
+
+
+@pytest.mark.parametrize("cfg,sample", [(3, [0, 1, 333, 512, 1023]), (2, [0, 131, 255])])
+def test_evaluate_and_filter_full_size_sampled(kr, oracle_lib, cfg, sample):
+    """The fused kernel at the full batch size (the benchmark's launch), checked on
+    sampled partitions; every partition's output is a strict staircase."""
+    w = workload(cfg)
+    fr = kr.evaluate_and_filter(w.space, *dev_tables(w))
+    for p in sample:
+        Tr, Er = oracle_lib.evaluate_partition(w.space, w.t, w.pw, w.tc, w.pc, p)
+        ix = oracle_lib.pareto(Tr, Er)
+        check_frontier(fr, p, (ix, Tr[ix], Er[ix]), "cfg%d part %d" % (cfg, p))
+    off = fr.off.cpu().numpy()
+    T, E, idx = fr.T.cpu().numpy(), fr.E.cpu().numpy(), fr.idx.cpu().numpy()
+    C = w.space.n_cand
+    for p in range(w.space.n_parts):
+        lo, hi = off[p], off[p + 1]
+        assert hi > lo
+        assert np.all(np.diff(T[lo:hi]) > 0) and np.all(np.diff(E[lo:hi]) < 0)
+        assert idx[lo:hi].min() >= 0 and idx[lo:hi].max() < C
+
+
+def test_fused_equals_unfused(kr):
+    w = workload(1)
+    d = dev_tables(w)
+    T, E = kr.evaluate_partition(w.space, *d)
+    C = w.space.n_cand
+    seg = np.arange(w.space.n_parts + 1, dtype=np.int64) * C
+    a = kr.pareto_filter(T, E, seg)
+    b = kr.evaluate_and_filter(w.space, *d)
+    for x, y in ((a.off, b.off), (a.idx, b.idx), (a.T, b.T), (a.E, b.E)):
+        assert torch.equal(x, y)
+
+
+def _tied(rng, n):
+    T = rng.integers(1, 40, size=n).astype(np.float64) * 0.125
+    E = rng.integers(1, 40, size=n).astype(np.float64) * 0.25
+    dup = rng.integers(0, max(n, 1), size=n // 8)
+    if len(dup):
+        T[dup] = T[dup[0]]
+        E[dup] = E[dup[0]]
+    return T, E
+
+
+@pytest.mark.parametrize("kind", ["tied", "continuous", "staircase", "mixed-lengths"])
+def test_pareto_filter(kr, oracle_lib, kind):
+    rng = np.random.default_rng({"tied": 1, "continuous": 2, "staircase": 3}.get(kind, 4))
+    if kind == "tied":
+        lens = [0, 1, 2, 7, 2047, 2048, 2049, 5000, 0, 12345]
+    elif kind == "continuous":
+        lens = [100000, 3, 65536, 1]
+    elif kind == "staircase":
+        lens = [9000, 4096, 1]  # every point survives: large runs through every merge level
+    else:
+        lens = list(rng.integers(0, 9000, size=40))
+    Ts, Es = [], []
+    for n in lens:
+        if kind == "tied":
+            T, E = _tied(rng, n)
+        elif kind == "staircase":
+            T = np.sort(rng.uniform(1.0, 2.0, size=n))
+            T = np.unique(T)
+            T = np.concatenate([T, 3.0 + np.arange(n - len(T))])
+            E = 10.0 - np.arange(n) * 1e-3
+            perm = rng.permutation(n)
+            T, E = T[perm], E[perm]
+        else:
+            T = rng.lognormal(size=n)
+            E = 1.0 / T + rng.random(n)
+        Ts.append(T)
+        Es.append(E)
+    seg = np.zeros(len(lens) + 1, dtype=np.int64)
+    seg[1:] = np.cumsum(lens)
+    T = np.concatenate(Ts) if Ts else np.zeros(0)
+    E = np.concatenate(Es) if Es else np.zeros(0)
+    fr = kr.pareto_filter(torch.from_numpy(T).cuda(), torch.from_numpy(E).cuda(), seg)
+    for g in range(len(lens)):
+        Tg, Eg = T[seg[g]:seg[g + 1]], E[seg[g]:seg[g + 1]]
+        ix = oracle_lib.pareto(Tg, Eg)
+        check_frontier(fr, g, (ix, Tg[ix], Eg[ix]), "%s seg %d (n=%d)" % (kind, g, lens[g]))
+
+
+def test_pareto_filter_capacity(kr):
+    T = torch.linspace(1.0, 2.0, 5000, dtype=torch.float64).cuda()
+    E = torch.linspace(2.0, 1.0, 5000, dtype=torch.float64).cuda()
+    seg = np.array([0, 5000], dtype=np.int64)
+    fr = kr.pareto_filter(T, E, seg, cap=100, sync=False)
+    torch.cuda.synchronize()
+    assert int(fr.off[-1]) == 5000  # the required size is reported
+    assert torch.equal(fr.idx[:100].cpu(), torch.arange(100, dtype=torch.int32))
+    fr = kr.pareto_filter(T, E, seg)  # grows its capacity and retries
+    assert fr.idx.numel() == 5000
+
+
+def compare_composed(kr, comp, ref, off, T, E, what):
+    assert int(comp.status.item()) == 0
+    info = comp.info.cpu().numpy()
+    assert info[0] == ref.delta and info[1] == ref.tmin_sum, what
+    assert int(comp.L.item()) == ref.L
+    assert_close(comp.F.cpu().numpy(), ref.F, RT_MINPLUS, what + " F")
+    np.testing.assert_array_equal(comp.pt_bin.cpu().numpy()[:len(ref.pt_bin)], ref.pt_bin)
+    np.testing.assert_array_equal(comp.bp.cpu().numpy(), ref.bp, err_msg=what + " bp")
+
+
+@pytest.fixture(scope="module")
+def config4():
+    return I.compose_frontiers()
+
+
+def test_compose_config4(kr, oracle_lib, config4):
+    off, T, E = config4
+    B = I.COMPOSE_SPACE["bins"]
+    comp = kr.compose_frontiers(torch.from_numpy(off).cuda(), torch.from_numpy(T).cuda(),
+                                torch.from_numpy(E).cuda(), B)
+    ref = oracle_lib.compose(off, T, E, B)
+    compare_composed(kr, comp, ref, off, T, E, "cfg4")
+    sb, st, se = comp.staircase()
+    rb, rt, re_ = oracle_lib.staircase(ref.F, ref.delta, ref.tmin_sum)
+    np.testing.assert_array_equal(sb.cpu().numpy(), rb)
+    assert_close(st.cpu().numpy(), rt, RT_TE, "cfg4 stair T")
+    assert_close(se.cpu().numpy(), re_, RT_MINPLUS, "cfg4 stair E")
+    # schedules behind every staircase bin and some other reachable bins
+    reach = np.flatnonzero(np.isfinite(ref.F))
+    rng = np.random.default_rng(4)
+    bins = np.concatenate([rb, rng.choice(reach, size=24, replace=False), [ref.L, B - 1]])
+    ch, _, Ts, Es, ok = kr.extract_schedule(comp, off, T, E, torch.from_numpy(
+        bins.astype(np.int32)).cuda())
+    ch, Ts, Es, ok = ch.cpu().numpy(), Ts.cpu().numpy(), Es.cpu().numpy(), ok.cpu().numpy()
+    for q, b in enumerate(bins):
+        if b >= ref.L or not np.isfinite(ref.F[b]):
+            assert ok[q] == 0
+            continue
+        rc, rts, res = oracle_lib.extract(off, T, E, ref, int(b))
+        assert ok[q] == 1
+        np.testing.assert_array_equal(ch[q], rc)
+        assert_close(Ts[q], rts, RT_TE, "extract T bin %d" % b)
+        assert_close(Es[q], res, RT_TE, "extract E bin %d" % b)
+
+
+@pytest.mark.parametrize("cfg", [0, 1])
+def test_end_to_end_path(kr, oracle_lib, cfg):
+    """Tables -> fused frontiers -> composition -> staircase -> extracted schedules,
+    against the oracle run on the same tables."""
+    w = workload(cfg)
+    fr = kr.evaluate_and_filter(w.space, *dev_tables(w))
+    ref_fr = oracle_lib.evaluate_and_filter(w.space, w.t, w.pw, w.tc, w.pc)
+    roff = np.zeros(w.space.n_parts + 1, dtype=np.int64)
+    roff[1:] = np.cumsum([len(x[0]) for x in ref_fr])
+    rT = np.concatenate([x[1] for x in ref_fr])
+    rE = np.concatenate([x[2] for x in ref_fr])
+    ridx = np.concatenate([x[0] for x in ref_fr])
+    comp = kr.compose_frontiers(fr.off, fr.T, fr.E, w.bins)
+    ref = oracle_lib.compose(roff, rT, rE, w.bins)
+    compare_composed(kr, comp, ref, roff, rT, rE, "cfg%d" % cfg)
+    sb, _, _ = comp.staircase()
+    ch, cc, Ts, Es, ok = kr.extract_schedule(comp, fr.off, fr.T, fr.E, sb, cand_idx=fr.idx)
+    assert ok.cpu().numpy().all()
+    f, pos, sm = kr.decode_candidates(w.space, cc.reshape(-1))
+    f, pos, sm = f.cpu().numpy(), pos.cpu().numpy(), sm.cpu().numpy()
+    cc = cc.cpu().numpy()
+    for q, b in enumerate(sb.cpu().numpy()):
+        rc, rts, res = oracle_lib.extract(roff, rT, rE, ref, int(b))
+        np.testing.assert_array_equal(ch[q].cpu().numpy(), rc)
+        assert Es[q].item() == pytest.approx(res, rel=RT_TE)
+        for k in range(w.space.n_parts):
+            cand = ridx[roff[k] + rc[k]]
+            assert cc[q, k] == cand
+            rf, rpos, rsm = oracle_lib.decode(w.space, int(cand))
+            x = q * w.space.n_parts + k
+            assert (f[x], tuple(pos[x]), tuple(sm[x])) == (rf, rpos, rsm)
+
+
+def test_compose_edge_cases(kr, oracle_lib):
+    cases = []
+    rng = np.random.default_rng(11)
+    # one partition
+    cases.append((np.array([0, 50]), rng.uniform(1e-3, 2e-3, 50), rng.uniform(1, 2, 50), 16, 0.0))
+    # single-point partitions: zero range
+    cases.append((np.array([0, 1, 2, 3]), np.array([1e-3, 2e-3, 3e-3]), np.array([1., 2., 3.]),
+                  4, 0.0))
+    # exact ties everywhere
+    n = [5, 7, 3, 9]
+    off = np.concatenate([[0], np.cumsum(n)])
+    cases.append((off, rng.integers(0, 6, off[-1]) * 1e-3 + 1e-3,
+                  rng.integers(1, 4, off[-1]) * 0.25, 40, 0.0))
+    # a caller-given width
+    cases.append((off, rng.uniform(1e-3, 4e-3, off[-1]), rng.uniform(1, 2, off[-1]), 64, 2.5e-4))
+    for i, (off, T, E, B, delta) in enumerate(cases):
+        off = off.astype(np.int64)
+        comp = kr.compose_frontiers(torch.from_numpy(off).cuda(), torch.from_numpy(T).cuda(),
+                                    torch.from_numpy(E).cuda(), B, delta=delta)
+        ref = oracle_lib.compose(off, T, E, B, delta=delta)
+        compare_composed(kr, comp, ref, off, T, E, "edge %d" % i)
+    # a caller-given width that needs too many bins: reported on the device
+    off = np.array([0, 3], dtype=np.int64)
+    comp = kr.compose_frontiers(torch.from_numpy(off).cuda(),
+                                torch.tensor([0.001, 1.0, 2.0], dtype=torch.float64).cuda(),
+                                torch.tensor([3.0, 2.0, 1.0], dtype=torch.float64).cuda(), 2,
+                                delta=0.5)
+    assert int(comp.status.item()) == kr.KR_ECAPACITY
+    assert int(comp.n_stair.item()) == 0
+
+
+def test_decode(kr, oracle_lib):
+    for sp in (I.SPACES[0]["space"], I.SPACES[2]["space"], I.SPACES[3]["space"]):
+        rng = np.random.default_rng(sp.n_kernels)
+        idx = rng.integers(0, sp.n_cand, size=500).astype(np.int32)
+        f, pos, sm = kr.decode_candidates(sp, torch.from_numpy(idx).cuda())
+        f, pos, sm = f.cpu().numpy(), pos.cpu().numpy(), sm.cpu().numpy()
+        for q, c in enumerate(idx):
+            rf, rpos, rsm = oracle_lib.decode(sp, int(c))
+            assert (f[q], tuple(pos[q]), tuple(sm[q])) == (rf, rpos, rsm)
+
+
+def test_deterministic(kr, config4):
+    w = workload(1)
+    d = dev_tables(w)
+    a = kr.evaluate_and_filter(w.space, *d)
+    b = kr.evaluate_and_filter(w.space, *d)
+    assert torch.equal(a.idx, b.idx) and torch.equal(a.T, b.T) and torch.equal(a.E, b.E)
+    off, T, E = (torch.from_numpy(x).cuda() for x in config4)
+    c1 = kr.compose_frontiers(off, T, E, 65536)
+    F1, bp1 = c1.F.clone(), c1.bp.clone()
+    c2 = kr.compose_frontiers(off, T, E, 65536)
+    assert torch.equal(F1, c2.F) and torch.equal(bp1, c2.bp)
