@@ -1,0 +1,234 @@
+"""Benchmark of the schedule-search hot path on one MI355X.
+
+One step = one pass of the whole path over one batch of synthetic input:
+  1. fused evaluation + frontier filter of the eval-stress batch: 1,024 partitions x
+     135,168 candidates (32 compute kernels, 33 launch positions, 32 SM choices, 128
+     frequencies) = 138,412,032 candidates;
+  2. composition of the compose-stress batch (512 precomputed frontiers of 256-2,048
+     points) over 65,536 time bins, staircase, and extraction of the leftmost
+     (max-throughput) schedule.
+Inputs are device-resident before the timed region.  `value` is candidates evaluated
+and Pareto-filtered per second (step 1's candidates over step 1's time, HIP events on
+the library's stream); `frontier_cells_per_s` is the composition's DP cells (sum over
+partitions of the reachable bins) over step 2's time.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--skip-cpu]
+       python bench.py --copy-calibration   (plain 1 GiB device copy, for counters)
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+FP64_VECTOR_TFLOPS = 78.6
+COUNTERS = os.path.join(ROOT, "profiles", "eval_filter_counters_eval_stress.txt")
+KERNEL_SOURCES = ["eval.hip", "kr_filter.h", "kr_device.h", "kr_launch.h"]
+METRIC = "schedule candidates evaluated+filtered/sec and frontier cells/sec on 1 MI355X"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2601_17654_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(n_launch_bytes_alg: float):
+    """HBM bytes per launch of the fused kernel from the committed counter summary, if
+    it was taken on the current kernel source; else None."""
+    if not os.path.exists(COUNTERS):
+        return None, "no counter summary"
+    vals = {}
+    for line in open(COUNTERS):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.strip().split("=", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_hash") != kernel_source_hash():
+        return None, "kernel changed since counters were taken"
+    try:
+        return float(vals["traffic_bytes_per_launch"]), "counters"
+    except (KeyError, ValueError):
+        return None, "incomplete counter summary"
+
+
+def copy_calibration():
+    import torch
+
+    n = 1 << 27  # 1 GiB of fp64
+    x = torch.ones(n, dtype=torch.float64, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n * 8, "copy_bytes_written": n * 8, "launches": 3}))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--skip-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--copy-calibration", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        log("bench.py runs on exactly one GPU: the schedule search here is a single-GPU "
+            "build (no collectives); --gpus %d is not supported." % args.gpus)
+        sys.exit(2)
+
+    import torch
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    from paper_2601_17654_amd import binding as kr
+    from paper_2601_17654_amd import inputs as I
+
+    torch.cuda.set_device(0)
+    t0 = time.time()
+    w = I.config_workload(3)
+    off4, T4, E4 = I.compose_frontiers()
+    B = I.COMPOSE_SPACE["bins"]
+    log("inputs generated in %.1f s" % (time.time() - t0))
+    sp = w.space
+    d = [torch.from_numpy(getattr(w, k)).cuda() for k in ("t", "pw", "tc", "pc")]
+    off4_d, T4_d, E4_d = (torch.from_numpy(x).cuda() for x in (off4, T4, E4))
+    table_bytes = sum(x.numel() * 8 for x in d)
+    n_cand = sp.n_parts * sp.n_cand
+
+    # exact output capacity from one untimed pass
+    fr = kr.evaluate_and_filter(sp, *d)
+    cap = int(fr.off[-1].item())
+    comp = kr.compose_frontiers(off4_d, T4_d, E4_d, B)
+    torch.cuda.synchronize()
+
+    def step(ev, phase_ev):
+        ev[0].record()
+        kr.set_phase_events(kr.PHASE_EVAL_TILE, *phase_ev[0])
+        kr.set_phase_events(kr.PHASE_MINPLUS, *phase_ev[1])
+        f = kr.evaluate_and_filter(sp, *d, cap=cap, sync=False)
+        ev[1].record()
+        kr.compose_frontiers(off4_d, T4_d, E4_d, B, out=comp)
+        ev[2].record()
+        kr.extract_schedule(comp, off4_d, T4_d, E4_d, comp.stair_bin[:1])
+        ev[3].record()
+        return f
+
+    def mk(n):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        for e in evs:
+            e.record()  # creates the HIP event behind the handle
+        return evs
+
+    for _ in range(args.warmup):
+        step(mk(4), [mk(2), mk(2)])
+    torch.cuda.synchronize()
+    evs = [mk(4) for _ in range(args.steps)]
+    pev = [[mk(2), mk(2)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for k in range(args.steps):
+        fr = step(evs[k], pev[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    kr.set_phase_events(kr.PHASE_EVAL_TILE)
+    kr.set_phase_events(kr.PHASE_MINPLUS)
+
+    ef_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    co_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    ex_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    kern_ms = float(np.mean([p[0][0].elapsed_time(p[0][1]) for p in pev]))
+    mp_ms = float(np.mean([p[1][0].elapsed_time(p[1][1]) for p in pev]))
+    ms_per_step = wall * 1e3 / args.steps
+    assert int(comp.status.item()) == 0 and int(fr.off[-1].item()) == cap
+
+    # composition cells: sum over partitions of the reachable bins after that partition
+    pt = comp.pt_bin.cpu().numpy()[: len(T4)]
+    Mk = np.maximum.reduceat(pt, off4[:-1]).astype(np.int64)
+    cells = int(np.sum(1 + np.cumsum(Mk)))
+
+    achieved = table_bytes / (kern_ms * 1e-3) / 1e9
+    traffic, tsrc = read_traffic(table_bytes)
+    roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+            "kernel": "eval_filter_kernel (fused evaluation + tile frontier)",
+            "kernel_ms": round(kern_ms, 4), "algorithmic_bytes": table_bytes,
+            "traffic_source": tsrc}
+
+    out = {
+        "metric": METRIC,
+        "value": n_cand / (ef_ms * 1e-3),
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {
+            "workload": "eval-stress (1024 partitions x 135,168 candidates: 32 kernels, "
+                        "33 positions, 32 SM choices, 128 frequencies) + compose-stress "
+                        "(512 frontiers of 256-2048 points, 65,536 bins)",
+            "candidates": n_cand, "frontier_points": cap, "compose_bins": B,
+            "compose_partitions": len(off4) - 1, "parallelism": "single GPU"},
+        "frontier_cells_per_s": cells / (co_ms * 1e-3),
+        "frontier_cells": cells,
+        "eval_filter_ms": round(ef_ms, 4),
+        "compose_ms": round(co_ms, 4),
+        "minplus_ms": round(mp_ms, 4),
+        "extract_ms": round(ex_ms, 4),
+        "roofline": roof,
+    }
+
+    if not args.skip_cpu:
+        import oracle
+
+        oracle.build(force=False)
+        t0 = time.perf_counter()
+        n = 0
+        mism = 0
+        off = fr.off.cpu().numpy()
+        gidx = fr.idx.cpu().numpy()
+        while n < sp.n_parts and (time.perf_counter() - t0) < args.cpu_seconds:
+            T, E = oracle.evaluate_partition(sp, w.t, w.pw, w.tc, w.pc, n)
+            ix = oracle.pareto(T, E)
+            mism += int(not np.array_equal(gidx[off[n]:off[n + 1]], ix))
+            n += 1
+        el = time.perf_counter() - t0
+        out["cpu_baseline"] = {
+            "value": n * sp.n_cand / el, "unit": "candidates/s", "cores": 1, "kind": "oracle",
+            "sample": "first %d of the 1024 eval-stress partitions (%d candidates), evaluate + "
+                      "GetFrontier, single-threaded C oracle, %.1f s" % (n, n * sp.n_cand, el)}
+        out["parity_check"] = {"partitions": n, "frontier_mismatches": mism}
+        t0 = time.perf_counter()
+        oracle.compose(off4, T4, E4, B)
+        el = time.perf_counter() - t0
+        out["cpu_baseline_compose"] = {"value": cells / el, "unit": "cells/s", "cores": 1,
+                                       "kind": "oracle", "sample": "full compose-stress batch, "
+                                       "%.1f s" % el}
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -120,9 +120,8 @@ int64_t kr_candidates_per_partition(const kr_space *space);
  *   n_total        host; = seg_off[n_seg]
  *   T, E           [n_total] device; T > 0 and E >= 0, finite
  *   seg_off        device [n_seg + 1]: non-decreasing, seg_off[0] = 0,
- *                  seg_off[n_seg] = n_total (trusted: not checked on the host)
- *   max_seg_len    host; an upper bound on every segment's length, < 2^31 (it sizes
- *                  the merge passes; a segment longer than this gives a wrong result)
+ *                  seg_off[n_seg] = n_total, every segment shorter than 2^31 (trusted:
+ *                  the host does not read it)
  *   cap            host; capacity of out_idx/out_T/out_E
  *   out_off        device [n_seg + 1]: out_off[g] = start of segment g's frontier;
  *                  out_off[n_seg] = total frontier points, even if > cap
@@ -132,10 +131,10 @@ int64_t kr_candidates_per_partition(const kr_space *space);
  * out_off[n_seg] after the stream completes.
  */
 kr_status kr_pareto_filter(int64_t n_total, const double *T, const double *E,
-                           const int64_t *seg_off, int32_t n_seg, int64_t max_seg_len,
-                           int64_t cap, int64_t *out_off, int32_t *out_idx, double *out_T,
-                           double *out_E, void *ws, size_t ws_bytes, void *stream);
-size_t kr_pareto_filter_workspace(int64_t n_total, int32_t n_seg, int64_t max_seg_len);
+                           const int64_t *seg_off, int32_t n_seg, int64_t cap, int64_t *out_off,
+                           int32_t *out_idx, double *out_T, double *out_E, void *ws,
+                           size_t ws_bytes, void *stream);
+size_t kr_pareto_filter_workspace(int64_t n_total, int32_t n_seg);
 
 /*
  * kr_evaluate_and_filter -- kr_evaluate_partition followed by kr_pareto_filter with
@@ -218,6 +217,22 @@ kr_status kr_extract_schedule(int32_t n_parts, int32_t n_bins, const int32_t *bp
 kr_status kr_decode_candidates(const kr_space *space, const int32_t *idx, int64_t n,
                                int32_t *f_out, int32_t *pos_out, int32_t *sm_out,
                                void *stream);
+
+/*
+ * kr_set_phase_events -- instrumentation for profilers and benchmarks (not part of the
+ * method).  When both events are non-NULL, later calls record `start_event` on their
+ * stream right before the phase's first kernel and `stop_event` right after its last
+ * one; NULL events switch the phase's recording off.  Events are hipEvent_t handles
+ * owned by the caller.  Library-global setting, not thread-safe.
+ *   KR_PHASE_EVAL_TILE  the fused evaluation + tile-frontier kernel of
+ *                       kr_evaluate_and_filter
+ *   KR_PHASE_MERGE      its staircase merges and output compaction
+ *   KR_PHASE_MINPLUS    the min-plus steps of kr_compose_frontiers
+ */
+#define KR_PHASE_EVAL_TILE 0
+#define KR_PHASE_MERGE 1
+#define KR_PHASE_MINPLUS 2
+kr_status kr_set_phase_events(int32_t phase, void *start_event, void *stop_event);
 
 /* Human-readable name of a status code. */
 const char *kr_status_string(kr_status status);

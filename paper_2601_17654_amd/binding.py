@@ -38,9 +38,9 @@ _SP = ctypes.POINTER(KrSpace)
 _SIGS = {
     "kr_evaluate_partition": (_i32, [_SP, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "kr_candidates_per_partition": (_i64, [_SP]),
-    "kr_pareto_filter": (_i32, [_i64, _vp, _vp, _vp, _i32, _i64, _i64, _vp, _vp, _vp, _vp, _vp,
-                                _sz, _vp]),
-    "kr_pareto_filter_workspace": (_sz, [_i64, _i32, _i64]),
+    "kr_pareto_filter": (_i32, [_i64, _vp, _vp, _vp, _i32, _i64, _vp, _vp, _vp, _vp, _vp, _sz,
+                                _vp]),
+    "kr_pareto_filter_workspace": (_sz, [_i64, _i32]),
     "kr_evaluate_and_filter": (_i32, [_SP, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _sz,
                                       _vp]),
     "kr_evaluate_and_filter_workspace": (_sz, [_SP]),
@@ -51,6 +51,7 @@ _SIGS = {
                                    _vp, _vp, _vp, _vp]),
     "kr_decode_candidates": (_i32, [_SP, _vp, _i64, _vp, _vp, _vp, _vp]),
     "kr_status_string": (ctypes.c_char_p, [_i32]),
+    "kr_set_phase_events": (_i32, [_i32, _vp, _vp]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -108,6 +109,16 @@ def _workspace(nbytes: int) -> torch.Tensor:
     return buf
 
 
+PHASE_EVAL_TILE, PHASE_MERGE, PHASE_MINPLUS = 0, 1, 2
+
+
+def set_phase_events(phase: int, start=None, stop=None) -> None:
+    """Record torch.cuda.Event pairs around a library phase (None switches it off)."""
+    a = ctypes.c_void_p(start.cuda_event) if start is not None else None
+    b = ctypes.c_void_p(stop.cuda_event) if stop is not None else None
+    _check("kr_set_phase_events", _lib.kr_set_phase_events(phase, a, b))
+
+
 def candidates_per_partition(space) -> int:
     return int(_lib.kr_candidates_per_partition(ctypes.byref(_space(space))))
 
@@ -156,8 +167,7 @@ def _finish_frontier(off, idx, T, E, cap, sync):
     return Frontier(off, idx[:total], T[:total], E[:total]), True
 
 
-def pareto_filter(T, E, seg_off, max_seg_len: Optional[int] = None, cap: Optional[int] = None,
-                  sync: bool = True) -> Frontier:
+def pareto_filter(T, E, seg_off, cap: Optional[int] = None, sync: bool = True) -> Frontier:
     """GetFrontier of every segment [seg_off[g], seg_off[g+1]) of (T, E)."""
     seg_host = np.asarray(seg_off.cpu() if isinstance(seg_off, torch.Tensor) else seg_off,
                           dtype=np.int64)
@@ -169,8 +179,6 @@ def pareto_filter(T, E, seg_off, max_seg_len: Optional[int] = None, cap: Optiona
     n_total = int(seg_host[-1])
     if T.numel() != n_total or E.numel() != n_total:
         raise ValueError("T/E must hold seg_off[-1] points")
-    if max_seg_len is None:
-        max_seg_len = int(np.diff(seg_host).max()) if n_seg > 0 else 0
     seg_dev = torch.from_numpy(seg_host).cuda()
     while True:
         c = int(cap) if cap is not None else min(n_total, max(4096 * max(n_seg, 1), 1))
@@ -178,12 +186,11 @@ def pareto_filter(T, E, seg_off, max_seg_len: Optional[int] = None, cap: Optiona
         idx = torch.empty(max(c, 1), dtype=torch.int32, device="cuda")
         oT = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
         oE = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
-        wsb = _lib.kr_pareto_filter_workspace(n_total, n_seg, max_seg_len)
+        wsb = _lib.kr_pareto_filter_workspace(n_total, n_seg)
         ws = _workspace(wsb)
         _check("kr_pareto_filter",
-               _lib.kr_pareto_filter(n_total, _ptr(T), _ptr(E), _ptr(seg_dev), n_seg, max_seg_len,
-                                     c, _ptr(off), _ptr(idx), _ptr(oT), _ptr(oE), _ptr(ws), wsb,
-                                     _stream()))
+               _lib.kr_pareto_filter(n_total, _ptr(T), _ptr(E), _ptr(seg_dev), n_seg, c, _ptr(off),
+                                     _ptr(idx), _ptr(oT), _ptr(oE), _ptr(ws), wsb, _stream()))
         fr, ok = _finish_frontier(off, idx, oT, oE, c, sync)
         if fr is not None:
             return fr

@@ -4,15 +4,16 @@
 #include <cstring>
 
 #include "../../include/kareus.h"
+#include "kr_filter.h"
 #include "kr_launch.h"
 
 using namespace kr;
 
 namespace {
 
-constexpr int kTile = 2048;        // points per tile of the stand-alone filter
-constexpr int kBuckets = 512;      // time buckets of the tile prefilter
 constexpr size_t kLdsBudget = 65536;
+constexpr size_t kLdsPerCu = 160 * 1024;
+constexpr int kSurvDoubles = KR_SURV_CAP * 20 / 8;
 constexpr size_t kAlign = 256;
 
 // Bump allocator over the caller's workspace (or a size query when base == nullptr).
@@ -62,73 +63,90 @@ bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)
     a->C = cf * s->n_freq;
     a->p_static = s->p_static;
     const int64_t S1 = a->S + 1;
-    a->slab_doubles = (int)(2 * a->N * S1 + 2 * S1 * (a->N + 1) + 2 * a->M * a->S);
-    a->pair_doubles = a->M == 2 ? (a->n_pp * 4 + 7) / 8 : 0;
-    size_t lds = (size_t)(a->slab_doubles + a->pair_doubles) * 8;
-    if (lds > kLdsBudget) return false;
+    const int64_t staged = 2 * a->N * S1 + 2 * a->M * a->S;  // t, pw, tc, pc
+    const int64_t sums = 2 * (a->N + 1) * S1;
+    const int64_t pairs = a->M == 2 ? (a->n_pp * 4 + 7) / 8 : 0;
+    a->surv_off = (int)(staged + sums + pairs);
+    a->lds_doubles = a->surv_off + (fused ? kSurvDoubles : 0);
+    if ((size_t)a->lds_doubles * 8 > kLdsBudget) return false;
     if (!fused) return true;
-    static const int cpts[] = {1, 2, 4, 5, 8};
-    int pick = 4;
-    for (int i = 0; i < 5; ++i)
-        if ((int64_t)256 * cpts[i] >= a->Cf) {
-            pick = i;
-            break;
+    // register prefetch: pf doubles per thread of each table, one of the comm tables
+    const int64_t slab = a->N * S1;
+    a->pf = (int)((slab + KR_BLOCK - 1) / KR_BLOCK);
+    if (a->pf > 8 || a->M * a->S > KR_BLOCK) return false;
+    a->one_comm = a->M == 1 && a->S <= KR_BLOCK;
+    if (a->one_comm) {
+        a->nchunk = KR_BLOCK / a->S;
+        a->cpt = (int)std::min<int64_t>(8, (a->n_pos + a->nchunk - 1) / a->nchunk);
+        a->ntiles = (a->n_pos + a->nchunk * a->cpt - 1) / (a->nchunk * a->cpt);
+        a->tile = a->nchunk * a->cpt * a->S;
+        // one tile per slab: the staged time table is dead once the tile is evaluated,
+        // so the survivor list can live on top of it
+        if (a->ntiles == 1 && a->N * S1 >= kSurvDoubles) {
+            a->surv_off = 0;
+            a->lds_doubles -= kSurvDoubles;
         }
-    for (; pick >= 0; --pick) {
-        const int tile = (int)std::min<int64_t>(a->Cf, 256 * cpts[pick]);
-        if (lds + (size_t)kBuckets * 8 + (size_t)tile * 20 <= kLdsBudget) {
-            a->cpt = cpts[pick];
-            a->tile = tile;
-            a->tiles_per_freq = (a->Cf + tile - 1) / tile;
-            return true;
-        }
+    } else {
+        a->cpt = (int)std::min<int64_t>(8, (a->Cf + KR_BLOCK - 1) / KR_BLOCK);
+        a->tile = KR_BLOCK * a->cpt;
+        a->ntiles = (a->Cf + a->tile - 1) / a->tile;
     }
-    return false;
+    // enough blocks to fill every CU at the LDS-limited occupancy
+    const size_t per_block = (size_t)a->lds_doubles * 8 + 1024;
+    const int64_t resident = std::max<int64_t>(1, std::min<size_t>(8, kLdsPerCu / per_block));
+    const int64_t target = 256 * resident;
+    int64_t nfb = std::max<int64_t>(1, (target + a->P - 1) / a->P);
+    nfb = std::min<int64_t>(nfb, a->F);
+    a->fb = (int)((a->F + nfb - 1) / nfb);
+    a->nfb = (a->F + a->fb - 1) / a->fb;
+    return true;
 }
 
-int levels_for(int64_t tiles)
+// Caller-owned events recorded around a phase (kr_set_phase_events).
+hipEvent_t g_phase_ev[3][2] = {};
+
+void phase_mark(int phase, int which, hipStream_t st)
 {
-    int l = 0;
-    while (((int64_t)1 << l) < tiles) ++l;
-    return l;
+    if (g_phase_ev[phase][0] && g_phase_ev[phase][1])
+        (void)hipEventRecord(g_phase_ev[phase][which], st);
 }
 
 struct FilterWs {
-    int64_t *seg_off, *tile_base;
-    int32_t *cnt[2];
+    int64_t *seg_off, *unit_base;
+    int32_t *ucnt, *fcnt, *runcnt;
     PointBufs buf[2];
     uint8_t *flags;
 };
 
-FilterWs carve_filter(Carve &c, int64_t n_total, int n_seg, int64_t n_tiles, bool own_seg_off)
+FilterWs carve_filter(Carve &c, int64_t n_total, int n_seg, int64_t n_units, bool own_seg_off)
 {
     FilterWs w;
+    const int64_t n = std::max<int64_t>(n_total, 1);
     w.seg_off = own_seg_off ? c.take<int64_t>(n_seg + 1) : nullptr;
-    w.tile_base = c.take<int64_t>(n_seg + 1);
-    for (int i = 0; i < 2; ++i) w.cnt[i] = c.take<int32_t>(std::max<int64_t>(n_tiles, 1));
+    w.unit_base = c.take<int64_t>(n_seg + 1);
+    w.ucnt = c.take<int32_t>(std::max<int64_t>(n_units, 1));
+    w.fcnt = c.take<int32_t>(std::max(n_seg, 1));
+    w.runcnt = c.take<int32_t>(n_total / KR_FIN_CAP + n_seg + 1);
     for (int i = 0; i < 2; ++i) {
-        w.buf[i].T = c.take<double>(std::max<int64_t>(n_total, 1));
-        w.buf[i].E = c.take<double>(std::max<int64_t>(n_total, 1));
-        w.buf[i].I = c.take<int32_t>(std::max<int64_t>(n_total, 1));
+        w.buf[i].T = c.take<double>(n);
+        w.buf[i].E = c.take<double>(n);
+        w.buf[i].I = c.take<int32_t>(n);
     }
-    w.flags = c.take<uint8_t>(std::max<int64_t>(n_total, 1));
+    w.flags = c.take<uint8_t>((n + 3) / 4 * 4);
     return w;
 }
 
-// Merge the tile frontiers of every segment level by level, then write the output.
-kr_status merge_and_finish(const SegLayout &L, FilterWs &w, int64_t max_tiles, int64_t cap,
-                           int64_t *out_off, int32_t *out_idx, double *out_T, double *out_E,
-                           hipStream_t st)
+// Union of every segment's unit frontiers, then the CSR output.
+kr_status finish_segments(const SegLayout &L, FilterWs &w, int64_t cap, int64_t *out_off,
+                          int32_t *out_idx, double *out_T, double *out_E, hipStream_t st)
 {
-    const int levels = levels_for(max_tiles);
-    for (int l = 0; l < levels; ++l) {
-        if (launch_merge_level(L, l, max_tiles, w.buf[l % 2], w.cnt[l % 2], w.buf[(l + 1) % 2],
-                               w.cnt[(l + 1) % 2], w.flags, st) != hipSuccess)
-            return KR_EHIP;
-    }
-    if (launch_finish(L, w.buf[levels % 2], w.cnt[levels % 2], cap, out_off, out_idx, out_T,
-                      out_E, st) != hipSuccess)
+    phase_mark(KR_PHASE_MERGE, 0, st);
+    if (launch_finalize(L, w.buf[0], w.ucnt, w.buf[1], w.fcnt, w.runcnt, w.flags, st) !=
+        hipSuccess)
         return KR_EHIP;
+    if (launch_output(L, w.buf[1], w.fcnt, cap, out_off, out_idx, out_T, out_E, st) != hipSuccess)
+        return KR_EHIP;
+    phase_mark(KR_PHASE_MERGE, 1, st);
     return KR_OK;
 }
 
@@ -158,58 +176,46 @@ kr_status kr_evaluate_partition(const kr_space *space, const double *t, const do
     return launch_eval(a, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
 }
 
-size_t kr_pareto_filter_workspace(int64_t n_total, int32_t n_seg, int64_t max_seg_len)
+size_t kr_pareto_filter_workspace(int64_t n_total, int32_t n_seg)
 {
-    if (n_total < 0 || n_seg < 0 || max_seg_len < 0) return 0;
-    const int64_t n_tiles = (n_total + kTile - 1) / kTile + n_seg;
+    if (n_total < 0 || n_seg < 0) return 0;
+    const int64_t n_units = (n_total + KR_TILE - 1) / KR_TILE + n_seg;
     Carve c(nullptr);
-    carve_filter(c, n_total, n_seg, n_tiles, false);
+    carve_filter(c, n_total, n_seg, n_units, false);
     return c.used;
 }
 
 kr_status kr_pareto_filter(int64_t n_total, const double *T, const double *E,
-                           const int64_t *seg_off, int32_t n_seg, int64_t max_seg_len, int64_t cap,
-                           int64_t *out_off, int32_t *out_idx, double *out_T, double *out_E,
-                           void *ws, size_t ws_bytes, void *stream)
+                           const int64_t *seg_off, int32_t n_seg, int64_t cap, int64_t *out_off,
+                           int32_t *out_idx, double *out_T, double *out_E, void *ws,
+                           size_t ws_bytes, void *stream)
 {
-    if (n_total < 0 || n_seg < 0 || max_seg_len < 0 || max_seg_len > 0x7FFFFFFF || cap < 0 ||
-        !seg_off || !out_off || (n_total > 0 && (!T || !E)) ||
-        (cap > 0 && (!out_idx || !out_T || !out_E)) || !ws)
+    if (n_total < 0 || n_seg < 0 || cap < 0 || !seg_off || !out_off ||
+        (n_total > 0 && (!T || !E)) || (cap > 0 && (!out_idx || !out_T || !out_E)) || !ws)
         return KR_EINVAL;
-    if (ws_bytes < kr_pareto_filter_workspace(n_total, n_seg, max_seg_len)) return KR_ECAPACITY;
+    if (ws_bytes < kr_pareto_filter_workspace(n_total, n_seg)) return KR_ECAPACITY;
     hipStream_t st = (hipStream_t)stream;
-    const int64_t n_tiles = (n_total + kTile - 1) / kTile + n_seg;
+    const int64_t n_units = (n_total + KR_TILE - 1) / KR_TILE + n_seg;
     Carve c(ws);
-    FilterWs w = carve_filter(c, n_total, n_seg, n_tiles, false);
+    FilterWs w = carve_filter(c, n_total, n_seg, n_units, false);
     SegLayout L;
     L.seg_off = seg_off;
-    L.tile_base = w.tile_base;
+    L.unit_base = w.unit_base;
     L.n_seg = n_seg;
-    L.tile = kTile;
-    L.tiles_per_group = 1;
-    L.group_elems = kTile;
-    if (n_seg > 0 && launch_tile_layout(seg_off, w.tile_base, n_seg, kTile, st) != hipSuccess)
+    L.unit_stride = KR_TILE;
+    if (n_seg > 0 && launch_tile_layout(seg_off, w.unit_base, n_seg, KR_TILE, st) != hipSuccess)
         return KR_EHIP;
-    TileOut o;
-    o.T = w.buf[0].T;
-    o.E = w.buf[0].E;
-    o.I = w.buf[0].I;
-    o.cnt = w.cnt[0];
-    o.tiles_per_seg = 0;
-    o.nb = kBuckets;
-    if (n_seg > 0 && launch_pareto_tiles(T, E, L, n_tiles, o, kTile / 256, st) != hipSuccess)
-        return KR_EHIP;
-    const int64_t max_tiles = (max_seg_len + kTile - 1) / kTile;
-    return merge_and_finish(L, w, max_tiles, cap, out_off, out_idx, out_T, out_E, st);
+    UnitOut o{w.buf[0].T, w.buf[0].E, w.buf[0].I, w.ucnt};
+    if (n_seg > 0 && launch_pareto_tiles(T, E, L, n_units, o, st) != hipSuccess) return KR_EHIP;
+    return finish_segments(L, w, cap, out_off, out_idx, out_T, out_E, st);
 }
 
 size_t kr_evaluate_and_filter_workspace(const kr_space *space)
 {
     EvalArgs a;
     if (!space_ok(space) || !eval_plan(space, true, &a)) return 0;
-    const int64_t tiles = (int64_t)a.P * a.F * a.tiles_per_freq;
     Carve c(nullptr);
-    carve_filter(c, (int64_t)a.P * a.C, a.P, tiles, true);
+    carve_filter(c, (int64_t)a.P * a.C, a.P, (int64_t)a.P * a.nfb, true);
     return c.used;
 }
 
@@ -230,27 +236,20 @@ kr_status kr_evaluate_and_filter(const kr_space *space, const double *t, const d
     a.pw = pw;
     a.tc = tc;
     a.pc = pc;
-    const int64_t tiles_per_seg = (int64_t)a.F * a.tiles_per_freq;
     Carve c(ws);
-    FilterWs w = carve_filter(c, (int64_t)a.P * a.C, a.P, tiles_per_seg * a.P, true);
-    if (launch_uniform_layout(w.seg_off, w.tile_base, a.P, a.C, tiles_per_seg, st) != hipSuccess)
+    FilterWs w = carve_filter(c, (int64_t)a.P * a.C, a.P, (int64_t)a.P * a.nfb, true);
+    if (launch_uniform_layout(w.seg_off, w.unit_base, a.P, a.C, a.nfb, st) != hipSuccess)
         return KR_EHIP;
-    TileOut o;
-    o.T = w.buf[0].T;
-    o.E = w.buf[0].E;
-    o.I = w.buf[0].I;
-    o.cnt = w.cnt[0];
-    o.tiles_per_seg = tiles_per_seg;
-    o.nb = kBuckets;
+    UnitOut o{w.buf[0].T, w.buf[0].E, w.buf[0].I, w.ucnt};
+    phase_mark(KR_PHASE_EVAL_TILE, 0, st);
     if (launch_eval_filter(a, o, st) != hipSuccess) return KR_EHIP;
+    phase_mark(KR_PHASE_EVAL_TILE, 1, st);
     SegLayout L;
     L.seg_off = w.seg_off;
-    L.tile_base = w.tile_base;
+    L.unit_base = w.unit_base;
     L.n_seg = a.P;
-    L.tile = a.tile;
-    L.tiles_per_group = a.tiles_per_freq;
-    L.group_elems = a.Cf;
-    return merge_and_finish(L, w, tiles_per_seg, cap, out_off, out_idx, out_T, out_E, st);
+    L.unit_stride = (int64_t)a.fb * a.Cf;
+    return finish_segments(L, w, cap, out_off, out_idx, out_T, out_E, st);
 }
 
 size_t kr_compose_frontiers_workspace(int32_t n_parts, int32_t n_bins)
@@ -319,7 +318,10 @@ kr_status kr_compose_frontiers(int32_t n_parts, const int64_t *off, const double
     a.status = status_out;
     a.stair_Tlo = stair_Tlo;
     a.stair_E = stair_E;
-    return launch_compose(a, w, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
+    hipEvent_t *ev = g_phase_ev[KR_PHASE_MINPLUS];
+    return launch_compose(a, w, ev[0] && ev[1] ? ev : nullptr, (hipStream_t)stream) == hipSuccess
+               ? KR_OK
+               : KR_EHIP;
 }
 
 kr_status kr_extract_schedule(int32_t n_parts, int32_t n_bins, const int32_t *bp,
@@ -371,6 +373,14 @@ kr_status kr_decode_candidates(const kr_space *space, const int32_t *idx, int64_
     if (cf * space->n_freq > 0x7FFFFFFF) return KR_EUNSUPPORTED;
     d.Cf = (int)cf;
     return launch_decode(d, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
+}
+
+kr_status kr_set_phase_events(int32_t phase, void *start_event, void *stop_event)
+{
+    if (phase < 0 || phase > 2) return KR_EINVAL;
+    g_phase_ev[phase][0] = (hipEvent_t)start_event;
+    g_phase_ev[phase][1] = (hipEvent_t)stop_event;
+    return KR_OK;
 }
 
 const char *kr_status_string(kr_status status)

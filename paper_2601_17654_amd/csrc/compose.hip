@@ -240,7 +240,8 @@ __global__ void __launch_bounds__(KR_BLOCK) staircase_kernel(ComposeArgs a)
     if (threadIdx.x == 0) *a.n_stair = n;
 }
 
-hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipStream_t st)
+hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipEvent_t *minplus_ev,
+                          hipStream_t st)
 {
     hipLaunchKernelGGL(compose_init_kernel, dim3(1), dim3(64), 0, st, a);
     hipLaunchKernelGGL(compose_range_kernel, dim3(a.P), dim3(KR_BLOCK), 0, st, a, w);
@@ -250,12 +251,14 @@ hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipStream_t 
     double *buf[2] = {w.F0, w.F1};
     double *prev = a.P == 1 ? a.F_out : buf[0];
     hipLaunchKernelGGL(compose_first_kernel, grid, dim3(KR_BLOCK), 0, st, a, w, prev);
+    if (minplus_ev) (void)hipEventRecord(minplus_ev[0], st);
     for (int k = 1; k < a.P; ++k) {
         double *cur = (k == a.P - 1) ? a.F_out : buf[k % 2];
         hipLaunchKernelGGL(minplus_step_kernel, grid, dim3(KR_BLOCK), 0, st, a, w, k,
                            (const double *)prev, cur);
         prev = cur;
     }
+    if (minplus_ev) (void)hipEventRecord(minplus_ev[1], st);
     hipLaunchKernelGGL(staircase_kernel, dim3(1), dim3(KR_BLOCK), 0, st, a);
     return hipGetLastError();
 }

@@ -38,6 +38,52 @@ struct SumI64 {
     __device__ __forceinline__ int64_t operator()(int64_t a, int64_t b) const { return a + b; }
 };
 
+// Barrier for LDS traffic only: unlike __syncthreads() it does not wait for
+// outstanding global loads, so register prefetches stay in flight across it.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Value of a uniform-indexed lane.
+__device__ __forceinline__ uint64_t lane_u64(uint64_t x, int lane)
+{
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)x, lane);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(x >> 32), lane);
+    return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ int32_t lane_i32(int32_t x, int lane)
+{
+    return __builtin_amdgcn_readlane(x, lane);
+}
+
+// One DPP step of a wave minimum over unsigned 64-bit values.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint64_t dpp_min_u64(uint64_t x)
+{
+    const uint32_t lo = (uint32_t)x, hi = (uint32_t)(x >> 32);
+    const uint32_t ylo = __builtin_amdgcn_update_dpp(lo, lo, CTRL, ROWS, 0xF, false);
+    const uint32_t yhi = __builtin_amdgcn_update_dpp(hi, hi, CTRL, ROWS, 0xF, false);
+    const uint64_t y = ((uint64_t)yhi << 32) | ylo;
+    return y < x ? y : x;
+}
+
+// Minimum over a full wave64 (all lanes active), uniform result: pairs, quads, half
+// rows and rows by DPP permutes, then rows 0-1 and 0-3 by row broadcasts; lane 63
+// ends up holding the minimum.
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t x)
+{
+    x = dpp_min_u64<0xB1, 0xF>(x);   // quad_perm [1,0,3,2]
+    x = dpp_min_u64<0x4E, 0xF>(x);   // quad_perm [2,3,0,1]
+    x = dpp_min_u64<0x141, 0xF>(x);  // row_half_mirror
+    x = dpp_min_u64<0x140, 0xF>(x);  // row_mirror
+    x = dpp_min_u64<0x142, 0xA>(x);  // row_bcast:15 into rows 1 and 3
+    x = dpp_min_u64<0x143, 0xC>(x);  // row_bcast:31 into rows 2 and 3
+    return lane_u64(x, 63);
+}
+
 template <typename T>
 __device__ __forceinline__ T shfl_up(T v, int d)
 {

@@ -4,6 +4,10 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#define KR_FIN_CAP 2560    // points the finalize kernel sorts in LDS
+#define KR_FIN_UNITS 2048  // units per segment the finalize kernel's LDS path takes
+#define KR_TILE 2048       // points per tile of the stand-alone filter
+
 namespace kr {
 
 struct EvalArgs {
@@ -13,20 +17,21 @@ struct EvalArgs {
     int Cf;                 // candidates per frequency
     int64_t C;              // candidates per partition
     double p_static;
-    int slab_doubles;       // LDS doubles of the table slab
-    int pair_doubles;       // LDS doubles holding the position-pair table
-    int tile;               // fused: candidates per tile
-    int tiles_per_freq;     // fused: tiles per frequency
-    int cpt;                // fused: candidates per thread (tile <= 256 * cpt)
+    int lds_doubles;        // dynamic LDS of the launch, in doubles
+    // fused evaluation + filter
+    int surv_off;           // LDS offset (doubles) of the survivor list
+    int nfb, fb;            // frequency blocks per partition, frequencies per block
+    int one_comm;           // one comm kernel: thread = (SM choice, run of positions)
+    int nchunk, cpt;        // position runs per tile / positions (or candidates) per thread
+    int ntiles, tile;       // tiles per frequency; candidates per tile (generic mapping)
+    int pf;                 // doubles per thread and table of the register prefetch
 };
 
-// Tile-local frontiers written by the fused kernel or the pareto tile kernel.
-struct TileOut {
+// Per-unit frontiers written by the fused kernel or the tile kernel.
+struct UnitOut {
     double *T, *E;
     int32_t *I;
-    int32_t *cnt;           // [segments * tiles_per_seg]
-    int64_t tiles_per_seg;  // fused path: F * tiles_per_freq
-    int nb;                 // time buckets of the prefilter
+    int32_t *cnt;  // [units]
 };
 
 struct DecodeArgs {
@@ -36,14 +41,13 @@ struct DecodeArgs {
     int M, S, n_pos, F, Cf;
 };
 
-// Segmented frontier: layout of tiles inside segments.
+// Units of segment g are unit_base[g] .. unit_base[g+1]-1; unit k of segment g has its
+// slot at element seg_off[g] + k * unit_stride.
 struct SegLayout {
-    const int64_t *seg_off;   // [n_seg + 1] element offsets
-    const int64_t *tile_base; // [n_seg + 1] first tile of each segment
+    const int64_t *seg_off;    // [n_seg + 1]
+    const int64_t *unit_base;  // [n_seg + 1]
     int n_seg;
-    int tile;                 // elements per tile
-    int tiles_per_group;      // tiles per frequency group (fused), else 1
-    int64_t group_elems;      // elements per group (fused: candidates per frequency)
+    int64_t unit_stride;
 };
 
 struct PointBufs {
@@ -52,20 +56,20 @@ struct PointBufs {
 };
 
 hipError_t launch_eval(const EvalArgs &a, hipStream_t st);
-hipError_t launch_eval_filter(const EvalArgs &a, const TileOut &o, hipStream_t st);
+hipError_t launch_eval_filter(const EvalArgs &a, const UnitOut &o, hipStream_t st);
 hipError_t launch_decode(const DecodeArgs &d, hipStream_t st);
 
 // pareto.hip
-hipError_t launch_uniform_layout(int64_t *seg_off, int64_t *tile_base, int n_seg,
-                                 int64_t seg_len, int64_t tiles_per_seg, hipStream_t st);
-hipError_t launch_tile_layout(const int64_t *seg_off, int64_t *tile_base, int n_seg, int tile,
+hipError_t launch_uniform_layout(int64_t *seg_off, int64_t *unit_base, int n_seg,
+                                 int64_t seg_len, int64_t units_per_seg, hipStream_t st);
+hipError_t launch_tile_layout(const int64_t *seg_off, int64_t *unit_base, int n_seg, int tile,
                               hipStream_t st);
 hipError_t launch_pareto_tiles(const double *T, const double *E, const SegLayout &L,
-                               int64_t n_tiles_bound, const TileOut &o, int cpt, hipStream_t st);
-hipError_t launch_merge_level(const SegLayout &L, int level, int64_t max_tiles,
-                              const PointBufs &in, const int32_t *cnt_in, const PointBufs &out,
-                              int32_t *cnt_out, uint8_t *flags, hipStream_t st);
-hipError_t launch_finish(const SegLayout &L, const PointBufs &fin, const int32_t *cnt,
+                               int64_t n_units_bound, const UnitOut &o, hipStream_t st);
+hipError_t launch_finalize(const SegLayout &L, const PointBufs &buf, const int32_t *ucnt,
+                           const PointBufs &fin, int32_t *fcnt, int32_t *runcnt, uint8_t *flags,
+                           hipStream_t st);
+hipError_t launch_output(const SegLayout &L, const PointBufs &fin, const int32_t *fcnt,
                          int64_t cap, int64_t *out_off, int32_t *out_idx, double *out_T,
                          double *out_E, hipStream_t st);
 
@@ -91,7 +95,8 @@ struct ComposeArgs {
     int32_t *L_out, *stair_bin, *n_stair, *status;
     double *stair_Tlo, *stair_E;
 };
-hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipStream_t st);
+hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipEvent_t *minplus_ev,
+                          hipStream_t st);
 
 struct ExtractArgs {
     int P, B, n_q;

@@ -2,40 +2,42 @@
 //
 // Rule: within a segment, sort points by (T, E, index) and keep a point iff its E is
 // strictly below every E before it -- the non-dominated set, exact duplicates
-// resolved to the smallest index.
+// resolved to the smallest index.  The rule is decomposable: the frontier of a union
+// is the frontier of the union of the parts' frontiers.
 //
-// Work split: every segment is cut into tiles; each tile's exact frontier is found in
-// LDS (kr_tile.h).  The frontier rule is decomposable -- the frontier of a union is
-// the frontier of the union of the parts' frontiers -- so tile frontiers (strict
-// staircases) are merged pairwise, level by level, until one staircase per segment
-// remains.  A merge needs no sort: an element's rank in the partner staircase comes
-// from a binary search, and it survives iff the partner element just before it in
-// key order has a larger E (staircases have strictly falling E).
+// Work split: every segment is cut into units (tiles of points, or the frequency
+// range of one fused workgroup) whose exact frontiers are written to the unit's slot.
+// One workgroup per segment then takes the union of its units' frontiers: sorted and
+// scanned in LDS when it fits, otherwise cut into LDS-sized chunks whose frontiers
+// are merged pairwise in device memory.  A pairwise merge of two staircases needs no
+// sort: an element's rank in the partner comes from a binary search, and it survives
+// iff the partner element just before it in key order has a larger E.
+#include "kr_filter.h"
 #include "kr_launch.h"
-#include "kr_tile.h"
+
 
 namespace kr {
 
-__global__ void uniform_layout_kernel(int64_t *seg_off, int64_t *tile_base, int n_seg,
-                                      int64_t seg_len, int64_t tiles_per_seg)
+__global__ void uniform_layout_kernel(int64_t *seg_off, int64_t *unit_base, int n_seg,
+                                      int64_t seg_len, int64_t units_per_seg)
 {
     const int g = blockIdx.x * KR_BLOCK + threadIdx.x;
     if (g > n_seg) return;
     seg_off[g] = (int64_t)g * seg_len;
-    tile_base[g] = (int64_t)g * tiles_per_seg;
+    unit_base[g] = (int64_t)g * units_per_seg;
 }
 
-hipError_t launch_uniform_layout(int64_t *seg_off, int64_t *tile_base, int n_seg,
-                                 int64_t seg_len, int64_t tiles_per_seg, hipStream_t st)
+hipError_t launch_uniform_layout(int64_t *seg_off, int64_t *unit_base, int n_seg,
+                                 int64_t seg_len, int64_t units_per_seg, hipStream_t st)
 {
     hipLaunchKernelGGL(uniform_layout_kernel, dim3((n_seg + 1 + KR_BLOCK - 1) / KR_BLOCK),
-                       dim3(KR_BLOCK), 0, st, seg_off, tile_base, n_seg, seg_len, tiles_per_seg);
+                       dim3(KR_BLOCK), 0, st, seg_off, unit_base, n_seg, seg_len, units_per_seg);
     return hipGetLastError();
 }
 
-// tile_base = exclusive prefix sum of ceil(len_g / tile); one block.
+// unit_base = exclusive prefix sum of ceil(len_g / tile); one block.
 __global__ void __launch_bounds__(KR_BLOCK)
-tile_layout_kernel(const int64_t *seg_off, int64_t *tile_base, int n_seg, int tile)
+tile_layout_kernel(const int64_t *seg_off, int64_t *unit_base, int n_seg, int tile)
 {
     __shared__ int64_t sc[KR_WAVES];
     int64_t carry = 0;
@@ -48,145 +50,133 @@ tile_layout_kernel(const int64_t *seg_off, int64_t *tile_base, int n_seg, int ti
         }
         int64_t tot;
         const int64_t ex = block_exclusive(nt, (int64_t)0, SumI64(), sc, &tot);
-        if (g < n_seg) tile_base[g] = carry + ex;
+        if (g < n_seg) unit_base[g] = carry + ex;
         carry += tot;
     }
-    if (threadIdx.x == 0) tile_base[n_seg] = carry;
+    if (threadIdx.x == 0) unit_base[n_seg] = carry;
 }
 
-hipError_t launch_tile_layout(const int64_t *seg_off, int64_t *tile_base, int n_seg, int tile,
+hipError_t launch_tile_layout(const int64_t *seg_off, int64_t *unit_base, int n_seg, int tile,
                               hipStream_t st)
 {
-    hipLaunchKernelGGL(tile_layout_kernel, dim3(1), dim3(KR_BLOCK), 0, st, seg_off, tile_base,
+    hipLaunchKernelGGL(tile_layout_kernel, dim3(1), dim3(KR_BLOCK), 0, st, seg_off, unit_base,
                        n_seg, tile);
     return hipGetLastError();
 }
 
-__device__ __forceinline__ int64_t tile_start(const SegLayout &L, int64_t k)
-{
-    return (k / L.tiles_per_group) * L.group_elems + (k % L.tiles_per_group) * (int64_t)L.tile;
-}
-
-// Segment holding global tile w (tile_base is non-decreasing).
-__device__ __forceinline__ int find_segment(const int64_t *tile_base, int n_seg, int64_t w)
+// Segment holding global unit w (unit_base is non-decreasing).
+__device__ __forceinline__ int find_segment(const int64_t *unit_base, int n_seg, int64_t w)
 {
     int lo = 0, hi = n_seg - 1;
     while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
-        if (tile_base[mid] <= w) lo = mid;
+        if (unit_base[mid] <= w) lo = mid;
         else hi = mid - 1;
     }
     return lo;
 }
 
-template <int CPT>
+// Exact frontier of one tile of up to 2,048 consecutive points of a segment.
 __global__ void __launch_bounds__(KR_BLOCK)
-pareto_tile_kernel(const double *T, const double *E, SegLayout L, TileOut o)
+pareto_tile_kernel(const double *T, const double *E, SegLayout L, UnitOut o)
 {
-    extern __shared__ uint64_t tile_lds[];
-    __shared__ TileScratch sc;
+    extern __shared__ double tile_lds[];
+    __shared__ FilterShared fsh;
     const int64_t w = blockIdx.x;
-    if (w >= L.tile_base[L.n_seg]) return;
-    const int g = find_segment(L.tile_base, L.n_seg, w);
-    const int64_t k = w - L.tile_base[g];
+    if (w >= L.unit_base[L.n_seg]) return;
+    const int g = find_segment(L.unit_base, L.n_seg, w);
     const int64_t s0 = L.seg_off[g];
-    const int64_t start = s0 + k * L.tile;
-    const int64_t end = min(start + (int64_t)L.tile, L.seg_off[g + 1]);
-    TileLds tl;
-    tl.nb = o.nb;
-    tl.cap = L.tile;
-    tl.bkt = tile_lds;
-    tl.sT = tl.bkt + o.nb;
-    tl.sE = tl.sT + L.tile;
-    tl.sI = (int32_t *)(tl.sE + L.tile);
-    double vT[CPT], vE[CPT];
-    int32_t vI[CPT];
-    bool ok[CPT];
+    const int64_t start = s0 + (w - L.unit_base[g]) * L.unit_stride;
+    const int64_t end = min(start + L.unit_stride, L.seg_off[g + 1]);
+    FilterLds fl;
+    fl.sh = &fsh;
+    fl.sT = (uint64_t *)tile_lds;
+    fl.sE = fl.sT + KR_SURV_CAP;
+    fl.sI = (int32_t *)(fl.sE + KR_SURV_CAP);
+    double vT[8], vE[8];
+    int32_t vI[8];
+    bool ok[8];
 #pragma unroll
-    for (int q = 0; q < CPT; ++q) {
+    for (int q = 0; q < 8; ++q) {
         const int64_t x = start + threadIdx.x + q * KR_BLOCK;
         ok[q] = x < end;
         vT[q] = ok[q] ? T[x] : 0.0;
         vE[q] = ok[q] ? E[x] : 0.0;
         vI[q] = (int32_t)(x - s0);
     }
-    const int n = tile_frontier<CPT>(vT, vE, vI, ok, tl, sc, o.T + start, o.E + start, o.I + start);
+    int parity = 0;
+    const int n = tile_frontier<8>(vT, vE, vI, ok, fl, parity, o.T + start, o.E + start,
+                                   o.I + start);
     if (threadIdx.x == 0) o.cnt[w] = n;
 }
 
 hipError_t launch_pareto_tiles(const double *T, const double *E, const SegLayout &L,
-                               int64_t n_tiles_bound, const TileOut &o, int cpt, hipStream_t st)
+                               int64_t n_units_bound, const UnitOut &o, hipStream_t st)
 {
-    if (n_tiles_bound == 0) return hipSuccess;
-    const size_t lds = (size_t)o.nb * 8 + (size_t)L.tile * 20;
-    const dim3 grid((unsigned)n_tiles_bound), block(KR_BLOCK);
-    if (cpt == 8) hipLaunchKernelGGL(pareto_tile_kernel<8>, grid, block, lds, st, T, E, L, o);
-    else return hipErrorInvalidValue;
+    if (n_units_bound == 0) return hipSuccess;
+    const size_t lds = (size_t)KR_SURV_CAP * 20;
+    hipLaunchKernelGGL(pareto_tile_kernel, dim3((unsigned)n_units_bound), dim3(KR_BLOCK), lds, st,
+                       T, E, L, o);
     return hipGetLastError();
 }
 
-// Number of elements of staircase (bT, bE, bI)[0..n) that precede key (t, e, i).
+// Loads that bypass the CU's L1, for data this block wrote earlier in the same launch.
+__device__ __forceinline__ double ld_l2(const double *p)
+{
+    return bitsd(__hip_atomic_load((const uint64_t *)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
+__device__ __forceinline__ int32_t ld_l2(const int32_t *p)
+{
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint8_t ld_l2(const uint8_t *p)
+{
+    const uint32_t word = __hip_atomic_load((const uint32_t *)((uintptr_t)p & ~(uintptr_t)3),
+                                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return (uint8_t)(word >> (8 * ((uintptr_t)p & 3)));
+}
+
+// Rank of key (t, e, i) in the sorted staircase b[0..n): number of elements before it.
 __device__ __forceinline__ int rank_in(const double *bT, const double *bE, const int32_t *bI,
                                        int n, uint64_t t, uint64_t e, int32_t i)
 {
     int lo = 0, hi = n;
     while (lo < hi) {
         const int mid = (lo + hi) >> 1;
-        if (key_less(dbits(bT[mid]), dbits(bE[mid]), bI[mid], t, e, i)) lo = mid + 1;
-        else hi = mid;
+        if (key_less(dbits(ld_l2(bT + mid)), dbits(ld_l2(bE + mid)), ld_l2(bI + mid), t, e, i))
+            lo = mid + 1;
+        else
+            hi = mid;
     }
     return lo;
 }
 
-__global__ void __launch_bounds__(KR_BLOCK)
-merge_kernel(SegLayout L, int level, int64_t pairs_per_seg, PointBufs in, const int32_t *cnt_in,
-             PointBufs out, int32_t *cnt_out, uint8_t *flags)
+// Merge staircases a = in[sa, sa+na) and b = in[sb, sb+nb) into out[sa ...); returns
+// the merged frontier's size.  Every thread of the block must call.
+__device__ inline int merge_pair(const PointBufs &in, const PointBufs &out, uint8_t *flags,
+                                 int64_t sa, int na, int64_t sb, int nb)
 {
     __shared__ int32_t sc[KR_WAVES];
-    const int64_t w = blockIdx.x;
-    const int g = (int)(w / pairs_per_seg);
-    const int64_t q = w % pairs_per_seg;
-    if (g >= L.n_seg) return;
-    const int64_t tb = L.tile_base[g];
-    const int64_t nt = L.tile_base[g + 1] - tb;
-    const int64_t kA = q << (level + 1);
-    if (kA >= nt) return;
-    const int64_t kB = kA + ((int64_t)1 << level);
-    const int64_t sA = L.seg_off[g] + tile_start(L, kA);
-    const int nA = cnt_in[tb + kA];
-    if (kB >= nt) {  // no partner: carry the staircase over
-        for (int x = threadIdx.x; x < nA; x += KR_BLOCK) {
-            out.T[sA + x] = in.T[sA + x];
-            out.E[sA + x] = in.E[sA + x];
-            out.I[sA + x] = in.I[sA + x];
-        }
-        if (threadIdx.x == 0) cnt_out[tb + kA] = nA;
-        return;
-    }
-    const int64_t sB = L.seg_off[g] + tile_start(L, kB);
-    const int nB = cnt_in[tb + kB];
-    const double *aT = in.T + sA, *aE = in.E + sA, *bT = in.T + sB, *bE = in.E + sB;
-    const int32_t *aI = in.I + sA, *bI = in.I + sB;
-    // merged order, with a survival flag per element
-    for (int x = threadIdx.x; x < nA + nB; x += KR_BLOCK) {
-        const bool fromA = x < nA;
-        const int y = fromA ? x : x - nA;
-        const double t = fromA ? aT[y] : bT[y];
-        const double e = fromA ? aE[y] : bE[y];
-        const int32_t id = fromA ? aI[y] : bI[y];
-        const int r = fromA ? rank_in(bT, bE, bI, nB, dbits(t), dbits(e), id)
-                            : rank_in(aT, aE, aI, nA, dbits(t), dbits(e), id);
+    const double *aT = in.T + sa, *aE = in.E + sa, *bT = in.T + sb, *bE = in.E + sb;
+    const int32_t *aI = in.I + sa, *bI = in.I + sb;
+    for (int x = threadIdx.x; x < na + nb; x += KR_BLOCK) {
+        const bool fromA = x < na;
+        const int y = fromA ? x : x - na;
+        const double t = ld_l2(fromA ? aT + y : bT + y);
+        const double e = ld_l2(fromA ? aE + y : bE + y);
+        const int32_t id = ld_l2(fromA ? aI + y : bI + y);
+        const int r = fromA ? rank_in(bT, bE, bI, nb, dbits(t), dbits(e), id)
+                            : rank_in(aT, aE, aI, na, dbits(t), dbits(e), id);
         const double *oE = fromA ? bE : aE;
-        const bool alive = !(r > 0 && oE[r - 1] <= e);
-        const int64_t dst = sA + y + r;
+        const bool alive = !(r > 0 && ld_l2(oE + r - 1) <= e);
+        const int64_t dst = sa + y + r;
         out.T[dst] = t;
         out.E[dst] = e;
         out.I[dst] = id;
         flags[dst] = alive;
     }
     __syncthreads();
-    // stable in-place compaction of the survivors
-    const int n = nA + nB;
+    const int n = na + nb;
     int base = 0;
     for (int c0 = 0; c0 < n; c0 += KR_BLOCK) {
         const int x = c0 + threadIdx.x;
@@ -195,54 +185,169 @@ merge_kernel(SegLayout L, int level, int64_t pairs_per_seg, PointBufs in, const 
         int32_t id = 0;
         int f = 0;
         if (has) {
-            t = out.T[sA + x];
-            e = out.E[sA + x];
-            id = out.I[sA + x];
-            f = flags[sA + x];
+            t = ld_l2(out.T + sa + x);
+            e = ld_l2(out.E + sa + x);
+            id = ld_l2(out.I + sa + x);
+            f = ld_l2(flags + sa + x);
         }
         __syncthreads();
         int tot;
         const int pos = block_exclusive(f, 0, SumI32(), sc, &tot);
         if (has && f) {
-            out.T[sA + base + pos] = t;
-            out.E[sA + base + pos] = e;
-            out.I[sA + base + pos] = id;
+            out.T[sa + base + pos] = t;
+            out.E[sa + base + pos] = e;
+            out.I[sa + base + pos] = id;
         }
         base += tot;
         __syncthreads();
     }
-    if (threadIdx.x == 0) cnt_out[tb + kA] = base;
+    return base;
 }
 
-hipError_t launch_merge_level(const SegLayout &L, int level, int64_t max_tiles,
-                              const PointBufs &in, const int32_t *cnt_in, const PointBufs &out,
-                              int32_t *cnt_out, uint8_t *flags, hipStream_t st)
+struct FinLds {
+    uint64_t sT[KR_FIN_CAP], sE[KR_FIN_CAP];
+    int32_t sI[KR_FIN_CAP];
+    int32_t upre[KR_FIN_UNITS + 1];
+};
+
+// Union of a segment's unit frontiers -> the segment's frontier in `fin` at the
+// segment start; its size in fcnt[g].  `buf` holds the unit slots (and is free to be
+// overwritten once they are gathered).  One block per segment.
+__global__ void __launch_bounds__(KR_BLOCK)
+finalize_kernel(SegLayout L, PointBufs buf, const int32_t *ucnt, PointBufs fin, int32_t *fcnt,
+                int32_t *runcnt, uint8_t *flags)
 {
-    const int64_t span = (int64_t)1 << (level + 1);
-    const int64_t pairs = (max_tiles + span - 1) / span;
-    const int64_t blocks = pairs * L.n_seg;
-    if (blocks == 0) return hipSuccess;
-    hipLaunchKernelGGL(merge_kernel, dim3((unsigned)blocks), dim3(KR_BLOCK), 0, st, L, level,
-                       pairs, in, cnt_in, out, cnt_out, flags);
+    __shared__ FinLds sh;
+    __shared__ int32_t sc[KR_WAVES];
+    const int g = blockIdx.x;
+    const int64_t s0 = L.seg_off[g];
+    const int64_t u0 = L.unit_base[g];
+    const int nu = (int)(L.unit_base[g + 1] - u0);
+    // unit sizes and their running offsets
+    int64_t total = 0;
+    const bool small_units = nu <= KR_FIN_UNITS;
+    for (int c0 = 0; c0 < nu; c0 += KR_BLOCK) {
+        const int k = c0 + threadIdx.x;
+        const int n = k < nu ? ucnt[u0 + k] : 0;
+        int tot;
+        const int ex = block_exclusive(n, 0, SumI32(), sc, &tot);
+        if (small_units && k < nu) sh.upre[k] = (int)total + ex;
+        total += tot;
+    }
+    if (small_units && threadIdx.x == 0) sh.upre[nu] = (int)total;
+    __syncthreads();
+    if (small_units && total <= KR_FIN_CAP) {
+        const int n = (int)total;
+        for (int x = threadIdx.x; x < n; x += KR_BLOCK) {
+            int lo = 0, hi = nu - 1;  // unit holding element x
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (sh.upre[mid] <= x) lo = mid;
+                else hi = mid - 1;
+            }
+            const int64_t src = s0 + (int64_t)lo * L.unit_stride + (x - sh.upre[lo]);
+            sh.sT[x] = dbits(buf.T[src]);
+            sh.sE[x] = dbits(buf.E[src]);
+            sh.sI[x] = buf.I[src];
+        }
+        __syncthreads();
+        lds_sort_keys(sh.sT, sh.sE, sh.sI, n);
+        const int cnt = lds_frontier_scan(sh.sT, sh.sE, sh.sI, n, fin.T + s0, fin.E + s0, fin.I + s0);
+        if (threadIdx.x == 0) fcnt[g] = cnt;
+        return;
+    }
+    // Large union: gather contiguously into fin, reduce LDS-sized chunks in place,
+    // then merge the chunk staircases pairwise (fin <-> buf).
+    int64_t pre = 0;
+    for (int k = 0; k < nu; ++k) {
+        const int n = ld_l2(ucnt + u0 + k);
+        const int64_t src = s0 + (int64_t)k * L.unit_stride;
+        for (int x = threadIdx.x; x < n; x += KR_BLOCK) {
+            fin.T[s0 + pre + x] = buf.T[src + x];
+            fin.E[s0 + pre + x] = buf.E[src + x];
+            fin.I[s0 + pre + x] = buf.I[src + x];
+        }
+        pre += n;
+    }
+    __syncthreads();
+    int32_t *rc = runcnt + s0 / KR_FIN_CAP + g;
+    const int nchunks = (int)((total + KR_FIN_CAP - 1) / KR_FIN_CAP);
+    for (int c = 0; c < nchunks; ++c) {
+        const int64_t c0 = (int64_t)c * KR_FIN_CAP;
+        const int n = (int)min((int64_t)KR_FIN_CAP, total - c0);
+        for (int x = threadIdx.x; x < n; x += KR_BLOCK) {
+            sh.sT[x] = dbits(ld_l2(fin.T + s0 + c0 + x));
+            sh.sE[x] = dbits(ld_l2(fin.E + s0 + c0 + x));
+            sh.sI[x] = ld_l2(fin.I + s0 + c0 + x);
+        }
+        __syncthreads();
+        lds_sort_keys(sh.sT, sh.sE, sh.sI, n);
+        const int cnt = lds_frontier_scan(sh.sT, sh.sE, sh.sI, n, fin.T + s0 + c0, fin.E + s0 + c0,
+                                          fin.I + s0 + c0);
+        if (threadIdx.x == 0) rc[c] = cnt;
+        __syncthreads();
+    }
+    PointBufs cur = fin, other = buf;
+    for (int span = 1; span < nchunks; span <<= 1) {
+        for (int r = 0; r < nchunks; r += 2 * span) {
+            const int64_t sa = s0 + (int64_t)r * KR_FIN_CAP;
+            const int na = ld_l2(rc + r);
+            int merged;
+            if (r + span < nchunks) {
+                const int64_t sb = s0 + (int64_t)(r + span) * KR_FIN_CAP;
+                merged = merge_pair(cur, other, flags, sa, na, sb, ld_l2(rc + r + span));
+            } else {
+                for (int x = threadIdx.x; x < na; x += KR_BLOCK) {
+                    other.T[sa + x] = ld_l2(cur.T + sa + x);
+                    other.E[sa + x] = ld_l2(cur.E + sa + x);
+                    other.I[sa + x] = ld_l2(cur.I + sa + x);
+                }
+                merged = na;
+            }
+            __syncthreads();
+            if (threadIdx.x == 0) rc[r] = merged;
+            __syncthreads();
+        }
+        const PointBufs t = cur;
+        cur = other;
+        other = t;
+    }
+    const int n = nchunks > 0 ? ld_l2(rc) : 0;
+    if (cur.T != fin.T) {
+        for (int x = threadIdx.x; x < n; x += KR_BLOCK) {
+            fin.T[s0 + x] = ld_l2(cur.T + s0 + x);
+            fin.E[s0 + x] = ld_l2(cur.E + s0 + x);
+            fin.I[s0 + x] = ld_l2(cur.I + s0 + x);
+        }
+    }
+    if (threadIdx.x == 0) fcnt[g] = n;
+}
+
+hipError_t launch_finalize(const SegLayout &L, const PointBufs &buf, const int32_t *ucnt,
+                           const PointBufs &fin, int32_t *fcnt, int32_t *runcnt, uint8_t *flags,
+                           hipStream_t st)
+{
+    if (L.n_seg == 0) return hipSuccess;
+    hipLaunchKernelGGL(finalize_kernel, dim3(L.n_seg), dim3(KR_BLOCK), 0, st, L, buf, ucnt, fin,
+                       fcnt, runcnt, flags);
     return hipGetLastError();
 }
 
 // out_off = exclusive prefix sum of the per-segment frontier sizes; one block.
 __global__ void __launch_bounds__(KR_BLOCK)
-count_scan_kernel(SegLayout L, const int32_t *cnt, int64_t *out_off)
+count_scan_kernel(int n_seg, const int32_t *fcnt, int64_t *out_off)
 {
     __shared__ int64_t sc[KR_WAVES];
     int64_t carry = 0;
-    for (int g0 = 0; g0 < L.n_seg; g0 += KR_BLOCK) {
+    for (int g0 = 0; g0 < n_seg; g0 += KR_BLOCK) {
         const int g = g0 + threadIdx.x;
-        int64_t c = 0;
-        if (g < L.n_seg && L.tile_base[g + 1] > L.tile_base[g]) c = cnt[L.tile_base[g]];
+        const int64_t c = g < n_seg ? fcnt[g] : 0;
         int64_t tot;
         const int64_t ex = block_exclusive(c, (int64_t)0, SumI64(), sc, &tot);
-        if (g < L.n_seg) out_off[g] = carry + ex;
+        if (g < n_seg) out_off[g] = carry + ex;
         carry += tot;
     }
-    if (threadIdx.x == 0) out_off[L.n_seg] = carry;
+    if (threadIdx.x == 0) out_off[n_seg] = carry;
 }
 
 __global__ void __launch_bounds__(KR_BLOCK)
@@ -261,11 +366,11 @@ copy_out_kernel(SegLayout L, PointBufs fin, const int64_t *out_off, int64_t cap,
     }
 }
 
-hipError_t launch_finish(const SegLayout &L, const PointBufs &fin, const int32_t *cnt,
+hipError_t launch_output(const SegLayout &L, const PointBufs &fin, const int32_t *fcnt,
                          int64_t cap, int64_t *out_off, int32_t *out_idx, double *out_T,
                          double *out_E, hipStream_t st)
 {
-    hipLaunchKernelGGL(count_scan_kernel, dim3(1), dim3(KR_BLOCK), 0, st, L, cnt, out_off);
+    hipLaunchKernelGGL(count_scan_kernel, dim3(1), dim3(KR_BLOCK), 0, st, L.n_seg, fcnt, out_off);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || L.n_seg == 0) return e;
     hipLaunchKernelGGL(copy_out_kernel, dim3(L.n_seg), dim3(KR_BLOCK), 0, st, L, fin, out_off, cap,

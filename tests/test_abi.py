@@ -61,7 +61,7 @@ def test_host_validation_without_gpu():
                                    null) == b.KR_EUNSUPPORTED
     assert L.kr_evaluate_and_filter_workspace(ctypes.byref(huge)) == 0
     # workspace sizes grow with the problem
-    assert L.kr_pareto_filter_workspace(10, 1, 10) < L.kr_pareto_filter_workspace(10 ** 6, 8, 10 ** 6)
+    assert L.kr_pareto_filter_workspace(10, 1) < L.kr_pareto_filter_workspace(10 ** 6, 8)
     assert L.kr_compose_frontiers_workspace(4, 1024) < L.kr_compose_frontiers_workspace(512, 65536)
     assert L.kr_compose_frontiers_workspace(0, 1024) == 0
     # too small a workspace is refused on the host

@@ -346,3 +346,50 @@ def test_deterministic(kr, config4):
     F1, bp1 = c1.F.clone(), c1.bp.clone()
     c2 = kr.compose_frontiers(off, T, E, 65536)
     assert torch.equal(F1, c2.F) and torch.equal(bp1, c2.bp)
+
+
+def test_adversarial_frontiers(kr, oracle_lib):
+    """Comm time dominating and comm energy falling steeply with comm time: almost every
+    candidate beats the fastest one's energy (more survivors than the on-chip list
+    holds) and the frontiers run to thousands of points (more than the finalize step
+    sorts on chip), so every fallback path runs."""
+    space = I.Space(2, 4, 1, 5, tuple(range(1, 65)), tuple(1005.0 + 15.0 * j for j in range(64)),
+                    p_static=0.0)
+    tab = I.make_tables(space, seed=21, comm_bytes=(4e6, 64e6))
+    F, S = space.n_freq, space.n_sm
+    tc = 10.0 + 1e-3 * np.arange(F * S, dtype=np.float64).reshape(F, S)
+    tab["tc"] = np.broadcast_to(tc[None, :, None, :], tab["tc"].shape).copy()
+    tab["pc"] = np.broadcast_to((1e6 / tc ** 2)[None, :, None, :], tab["pc"].shape).copy()
+    d = [torch.from_numpy(tab[k]).cuda() for k in ("t", "pw", "tc", "pc")]
+    fr = kr.evaluate_and_filter(space, *d)
+    T, E = kr.evaluate_partition(space, *d)
+    seg = np.arange(space.n_parts + 1, dtype=np.int64) * space.n_cand
+    un = kr.pareto_filter(T, E, seg)
+    sizes = []
+    for p in range(space.n_parts):
+        Tr, Er = oracle_lib.evaluate_partition(space, tab["t"], tab["pw"], tab["tc"], tab["pc"], p)
+        ix = oracle_lib.pareto(Tr, Er)
+        sizes.append(len(ix))
+        check_frontier(fr, p, (ix, Tr[ix], Er[ix]), "fused part %d" % p)
+        check_frontier(un, p, (ix, Tr[ix], Er[ix]), "unfused part %d" % p)
+    assert min(sizes) > 2560
+
+
+@pytest.mark.parametrize("n", [300, 2048, 20000, 9000, 30000])
+def test_pareto_filter_union_paths(kr, oracle_lib, n):
+    """One segment: small unions are sorted on chip; unions larger than the on-chip
+    capacity (the sorted staircase, every point kept) go through the chunked merge."""
+    rng = np.random.default_rng(n)
+    if n in (9000, 30000):
+        T = np.arange(n, dtype=np.float64) + 1.0
+        E = 1e5 - np.arange(n, dtype=np.float64)
+        if n == 30000:
+            perm = rng.permutation(n)
+            T, E = T[perm], E[perm]
+    else:
+        T = rng.lognormal(size=n)
+        E = 1.0 / T + rng.random(n)
+    seg = np.array([0, n], dtype=np.int64)
+    fr = kr.pareto_filter(torch.from_numpy(T).cuda(), torch.from_numpy(E).cuda(), seg)
+    ix = oracle_lib.pareto(T, E)
+    check_frontier(fr, 0, (ix, T[ix], E[ix]), "n=%d" % n)
