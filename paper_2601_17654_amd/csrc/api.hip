@@ -15,6 +15,7 @@ constexpr size_t kLdsBudget = 65536;
 constexpr size_t kLdsPerCu = 160 * 1024;
 constexpr int kSurvDoubles = KR_SURV_CAP * 20 / 8;
 constexpr size_t kAlign = 256;
+constexpr int64_t kWaveBlocksPerSlot = 4;
 
 // Bump allocator over the caller's workspace (or a size query when base == nullptr).
 struct Carve {
@@ -46,6 +47,34 @@ int64_t cand_per_freq(const kr_space *s)
     return npp * S * S;
 }
 
+// One comm kernel and at most 64 SM choices: one wave per slab.  Lane (h, s) takes SM
+// choice s and positions [h*span, (h+1)*span), R of them per register chunk.
+bool wave_plan(EvalArgs *a)
+{
+    if (a->M != 1 || a->S > 64) return false;
+    const int64_t rows = (int64_t)(a->N + KR_PAD) * (a->S + 1);  // slab and pad rows
+    const int64_t rows16 = (rows + 1) / 2 * 2;  // keeps the second table 16-byte aligned
+    const int64_t lds = 2 * rows16 + 4 * (a->N + 2);  // t, pw, all-SM column records
+    if ((size_t)lds * 8 > kLdsBudget) return false;
+    a->wave = 1;
+    a->w_pw = (int)rows16;
+    a->w_a0 = (int)(2 * rows16);
+    a->lds_doubles = (int)lds;
+    a->H = 64 / a->S;
+    a->span = (a->n_pos + a->H - 1) / a->H;
+    a->R = a->span <= 2 ? 2 : a->span <= 4 ? 4 : a->span <= 8 ? 8 : 17;
+    a->nch = (a->span + a->R - 1) / a->R;
+    // a few times more one-wave blocks than fit on the chip at once, so the
+    // dispatcher balances uneven slabs; within a block slab copies overlap the filter
+    const int64_t resident = std::max<int64_t>(1, std::min<int64_t>(16, kLdsPerCu / (lds * 8)));
+    const int64_t target = kWaveBlocksPerSlot * 256 * resident;
+    int64_t nfb = std::max<int64_t>(1, (target + a->P - 1) / a->P);
+    nfb = std::min<int64_t>(nfb, a->F);
+    a->fb = (int)((a->F + nfb - 1) / nfb);
+    a->nfb = (a->F + a->fb - 1) / a->fb;
+    return true;
+}
+
 // Shape of the evaluation launch; false if the slab does not fit on chip.
 bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)
 {
@@ -63,6 +92,7 @@ bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)
     a->C = cf * s->n_freq;
     a->p_static = s->p_static;
     const int64_t S1 = a->S + 1;
+    if (fused && wave_plan(a)) return true;
     const int64_t staged = 2 * a->N * S1 + 2 * a->M * a->S;  // t, pw, tc, pc
     const int64_t sums = 2 * (a->N + 1) * S1;
     const int64_t pairs = a->M == 2 ? (a->n_pp * 4 + 7) / 8 : 0;
@@ -241,8 +271,11 @@ kr_status kr_evaluate_and_filter(const kr_space *space, const double *t, const d
     if (launch_uniform_layout(w.seg_off, w.unit_base, a.P, a.C, a.nfb, st) != hipSuccess)
         return KR_EHIP;
     UnitOut o{w.buf[0].T, w.buf[0].E, w.buf[0].I, w.ucnt};
+    a.dma16 = a.wave && (a.N * (a.S + 1)) % 2 == 0 && (uintptr_t)t % 16 == 0 &&
+              (uintptr_t)pw % 16 == 0;
     phase_mark(KR_PHASE_EVAL_TILE, 0, st);
-    if (launch_eval_filter(a, o, st) != hipSuccess) return KR_EHIP;
+    if ((a.wave ? launch_eval_filter_wave(a, o, st) : launch_eval_filter(a, o, st)) != hipSuccess)
+        return KR_EHIP;
     phase_mark(KR_PHASE_EVAL_TILE, 1, st);
     SegLayout L;
     L.seg_off = w.seg_off;

@@ -7,6 +7,7 @@
 #define KR_FIN_CAP 2560    // points the finalize kernel sorts in LDS
 #define KR_FIN_UNITS 2048  // units per segment the finalize kernel's LDS path takes
 #define KR_TILE 2048       // points per tile of the stand-alone filter
+#define KR_PAD 4           // rows the wave kernel's end-cursor search reads per step
 
 namespace kr {
 
@@ -25,6 +26,12 @@ struct EvalArgs {
     int nchunk, cpt;        // position runs per tile / positions (or candidates) per thread
     int ntiles, tile;       // tiles per frequency; candidates per tile (generic mapping)
     int pf;                 // doubles per thread and table of the register prefetch
+    // one wave per slab (one comm kernel, at most 64 SM choices)
+    int wave;               // use the wave kernel
+    int H, span;            // position runs per SM choice, positions per run
+    int R, nch;             // positions per chunk (registers), chunks per run
+    int w_pw, w_a0;         // LDS offsets (doubles) of the power slab and the column sums
+    int dma16;              // 16-byte direct copies (slab length even, tables 16-byte aligned)
 };
 
 // Per-unit frontiers written by the fused kernel or the tile kernel.
@@ -57,6 +64,7 @@ struct PointBufs {
 
 hipError_t launch_eval(const EvalArgs &a, hipStream_t st);
 hipError_t launch_eval_filter(const EvalArgs &a, const UnitOut &o, hipStream_t st);
+hipError_t launch_eval_filter_wave(const EvalArgs &a, const UnitOut &o, hipStream_t st);
 hipError_t launch_decode(const DecodeArgs &d, hipStream_t st);
 
 // pareto.hip
