@@ -33,7 +33,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 FP64_VECTOR_TFLOPS = 78.6
 COUNTERS = os.path.join(ROOT, "profiles", "eval_filter_counters_eval_stress.txt")
-KERNEL_SOURCES = ["eval.hip", "kr_filter.h", "kr_device.h", "kr_launch.h"]
+KERNEL_SOURCES = ["eval_wave.hip", "kr_filter.h", "kr_device.h", "kr_launch.h", "api.hip"]
 METRIC = "schedule candidates evaluated+filtered/sec and frontier cells/sec on 1 MI355X"
 
 
@@ -169,7 +169,7 @@ def main():
     traffic, tsrc = read_traffic(table_bytes)
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-            "kernel": "eval_filter_kernel (fused evaluation + tile frontier)",
+            "kernel": "eval_filter_wave_kernel (fused evaluation + frontier, one wave per slab)",
             "kernel_ms": round(kern_ms, 4), "algorithmic_bytes": table_bytes,
             "traffic_source": tsrc}
 

@@ -15,7 +15,7 @@ constexpr size_t kLdsBudget = 65536;
 constexpr size_t kLdsPerCu = 160 * 1024;
 constexpr int kSurvDoubles = KR_SURV_CAP * 20 / 8;
 constexpr size_t kAlign = 256;
-constexpr int64_t kWaveBlocksPerSlot = 4;
+constexpr int64_t kWaveBlocksPerSlot = 32;
 
 // Bump allocator over the caller's workspace (or a size query when base == nullptr).
 struct Carve {
@@ -48,22 +48,29 @@ int64_t cand_per_freq(const kr_space *s)
 }
 
 // One comm kernel and at most 64 SM choices: one wave per slab.  Lane (h, s) takes SM
-// choice s and positions [h*span, (h+1)*span), R of them per register chunk.
+// choice s and the h-th run of launch positions, R of them per register chunk.
 bool wave_plan(EvalArgs *a)
 {
     if (a->M != 1 || a->S > 64) return false;
     const int64_t rows = (int64_t)(a->N + KR_PAD) * (a->S + 1);  // slab and pad rows
     const int64_t rows16 = (rows + 1) / 2 * 2;  // keeps the second table 16-byte aligned
-    const int64_t lds = 2 * rows16 + 4 * (a->N + 2);  // t, pw, all-SM column records
+    const int64_t lds = 2 * rows16 + 2 * (a->N + 2);  // t, pw, all-SM column sums
     if ((size_t)lds * 8 > kLdsBudget) return false;
     a->wave = 1;
     a->w_pw = (int)rows16;
     a->w_a0 = (int)(2 * rows16);
     a->lds_doubles = (int)lds;
+    // runs of span positions, a multiple of 8 when there are several (the running-sum
+    // pass keeps a lane's starting sums at 8-row block boundaries); the last run takes
+    // the rest
     a->H = 64 / a->S;
-    a->span = (a->n_pos + a->H - 1) / a->H;
-    a->R = a->span <= 2 ? 2 : a->span <= 4 ? 4 : a->span <= 8 ? 8 : 17;
-    a->nch = (a->span + a->R - 1) / a->R;
+    a->span = a->H == 1 ? a->n_pos : std::max(8, a->n_pos / a->H / 8 * 8);
+    const int last = std::max(0, a->n_pos - (a->H - 1) * a->span);
+    const int maxrun = std::max(std::min(a->span, a->n_pos), last);
+    a->R = maxrun <= 2 ? 2 : maxrun <= 4 ? 4 : maxrun <= 8 ? 8 : 17;
+    a->nch = (maxrun + a->R - 1) / a->R;
+    // filter scratch: pad rows of each table and the column-sum area below record N + 1
+    a->wcap = (int)std::min<int64_t>(64, std::min<int64_t>(KR_PAD * (a->S + 1), 4 * (a->N + 1)));
     // a few times more one-wave blocks than fit on the chip at once, so the
     // dispatcher balances uneven slabs; within a block slab copies overlap the filter
     const int64_t resident = std::max<int64_t>(1, std::min<int64_t>(16, kLdsPerCu / (lds * 8)));

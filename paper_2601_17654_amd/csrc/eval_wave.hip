@@ -41,6 +41,15 @@ __device__ __forceinline__ void wave_lds_fence()
 // the inputs of every unrolled round alive at once).
 __device__ __forceinline__ void pin(double &x) { asm volatile("" : "+v"(x)); }
 
+// Minimum of two non-NaN doubles in one instruction (the compiler's fmin adds operand
+// canonicalisation it cannot prove unnecessary here).
+__device__ __forceinline__ double vmin(double a, double b)
+{
+    double r;
+    asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+
 // s_waitcnt encodings (gfx9): vmcnt [3:0]+[15:14], expcnt [6:4], lgkmcnt [11:8].
 #define KR_WAIT_VM0 0x0F70
 #define KR_WAIT_LGKM0 0xC07F
@@ -64,6 +73,52 @@ __device__ __forceinline__ void copy_to_lds(const double *g, double *l, int n)
                 __builtin_amdgcn_global_load_lds(src, dst, 4, 0, 0);
         }
     }
+}
+
+__device__ __forceinline__ void emit(const Key &k, int n, double *oT, double *oE, int32_t *oI)
+{
+    if (threadIdx.x == 0) {
+        oT[n] = bitsd(k.t);
+        oE[n] = bitsd(k.e);
+        oI[n] = k.i;
+    }
+}
+
+// One DPP step of a wave minimum over doubles (rows not written keep their own value).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_min_f64(double x)
+{
+    const uint64_t b = dbits(x);
+    const uint32_t lo = (uint32_t)b, hi = (uint32_t)(b >> 32);
+    uint32_t ylo, yhi;
+    if constexpr (ROWS == 0xF) {  // every lane reads a lane of its own row
+        ylo = __builtin_amdgcn_mov_dpp(lo, CTRL, 0xF, 0xF, false);
+        yhi = __builtin_amdgcn_mov_dpp(hi, CTRL, 0xF, 0xF, false);
+    } else {  // rows outside ROWS keep their own value
+        ylo = __builtin_amdgcn_update_dpp(lo, lo, CTRL, ROWS, 0xF, false);
+        yhi = __builtin_amdgcn_update_dpp(hi, hi, CTRL, ROWS, 0xF, false);
+    }
+    return vmin(bitsd(((uint64_t)yhi << 32) | ylo), x);
+}
+
+// Minima over the wave of two non-negative doubles (same DPP pattern as wave_min_u64),
+// interleaved; results uniform.
+__device__ __forceinline__ void wave_min2_f64(double &x, double &y)
+{
+    x = dpp_min_f64<0xB1, 0xF>(x);
+    y = dpp_min_f64<0xB1, 0xF>(y);
+    x = dpp_min_f64<0x4E, 0xF>(x);
+    y = dpp_min_f64<0x4E, 0xF>(y);
+    x = dpp_min_f64<0x141, 0xF>(x);
+    y = dpp_min_f64<0x141, 0xF>(y);
+    x = dpp_min_f64<0x140, 0xF>(x);
+    y = dpp_min_f64<0x140, 0xF>(y);
+    x = dpp_min_f64<0x142, 0xA>(x);
+    y = dpp_min_f64<0x142, 0xA>(y);
+    x = dpp_min_f64<0x143, 0xC>(x);
+    y = dpp_min_f64<0x143, 0xC>(y);
+    x = bitsd(lane_u64(dbits(x), 63));
+    y = bitsd(lane_u64(dbits(y), 63));
 }
 
 // Least (T, E, index) candidate among those with pred(r) true.  Fast path when exactly
@@ -95,78 +150,135 @@ __device__ __forceinline__ Key chunk_pick(const double (&vT)[R], const double (&
     return wave_min_key(loc);
 }
 
-__device__ __forceinline__ void emit(const Key &k, int n, double *oT, double *oE, int32_t *oI)
-{
-    if (threadIdx.x == 0) {
-        oT[n] = bitsd(k.t);
-        oE[n] = bitsd(k.e);
-        oI[n] = k.i;
-    }
-}
+// LDS scratch of the filter: room for `cap` candidates (T, E, index).
+struct Scratch {
+    double *T, *E;
+    int32_t *I;
+    int cap;
+};
 
 // Frontier of the wave's chunk (invalid slots hold T = E = +inf; valid ones are
-// finite).  Candidate index of slot r of a lane is ibase + r * S.  Writes the frontier
-// in ascending T to o*[0 .. n) and returns n (uniform).
+// finite); tl, el are each lane's least T and E.  Candidate index of slot r of a lane
+// is ibase + r * S.  Writes the frontier in ascending T to o*[0 .. n) and returns n
+// (uniform).
+//
+// A (least in (T, E, index) order) and Z (least in (E, T, index) order) come from wave
+// minima and ballots over the slots.  Every other kept point lies strictly inside their box
+// (T < T_Z, E < E_A), and only box members can beat a box member, so the box is
+// gathered one candidate per lane and each keeps itself iff no other member precedes
+// it with energy at or below its own; kept points are placed by their rank in T.  A
+// box larger than the scratch takes repeated wave minima instead (same result).
 template <int R>
-__device__ inline int wave_frontier(const double (&vT)[R], const double (&vE)[R], int ibase, int S,
-                                    double *oT, double *oE, int32_t *oI)
+__device__ inline int wave_frontier(const double (&vT)[R], const double (&vE)[R], double tl,
+                                    double el, int ibase, int S, const Scratch &sc, double *oT,
+                                    double *oE, int32_t *oI)
 {
-    double tl = INFINITY, el = INFINITY;
+    const int lane = threadIdx.x;
+    wave_min2_f64(tl, el);
+    const uint64_t tab = dbits(tl), ezb = dbits(el);
+    if (tab >= KR_INF_BITS) return 0;  // no valid candidate
+    const Key A = chunk_pick<R>(vT, vE, ibase, S, [&](int r) { return dbits(vT[r]) == tab; });
+    const double TA = bitsd(A.t), EA = bitsd(A.e), EZ = el;
+    const int32_t iA = A.i;
+    const bool single = A.e == ezb;  // A has the least energy too: A is Z, nothing beats it
+    int nkeep = 0;                   // kept points strictly inside the box
+    if (!single) {
+        const Key Z = chunk_pick<R>(vT, vE, ibase, S, [&](int r) { return dbits(vE[r]) == ezb; });
+        const double TZ = bitsd(Z.t);
+        const int32_t iZ = Z.i;
+        uint32_t rows = 0;
+        int tot = 0;
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-        tl = vT[r] < tl ? vT[r] : tl;
-        el = vE[r] < el ? vE[r] : el;
-    }
-    const uint64_t TA = wave_min_u64(dbits(tl));
-    if (TA == KR_INF_BITS) return 0;
-    const uint64_t EZ = wave_min_u64(dbits(el));
-    const Key A = chunk_pick<R>(vT, vE, ibase, S, [&](int r) { return dbits(vT[r]) == TA; });
-    emit(A, 0, oT, oE, oI);
-    if (A.e == EZ) return 1;  // A has the least energy too: nothing beats it
-    const Key Z = chunk_pick<R>(vT, vE, ibase, S, [&](int r) { return dbits(vE[r]) == EZ; });
-    // candidates strictly inside the box of A and Z
-    uint32_t rows = 0;
-    int nbox = 0;
-    Key one = key_none();
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const uint64_t m = __ballot(dbits(vT[r]) < Z.t && dbits(vE[r]) < A.e);
-        if (m) {
-            rows |= 1u << r;
-            nbox += __popcll(m);
-            const int L = __ffsll((long long)m) - 1;
-            one = Key{lane_u64(dbits(vT[r]), L), lane_u64(dbits(vE[r]), L),
-                      lane_i32(ibase, L) + r * S};
+        for (int r = 0; r < R; ++r) {
+            const uint64_t m = __ballot(vT[r] < TZ && vE[r] < EA);
+            tot += __popcll(m);
+            rows |= (m != 0 ? 1u : 0u) << r;
         }
-    }
-    int n = 1;
-    if (nbox == 1) {
-        emit(one, n++, oT, oE, oI);  // lies below A's energy and before Z: kept
-    } else if (nbox > 1) {
-        uint64_t bound = A.e;
-        for (;;) {
-            Key loc = key_none();
+        if (tot > 0 && tot <= sc.cap) {
+            int base = 0;
 #pragma unroll
             for (int r = 0; r < R; ++r)
                 if (rows >> r & 1u) {
-                    const Key c{dbits(vT[r]), dbits(vE[r]), ibase + r * S};
-                    if (c.t < Z.t && c.e < bound && kless(c, loc)) loc = c;
+                    const bool b = vT[r] < TZ && vE[r] < EA;
+                    const uint64_t m = __ballot(b);
+                    if (b) {
+                        const int q = base + (int)__builtin_amdgcn_mbcnt_hi(
+                                                   (uint32_t)(m >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+                        sc.T[q] = vT[r];
+                        sc.E[q] = vE[r];
+                        sc.I[q] = ibase + r * S;
+                    }
+                    base += __popcll(m);
                 }
-            const Key w = wave_min_key(loc);
-            if (w.t == KR_INF_BITS) break;
-            emit(w, n++, oT, oE, oI);
-            bound = w.e;
+            wave_lds_fence();
+            const bool mine = lane < tot;
+            const int q = min(lane, tot - 1);
+            const double xT = sc.T[q], xE = sc.E[q];
+            const int32_t xI = sc.I[q];
+            bool dom = false;
+            for (int y = 0; y < tot; ++y) {
+                const double yT = bitsd(lane_u64(dbits(xT), y));
+                const double yE = bitsd(lane_u64(dbits(xE), y));
+                const int32_t yI = lane_i32(xI, y);
+                const bool before = yT < xT || (yT == xT && (yE < xE || (yE == xE && yI < xI)));
+                dom = dom || (before && yE <= xE);
+            }
+            const bool kept = mine && !dom;
+            uint64_t km = __ballot(kept);
+            nkeep = __popcll(km);
+            int rank = 0;  // kept points are strictly ordered in T
+            while (km) {
+                const int y = __ffsll((long long)km) - 1;
+                km &= km - 1;
+                rank += bitsd(lane_u64(dbits(xT), y)) < xT ? 1 : 0;
+            }
+            if (kept) {
+                oT[1 + rank] = xT;
+                oE[1 + rank] = xE;
+                oI[1 + rank] = xI;
+            }
+            wave_lds_fence();
+            if (mine) {  // give the pad rows back
+                sc.T[lane] = INFINITY;
+                sc.E[lane] = 0.0;
+            }
+        } else if (tot > 0) {
+            uint64_t bound = dbits(EA);
+            const uint64_t zt = dbits(TZ);
+            for (;;) {
+                Key loc = key_none();
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    if (rows >> r & 1u) {
+                        const Key c{dbits(vT[r]), dbits(vE[r]), ibase + r * S};
+                        if (c.t < zt && c.e < bound && kless(c, loc)) loc = c;
+                    }
+                const Key w = wave_min_key(loc);
+                if (w.t == KR_INF_BITS) break;
+                ++nkeep;
+                emit(w, nkeep, oT, oE, oI);
+                bound = w.e;
+            }
+        }
+        if (lane == 1) {
+            oT[1 + nkeep] = TZ;
+            oE[1 + nkeep] = EZ;
+            oI[1 + nkeep] = iZ;
         }
     }
-    emit(Z, n++, oT, oE, oI);
-    return n;
+    if (lane == 0) {
+        oT[0] = TA;
+        oE[0] = EA;
+        oI[0] = iA;
+    }
+    return single ? 1 : nkeep + 2;
 }
 
-// All-SM column record of row i: the running sums before row i and the row's own
-// entries.  Record N holds the totals (and zeros).
+// All-SM column running sums before row i: A0[i], B0[i].  Record N holds the totals;
+// record N + 1 is zeros.
 struct alignas(16) ColRec {
-    double a, b;  // A0[i], B0[i]
-    double t, w;  // t[i][0], pw[i][0]
+    double a, b;
 };
 
 // What a round leaves for its tail, which runs one round later so that the loads it
@@ -178,32 +290,27 @@ struct Tail {
     double rem;       // comm time left when compute reaches kernel j
     double tau;       // A0[p] + comm time
     double tj, wj;    // t[j][sg], pw[j][sg]
-    ColRec cj;        // record j
-    double c1a, c1b;  // sums of record j + 1
+    double t0, w0;    // t[j][0], pw[j][0]
+    ColRec cj, c1;    // records j and j + 1
 };
 
 // Rest of the walk after the comm kernel (compute back in the all-SM state), written
-// without branches; results of invalid rounds are +inf.
-__device__ __forceinline__ void finish_tail(const Tail &q, int N, double p_static, double ctail,
+// without branches.  When the comm kernel outlasts compute (j == N) the same lines
+// give T = tau and E_c = ec exactly: row N is a pad row (t = +inf, pw = 0), so w = 1,
+// nothing is added but +0, and record N holds the totals.  Invalid rounds give +inf.
+__device__ __forceinline__ void finish_tail(const Tail &q, double p_static, double ctail,
                                             double a0, double b0, double &T_out, double &E_out)
 {
-    // comm ends inside kernel j: finish kernel j's remaining fraction, then the rest
     double Ec = q.ec + q.wj * q.rem;
-    double w = 1.0 - q.rem / q.tj;
-    w = w < 0.0 ? 0.0 : w;
-    const bool part = w < 1.0;
-    const double need = w * q.cj.t;
-    const double Ecp = Ec + q.cj.w * need;
+    const double w = __builtin_fmax(1.0 - q.rem / q.tj, 0.0);
+    const bool part = w < 1.0;  // kernel j is left partly done: finish it in state 0
+    const double need = w * q.t0;
     const double used = part ? need : 0.0;
-    Ec = part ? Ecp : Ec;
-    const double Ai = part ? q.c1a : q.cj.a, Bi = part ? q.c1b : q.cj.b;
+    Ec = Ec + q.w0 * used;
+    const double Ai = part ? q.c1.a : q.cj.a, Bi = part ? q.c1.b : q.cj.b;
     Ec = Ec + (b0 - Bi);
     const double el = used + (a0 - Ai);
-    const double Tin = q.tau + el;
-    // j == N: compute finished while the comm kernel ran
-    const bool over = q.j == N;
-    const double T = over ? q.tau : Tin;
-    Ec = over ? q.ec : Ec;
+    const double T = q.tau + el;
     double E = p_static * T;
     E = E + Ec;
     E = E + ctail;
@@ -212,14 +319,18 @@ __device__ __forceinline__ void finish_tail(const Tail &q, int N, double p_stati
 }
 
 // Block (p, b): one wave, partition p, frequencies [b*fb, min(F, (b+1)*fb)).  LDS:
-// t slab [N + KR_PAD][S1] at 0, pw slab (same shape) at w_pw, all-SM column records
+// t slab [N + KR_PAD][S1] at 0, pw slab (same shape) at w_pw, all-SM column sums
 // [N + 2] at w_a0.  The pad rows hold t = +inf (pw = 0), so an end-cursor search that
-// runs past the last kernel stops by itself; the last record is zeros.  SC > 0 fixes the
-// number of SM choices at compile time (row offsets become immediates).
-// Rounds: round r of a chunk evaluates position c0 + r of every lane.  Its end-kernel
-// search reads a batch of K rows loaded one round earlier; the loads for its tail and
-// for the next round are issued right after the search, and the previous round's tail
-// is finished while they are in flight.
+// runs past the last kernel stops by itself.  SC > 0 fixes the number of SM choices at
+// compile time (row offsets become immediates).
+//
+// Lane (h, s) takes positions [plo, phi): runs of `span` positions (a multiple of 8
+// when there are several runs), the last run taking the rest.  Round r of a chunk
+// evaluates position c0 + r of every lane.  Its end-cursor search reads a batch of K
+// rows loaded one round earlier; the loads for its tail and for the next round are
+// issued right after the search, and the previous round's tail is finished while they
+// are in flight.  Cursors of a lane past its last position keep moving (their results
+// are discarded); only their LDS addresses are clamped.
 template <int R, int W, int SC>
 __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOut o)
 {
@@ -232,20 +343,25 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
     const int p = blockIdx.x / a.nfb, fbk = blockIdx.x - p * a.nfb;
     const int f0 = fbk * a.fb, f1 = min(a.F, f0 + a.fb);
     const int s = lane % S, h = lane / S, sg = s + 1;
-    const int plo = h < a.H ? min(a.n_pos, h * a.span) : 0;
-    const int phi = h < a.H ? min(a.n_pos, plo + a.span) : 0;
+    const bool on = h < a.H;
+    const int plo = on ? min(a.n_pos, h * a.span) : 0;
+    const int phi = on ? (h == a.H - 1 ? a.n_pos : min(a.n_pos, plo + a.span)) : 0;
     const size_t slot0 = (size_t)p * a.C + (size_t)f0 * a.Cf;
     double *oT = o.T + slot0, *oE = o.E + slot0;
     int32_t *oI = o.I + slot0;
     int count = 0;
-    auto col = [&](const double *L, int row) { return L[row * S1 + sg]; };
+    const double *Ct = Lt + sg;  // column sg of the time table; pw at + w_pw
+    const int pwo = a.w_pw;
+    // filter scratch: the pad rows (restored after use) and the column sums (rewritten
+    // for every slab; record N + 1 is beyond the scratch)
+    const Scratch sc{Lt + slab, Lp + slab, (int32_t *)C0, a.wcap};
 
     // pad rows and the zero record (never overwritten by the slab copies)
     for (int x = lane; x < K * S1; x += 64) {
         Lt[slab + x] = INFINITY;
         Lp[slab + x] = 0.0;
     }
-    if (lane == 0) C0[N + 1] = ColRec{0.0, 0.0, 0.0, 0.0};
+    if (lane == 0) C0[N + 1] = ColRec{0.0, 0.0};
 
     {
         const size_t pf = (size_t)p * a.F + f0;
@@ -261,90 +377,94 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
         const double tcm = tc_next;
         const double ctail = pc_next * tc_next;
 
-        // Running sums, one instruction stream: lane 0 sums the all-SM column over
-        // every row and writes the records; a lane of a later position run sums its own
-        // column up to its first position.  Rows are loaded 8 at a time, one block ahead.
-        const int ccol = lane == 0 ? 0 : sg;
-        const int nrow = lane == 0 ? N : plo;
-        double sa = 0.0, sb = 0.0;
+        // Running sums, 8 rows at a time: every lane sums its column (lane 0 the all-SM
+        // column, writing the records; the others their comm-time column) and keeps the
+        // sums at its first position, which is a multiple of 8 (or 0).
+        double pA = 0.0, pB = 0.0, a0, b0;
         {
-            double vt[8], vw[8];
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const int i = min(q, N - 1);
-                vt[q] = Lt[i * S1 + ccol];
-                vw[q] = Lp[i * S1 + ccol];
-            }
+            const int cc = lane == 0 ? 0 : sg;
+            double sa = 0.0, sb = 0.0;
             for (int i0 = 0; i0 < N; i0 += 8) {
-                double nt[8], nw[8];
-                if (i0 + 8 < N) {
+                const double *bt = Lt + (i0 * S1 + cc), *bw = Lp + (i0 * S1 + cc);
+                double vt[8], vw[8], ra[8], rb[8];
+                if (i0 + 8 <= N) {
 #pragma unroll
                     for (int q = 0; q < 8; ++q) {
-                        const int i = min(i0 + 8 + q, N - 1);
-                        nt[q] = Lt[i * S1 + ccol];
-                        nw[q] = Lp[i * S1 + ccol];
+                        vt[q] = bt[q * S1];
+                        vw[q] = bw[q * S1];
+                    }
+                } else {
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        vt[q] = i0 + q < N ? bt[q * S1] : 0.0;
+                        vw[q] = i0 + q < N ? bw[q * S1] : 0.0;
                     }
                 }
-                double ra[8], rb[8];
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
                     ra[q] = sa;
                     rb[q] = sb;
-                    if (i0 + q < nrow) {
-                        sa = sa + vt[q];
-                        sb = sb + vw[q] * vt[q];
-                    }
+                    sa = sa + vt[q];  // rows past N add +0: exact
+                    sb = sb + vw[q] * vt[q];
+                }
+                if (i0 + 8 == plo) {
+                    pA = sa;
+                    pB = sb;
                 }
                 if (lane == 0) {
+                    double *c = (double *)(C0 + i0);
 #pragma unroll
                     for (int q = 0; q < 8; ++q)
-                        if (i0 + q < N) C0[i0 + q] = ColRec{ra[q], rb[q], vt[q], vw[q]};
-                }
-#pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    vt[q] = nt[q];
-                    vw[q] = nw[q];
+                        if (i0 + q < N) {
+                            c[2 * q] = ra[q];
+                            c[2 * q + 1] = rb[q];
+                        }
                 }
             }
+            if (lane == 0) {
+                ((double *)(C0 + N))[0] = sa;
+                ((double *)(C0 + N))[1] = sb;
+            }
+            a0 = bitsd(lane_u64(dbits(sa), 0));
+            b0 = bitsd(lane_u64(dbits(sb), 0));
         }
-        if (lane == 0) C0[N] = ColRec{sa, sb, 0.0, 0.0};
-        const double a0 = bitsd(lane_u64(dbits(sa), 0)), b0 = bitsd(lane_u64(dbits(sb), 0));
-        double pA = lane == 0 ? 0.0 : sa, pB = lane == 0 ? 0.0 : sb;
         wave_lds_fence();
 
         int j = plo;  // end cursor
         double jA = pA, jB = pB;
-        double bt[K], bw[K], qt, qw, sA, sB;  // loaded one round ahead
-        auto load_next = [&](int pp) {  // inputs of the round at position pp (<= N + 1)
-            const double *bt0 = Lt + (min(max(j, pp), N) * S1 + sg);  // rows jb .. jb + K - 1
-            const double *bw0 = bt0 + a.w_pw;
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-                bt[k] = bt0[k * S1];
-                bw[k] = bw0[k * S1];
-            }
-            const int pr = max(pp - 1, 0);  // row of the launch-cursor step
-            qt = col(Lt, pr);
-            qw = col(Lp, pr);
-            const ColRec cs = C0[pp];
-            sA = cs.a;
-            sB = cs.b;
-        };
-        load_next(plo);
         for (int ch = 0; ch < a.nch; ++ch) {
             const int c0 = plo + ch * R;
             const int nv = max(0, min(R, phi - c0));
             double vT[R], vE[R];
+            double bt[K], bw[K], qt, qw, sA, sB;  // inputs of the next round
+            auto load_batch = [&](int jb) {  // rows jb .. jb + K - 1 of column sg
+                const double *b0p = Ct + __umul24(jb, S1);
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    bt[k] = b0p[k * S1];
+                    bw[k] = b0p[k * S1 + pwo];
+                }
+            };
+            load_batch(min(max(j, c0), N));
+            {
+                const int pr = max(c0 - 1, 0);
+                qt = Ct[__umul24(pr, S1)];
+                qw = Ct[__umul24(pr, S1) + pwo];
+                const ColRec cs = C0[min(c0, N + 1)];
+                sA = cs.a;
+                sB = cs.b;
+            }
             Tail prev;
+            double tl = INFINITY, el = INFINITY;  // this lane's least T and E
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 const int pp = c0 + r;
                 const bool valid = r < nv;
-                if (valid && pp > plo) {  // launch cursor: A[pp], B[pp] of column sg
+                if (r > 0 || ch > 0) {  // launch cursor: A[pp], B[pp] of column sg
                     pA = pA + qt;
                     pB = pB + qw * qt;
                 }
-                if (valid && j < pp) {
+                if (j < pp) {
                     j = pp;
                     jA = pA;
                     jB = pB;
@@ -364,9 +484,9 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
                         }
                     }
                 }
-                if (__ballot(go && j < N)) {  // more than K - 1 kernels: one row at a time
+                if (__ballot(go && j < N)) {  // K or more kernels: one row at a time
                     while (go && j < N) {
-                        const double t1 = col(Lt, j), w1 = col(Lp, j);
+                        const double t1 = Ct[__umul24(j, S1)], w1 = Ct[__umul24(j, S1) + pwo];
                         const double nA = jA + t1;
                         if (nA - pA <= tcm) {
                             jA = nA;
@@ -377,29 +497,43 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
                         }
                     }
                 }
+                const int jc = min(j, N);  // j can pass N only on a lane past its positions
                 Tail cur;
-                cur.j = j;
+                cur.j = jc;
                 cur.valid = valid;
                 cur.ec = sB + (jB - pB);
                 cur.rem = tcm - (jA - pA);
                 cur.tau = sA + tcm;
                 {
-                    cur.tj = col(Lt, j);  // a pad row when j == N (unused then)
-                    cur.wj = col(Lp, j);
-                    cur.cj = C0[j];
-                    const ColRec c1 = C0[j + 1];
-                    cur.c1a = c1.a;
-                    cur.c1b = c1.b;
+                    const int row = __umul24(jc, S1);
+                    cur.tj = Ct[row];  // a pad row when j == N
+                    cur.wj = Ct[row + pwo];
+                    cur.t0 = Lt[row];
+                    cur.w0 = Lp[row];
+                    cur.cj = C0[jc];
+                    cur.c1 = C0[jc + 1];
                 }
-                if (r + 1 < R || ch + 1 < a.nch) load_next(pp + 1);
+                if (r + 1 < R) {
+                    load_batch(min(max(j, pp + 1), N));
+                    const int pr = min(pp, N);
+                    qt = Ct[__umul24(pr, S1)];
+                    qw = Ct[__umul24(pr, S1) + pwo];
+                    const ColRec cs = C0[min(pp + 1, N + 1)];
+                    sA = cs.a;
+                    sB = cs.b;
+                }
                 if (r > 0) {
-                    finish_tail(prev, N, a.p_static, ctail, a0, b0, vT[r - 1], vE[r - 1]);
+                    finish_tail(prev, a.p_static, ctail, a0, b0, vT[r - 1], vE[r - 1]);
+                    tl = vmin(tl, vT[r - 1]);
+                    el = vmin(el, vE[r - 1]);
                     pin(vT[r - 1]);
                     pin(vE[r - 1]);
                 }
                 prev = cur;
             }
-            finish_tail(prev, N, a.p_static, ctail, a0, b0, vT[R - 1], vE[R - 1]);
+            finish_tail(prev, a.p_static, ctail, a0, b0, vT[R - 1], vE[R - 1]);
+            tl = vmin(tl, vT[R - 1]);
+            el = vmin(el, vE[R - 1]);
             if (ch == a.nch - 1 && f + 1 < f1) {
                 // every LDS read of this slab has returned: the next slab may land
                 wave_lds_fence();
@@ -411,7 +545,8 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
                 pc_next = a.pc[pn * S + s];
             }
             const int ibase = f * a.Cf + c0 * S + s;
-            count += wave_frontier<R>(vT, vE, ibase, S, oT + count, oE + count, oI + count);
+            count += wave_frontier<R>(vT, vE, tl, el, ibase, S, sc, oT + count, oE + count,
+                                      oI + count);
         }
     }
     if (lane == 0) o.cnt[blockIdx.x] = count;
@@ -432,7 +567,7 @@ hipError_t launch_eval_filter_wave(const EvalArgs &a, const UnitOut &o, hipStrea
     const size_t lds = (size_t)a.lds_doubles * sizeof(double);
     if (a.S == 32 && a.R == 17) launch_wave_r<17, 32>(a, o, lds, st);
     else if (a.S == 16 && a.R == 8) launch_wave_r<8, 16>(a, o, lds, st);
-    else if (a.S == 8 && a.R == 4) launch_wave_r<4, 8>(a, o, lds, st);
+    else if (a.S == 8 && a.R == 8) launch_wave_r<8, 8>(a, o, lds, st);
     else {
         switch (a.R) {
         case 2: launch_wave_r<2, 0>(a, o, lds, st); break;

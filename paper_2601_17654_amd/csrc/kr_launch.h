@@ -32,6 +32,7 @@ struct EvalArgs {
     int R, nch;             // positions per chunk (registers), chunks per run
     int w_pw, w_a0;         // LDS offsets (doubles) of the power slab and the column sums
     int dma16;              // 16-byte direct copies (slab length even, tables 16-byte aligned)
+    int wcap;               // candidates the wave filter's LDS scratch holds
 };
 
 // Per-unit frontiers written by the fused kernel or the tile kernel.
