@@ -150,7 +150,7 @@ void phase_mark(int phase, int which, hipStream_t st)
 
 struct FilterWs {
     int64_t *seg_off, *unit_base;
-    int32_t *ucnt, *fcnt, *runcnt;
+    int32_t *ucnt, *fcnt, *runcnt, *lists;
     PointBufs buf[2];
     uint8_t *flags;
 };
@@ -164,6 +164,7 @@ FilterWs carve_filter(Carve &c, int64_t n_total, int n_seg, int64_t n_units, boo
     w.ucnt = c.take<int32_t>(std::max<int64_t>(n_units, 1));
     w.fcnt = c.take<int32_t>(std::max(n_seg, 1));
     w.runcnt = c.take<int32_t>(n_total / KR_FIN_CAP + n_seg + 1);
+    w.lists = c.take<int32_t>(2 * (int64_t)n_seg + 2);
     for (int i = 0; i < 2; ++i) {
         w.buf[i].T = c.take<double>(n);
         w.buf[i].E = c.take<double>(n);
@@ -178,7 +179,7 @@ kr_status finish_segments(const SegLayout &L, FilterWs &w, int64_t cap, int64_t 
                           int32_t *out_idx, double *out_T, double *out_E, hipStream_t st)
 {
     phase_mark(KR_PHASE_MERGE, 0, st);
-    if (launch_finalize(L, w.buf[0], w.ucnt, w.buf[1], w.fcnt, w.runcnt, w.flags, st) !=
+    if (launch_finalize(L, w.buf[0], w.ucnt, w.buf[1], w.fcnt, w.runcnt, w.flags, w.lists, st) !=
         hipSuccess)
         return KR_EHIP;
     if (launch_output(L, w.buf[1], w.fcnt, cap, out_off, out_idx, out_T, out_E, st) != hipSuccess)

@@ -103,10 +103,10 @@ __device__ __forceinline__ T wave_inclusive(T x, Op op)
     return x;
 }
 
-// Exclusive block scan (blockDim.x == KR_BLOCK).  `lds` holds KR_WAVES values.
-// Returns the exclusive prefix; *total receives the block aggregate.  Contains two
-// barriers; every thread of the block must call it.
-template <typename T, typename Op>
+// Exclusive block scan (blockDim.x == 64 * NW, KR_BLOCK by default).  `lds` holds NW
+// values.  Returns the exclusive prefix; *total receives the block aggregate.  Contains
+// two barriers; every thread of the block must call it.
+template <typename T, typename Op, int NW = KR_WAVES>
 __device__ __forceinline__ T block_exclusive(T v, T identity, Op op, T *lds, T *total)
 {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -115,7 +115,7 @@ __device__ __forceinline__ T block_exclusive(T v, T identity, Op op, T *lds, T *
     __syncthreads();
     T before = identity, all = identity;
 #pragma unroll
-    for (int w = 0; w < KR_WAVES; ++w) {
+    for (int w = 0; w < NW; ++w) {
         T s = lds[w];
         if (w < wave) before = op(before, s);
         all = op(all, s);

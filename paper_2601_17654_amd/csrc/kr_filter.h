@@ -197,18 +197,23 @@ __device__ inline int tile_frontier(const double (&vT)[CAP], const double (&vE)[
 // need not be a power of two.  Every thread of the block must call.
 __device__ inline void lds_sort_keys(uint64_t *sT, uint64_t *sE, int32_t *sI, int n)
 {
-    int m = 1;
-    while (m < n) m <<= 1;
-    for (int k = 2; k <= m; k <<= 1) {
-        for (int j = k >> 1; j > 0; j >>= 1) {
+    int m = 1, lm = 0;
+    while (m < n) {
+        m <<= 1;
+        ++lm;
+    }
+    for (int lk = 1; lk <= lm; ++lk) {
+        const int k = 1 << lk;
+        for (int lj = lk - 1; lj >= 0; --lj) {
+            const int j = 1 << lj;  // q / j and q % j by shift and mask
             for (int q = threadIdx.x; q < (m >> 1); q += KR_BLOCK) {
                 int lo, hi;
-                if (j == (k >> 1)) {  // first stage of a merge: mirror within the block
-                    const int blk = q / j, r = q % j;
+                if (lj == lk - 1) {  // first stage of a merge: mirror within the block
+                    const int blk = q >> lj, r = q & (j - 1);
                     lo = blk * k + r;
                     hi = blk * k + (k - 1 - r);
                 } else {
-                    lo = 2 * j * (q / j) + (q % j);
+                    lo = ((q >> lj) << (lj + 1)) + (q & (j - 1));
                     hi = lo + j;
                 }
                 if (hi < n) {

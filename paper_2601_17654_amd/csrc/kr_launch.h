@@ -75,9 +75,10 @@ hipError_t launch_tile_layout(const int64_t *seg_off, int64_t *unit_base, int n_
                               hipStream_t st);
 hipError_t launch_pareto_tiles(const double *T, const double *E, const SegLayout &L,
                                int64_t n_units_bound, const UnitOut &o, hipStream_t st);
+// lists: 2 * n_seg + 2 ints of scratch
 hipError_t launch_finalize(const SegLayout &L, const PointBufs &buf, const int32_t *ucnt,
                            const PointBufs &fin, int32_t *fcnt, int32_t *runcnt, uint8_t *flags,
-                           hipStream_t st);
+                           int32_t *lists, hipStream_t st);
 hipError_t launch_output(const SegLayout &L, const PointBufs &fin, const int32_t *fcnt,
                          int64_t cap, int64_t *out_off, int32_t *out_idx, double *out_T,
                          double *out_E, hipStream_t st);

@@ -7,11 +7,12 @@
 //
 // Work split: every segment is cut into units (tiles of points, or the frequency
 // range of one fused workgroup) whose exact frontiers are written to the unit's slot.
-// One workgroup per segment then takes the union of its units' frontiers: sorted and
-// scanned in LDS when it fits, otherwise cut into LDS-sized chunks whose frontiers
-// are merged pairwise in device memory.  A pairwise merge of two staircases needs no
-// sort: an element's rank in the partner comes from a binary search, and it survives
-// iff the partner element just before it in key order has a larger E.
+// The union of a segment's unit frontiers is then sorted by a merge sort in LDS and
+// scanned: a 256-thread block per segment of up to 512 points, a 1024-thread block
+// for the few segments of up to 4096, and beyond that LDS-sized chunks whose
+// frontiers are merged pairwise in device memory.  A pairwise merge of two staircases
+// needs no sort: an element's rank in the partner comes from a binary search, and it
+// survives iff the partner element just before it in key order has a larger E.
 #include "kr_filter.h"
 #include "kr_launch.h"
 
@@ -210,16 +211,247 @@ struct FinLds {
     int32_t upre[KR_FIN_UNITS + 1];
 };
 
+// ----------------------------------------------------------------------------
 // Union of a segment's unit frontiers -> the segment's frontier in `fin` at the
-// segment start; its size in fcnt[g].  `buf` holds the unit slots (and is free to be
-// overwritten once they are gathered).  One block per segment.
-__global__ void __launch_bounds__(KR_BLOCK)
-finalize_kernel(SegLayout L, PointBufs buf, const int32_t *ucnt, PointBufs fin, int32_t *fcnt,
-                int32_t *runcnt, uint8_t *flags)
+// segment start, its size in fcnt[g].  `buf` holds the unit slots (free to be
+// overwritten once they are gathered).
+//
+// Segments of at most NT * PER points in at most NT units: one block of NT threads
+// per segment sorts the union in LDS by merging.  Thread t gathers points t * PER ..
+// t * PER + PER - 1 and sorts them in registers; the sorted runs are then merged
+// pairwise, one level per doubling of the run width.  At a level every point finds
+// its rank in the partner run by a binary search and moves to (its place in its own
+// run) + (that rank) -- keys are distinct, so the places form a permutation.  The
+// levels move (T, 16-bit point id) pairs between two buffers; E and the index stay in
+// place and are read on a tie in T only.  A strict prefix-minimum scan of E over the
+// sorted order gives the frontier.
+//
+// Three stages: every segment first meets the small instance (a block per segment);
+// what it cannot take goes on a list for the large instance (one block per listed
+// segment, looping), and what that cannot take on a second list for the chunked
+// fallback at the end of this section.
+#define KR_FM_SMALL_NT 256
+#define KR_FM_SMALL_PER 2
+#define KR_FM_LARGE_NT 1024
+#define KR_FM_LARGE_PER 4
+
+template <int NT, int PER>
+struct MergeLds {
+    static constexpr int CAP = NT * PER;
+    uint64_t T[2][CAP];
+    uint16_t id[2][CAP];
+    uint64_t E[CAP];
+    int32_t I[CAP];
+    int32_t upre[NT + 1];  // upre[u] = points in units before u
+    int32_t sc32[NT / 64];
+    uint64_t sc64[NT / 64];
+};
+
+struct MKey {
+    uint64_t t, e;
+    int32_t i;
+};
+
+__device__ __forceinline__ bool mk_less(const MKey &a, const MKey &b)
 {
-    __shared__ FinLds sh;
-    __shared__ int32_t sc[KR_WAVES];
+    return key_less(a.t, a.e, a.i, b.t, b.e, b.i);
+}
+
+// Key of the point at a level position (T there, id -> E and index) below another's.
+__device__ __forceinline__ bool pos_less(uint64_t ta, int xa, uint64_t tb, int xb,
+                                         const uint64_t *E, const int32_t *I)
+{
+    if (ta != tb) return ta < tb;
+    const uint64_t ea = E[xa], eb = E[xb];
+    if (ea != eb) return ea < eb;
+    return I[xa] < I[xb];
+}
+
+// Stage entry: unit prefix of segment g into sh.upre and the point count n, or false
+// when the segment has more than NT units or NT * PER points.  Block-uniform.
+template <int NT, int PER>
+__device__ __forceinline__ bool merge_prefix(int g, const SegLayout &L, const int32_t *ucnt,
+                                             MergeLds<NT, PER> &sh, int &n)
+{
+    const int tid = threadIdx.x;
+    const int64_t u0 = L.unit_base[g];
+    const int nu = (int)(L.unit_base[g + 1] - u0);
+    if (nu > NT) return false;
+    const int ex = block_exclusive<int, SumI32, NT / 64>(tid < nu ? ucnt[u0 + tid] : 0, 0,
+                                                         SumI32(), sh.sc32, &n);
+    if (n > MergeLds<NT, PER>::CAP) return false;
+    if (tid < nu) sh.upre[tid] = ex;
+    if (tid == 0) sh.upre[nu] = n;
+    return true;
+}
+
+template <int NT, int PER>
+__device__ __forceinline__ void merge_segment(int g, int n, const SegLayout &L,
+                                              const PointBufs &buf, const PointBufs &fin,
+                                              int32_t *fcnt, MergeLds<NT, PER> &sh)
+{
+    static_assert(NT * PER <= 65536 && (PER & (PER - 1)) == 0, "16-bit ids, power-of-two runs");
+    const int tid = threadIdx.x;
+    const int64_t s0 = L.seg_off[g];
+    const int nu = (int)(L.unit_base[g + 1] - L.unit_base[g]);
+    lds_barrier();  // upre
+    const int q0 = min(n, tid * PER), q1 = min(n, q0 + PER);
+    MKey k[PER];
+    int u = 0;  // unit holding point q0: the last u < nu with upre[u] <= q0
+#pragma unroll
+    for (int step = NT / 2; step >= 1; step >>= 1)
+        if (u + step < nu && sh.upre[u + step] <= q0) u += step;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int x = q0 + j;
+        k[j] = MKey{~0ull, ~0ull, 0x7FFFFFFF};  // beyond the segment: sorts last, dropped
+        if (x < q1) {
+            while (sh.upre[u + 1] <= x) ++u;  // skip ended and empty units (x < upre[nu])
+            const int64_t src = s0 + (int64_t)u * L.unit_stride + (x - sh.upre[u]);
+            k[j] = MKey{dbits(buf.T[src]), dbits(buf.E[src]), buf.I[src]};
+        }
+    }
+#pragma unroll
+    for (int w = 2; w <= PER; w <<= 1)
+#pragma unroll
+        for (int j = w >> 1; j > 0; j >>= 1)
+#pragma unroll
+            for (int i = 0; i < PER; ++i) {
+                const int l = i ^ j;
+                if (l > i && ((i & w) == 0 ? mk_less(k[l], k[i]) : mk_less(k[i], k[l]))) {
+                    const MKey x = k[i];
+                    k[i] = k[l];
+                    k[l] = x;
+                }
+            }
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+        if (q0 + j < q1) {
+            sh.T[0][q0 + j] = k[j].t;
+            sh.id[0][q0 + j] = (uint16_t)(q0 + j);
+            sh.E[q0 + j] = k[j].e;
+            sh.I[q0 + j] = k[j].i;
+        }
+    lds_barrier();
+    int cur = 0;
+    for (int w = PER; w < n; w <<= 1) {  // sorted runs of width w -> width 2w
+        const uint64_t *inT = sh.T[cur];
+        const uint16_t *inI = sh.id[cur];
+        // this thread's points all lie in one run; its partner is [p0, p0 + plen)
+        const int a0 = q0 & ~(2 * w - 1);
+        const bool in_a = q0 - a0 < w;
+        const int p0 = in_a ? min(n, a0 + w) : a0;
+        const int plen = in_a ? min(n, a0 + 2 * w) - p0 : w;
+        const int own0 = in_a ? a0 : a0 + w;
+        uint64_t t[PER];
+        int x[PER], r[PER];
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int q = min(q0 + j, n - 1);
+            t[j] = inT[q];
+            x[j] = inI[q];
+            r[j] = 0;
+        }
+        // rank in the partner: the number of its points below the key (lifting search)
+        if (q0 < q1)
+            for (int step = w; step >= 1; step >>= 1)
+#pragma unroll
+                for (int j = 0; j < PER; ++j) {
+                    const int c = r[j] + step;
+                    if (c <= plen &&
+                        pos_less(inT[p0 + c - 1], inI[p0 + c - 1], t[j], x[j], sh.E, sh.I))
+                        r[j] = c;
+                }
+#pragma unroll
+        for (int j = 0; j < PER; ++j)
+            if (q0 + j < q1) {
+                const int dst = a0 + (q0 + j - own0) + r[j];
+                sh.T[cur ^ 1][dst] = t[j];
+                sh.id[cur ^ 1][dst] = (uint16_t)x[j];
+            }
+        cur ^= 1;
+        lds_barrier();
+    }
+    // keep a point iff its E is below every E before it in key order
+    const uint16_t *ord = sh.id[cur];
+    uint64_t e[PER];
+    uint64_t m = KR_INF_BITS;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        e[j] = q0 + j < q1 ? sh.E[ord[q0 + j]] : KR_INF_BITS;
+        m = e[j] < m ? e[j] : m;
+    }
+    uint64_t all;
+    const uint64_t best0 =
+        block_exclusive<uint64_t, MinU64, NT / 64>(m, KR_INF_BITS, MinU64(), sh.sc64, &all);
+    uint64_t best = best0;
+    int nkeep = 0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+        if (e[j] < best) {
+            ++nkeep;
+            best = e[j];
+        }
+    int count;
+    int opos = block_exclusive<int, SumI32, NT / 64>(nkeep, 0, SumI32(), sh.sc32, &count);
+    best = best0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+        if (e[j] < best) {
+            const int q = q0 + j;
+            fin.T[s0 + opos] = bitsd(sh.T[cur][q]);
+            fin.E[s0 + opos] = bitsd(e[j]);
+            fin.I[s0 + opos] = sh.I[ord[q]];
+            ++opos;
+            best = e[j];
+        }
+    if (tid == 0) fcnt[g] = count;
+}
+
+// Stage 1: a block per segment.  lists[0] counts the segments passed on (zero on
+// entry), lists[2 ...] holds them; lists[1] (the second list's count) is cleared here.
+__global__ void __launch_bounds__(KR_FM_SMALL_NT)
+finalize_small_kernel(SegLayout L, PointBufs buf, const int32_t *ucnt, PointBufs fin,
+                      int32_t *fcnt, int32_t *lists)
+{
+    __shared__ MergeLds<KR_FM_SMALL_NT, KR_FM_SMALL_PER> sh;
     const int g = blockIdx.x;
+    if (g == 0 && threadIdx.x == 0) lists[1] = 0;
+    int n;
+    if (merge_prefix(g, L, ucnt, sh, n)) merge_segment(g, n, L, buf, fin, fcnt, sh);
+    else if (threadIdx.x == 0) lists[2 + atomicAdd(&lists[0], 1)] = g;
+}
+
+// Stage 2: the listed segments, a block each (blocks loop over the list); those it
+// cannot take go on the second list (count lists[1], entries from lists[2 + n_seg]).
+__global__ void __launch_bounds__(KR_FM_LARGE_NT)
+finalize_large_kernel(SegLayout L, PointBufs buf, const int32_t *ucnt, PointBufs fin,
+                      int32_t *fcnt, int32_t *lists)
+{
+    __shared__ MergeLds<KR_FM_LARGE_NT, KR_FM_LARGE_PER> sh;
+    const int cnt = lists[0];
+    for (int i = blockIdx.x; i < cnt; i += gridDim.x) {
+        const int g = lists[2 + i];
+        int n;
+        if (merge_prefix(g, L, ucnt, sh, n)) merge_segment(g, n, L, buf, fin, fcnt, sh);
+        else if (threadIdx.x == 0) lists[2 + L.n_seg + atomicAdd(&lists[1], 1)] = g;
+        __syncthreads();  // LDS reuse by the next segment
+    }
+}
+
+__global__ void finalize_lists_init_kernel(int32_t *lists)
+{
+    if (threadIdx.x == 0) lists[0] = 0;
+}
+
+// Stage 3, the segments on the second list: one block per segment (blocks loop over
+// the list).  The union is sorted in LDS when it fits; otherwise it is cut into
+// LDS-sized chunks whose frontiers are merged pairwise in device memory.
+__device__ void finalize_block_segment(int g, const SegLayout &L, const PointBufs &buf,
+                                       const int32_t *ucnt, const PointBufs &fin,
+                                       int32_t *fcnt, int32_t *runcnt, uint8_t *flags,
+                                       FinLds &sh, int32_t *sc)
+{
     const int64_t s0 = L.seg_off[g];
     const int64_t u0 = L.unit_base[g];
     const int nu = (int)(L.unit_base[g + 1] - u0);
@@ -323,13 +555,33 @@ finalize_kernel(SegLayout L, PointBufs buf, const int32_t *ucnt, PointBufs fin, 
     if (threadIdx.x == 0) fcnt[g] = n;
 }
 
+__global__ void __launch_bounds__(KR_BLOCK)
+finalize_block_kernel(SegLayout L, PointBufs buf, const int32_t *ucnt, PointBufs fin,
+                      int32_t *fcnt, int32_t *runcnt, uint8_t *flags, const int32_t *lists)
+{
+    __shared__ FinLds sh;
+    __shared__ int32_t sc[KR_WAVES];
+    const int cnt = lists[1];
+    for (int i = blockIdx.x; i < cnt; i += gridDim.x) {
+        finalize_block_segment(lists[2 + L.n_seg + i], L, buf, ucnt, fin, fcnt, runcnt, flags,
+                               sh, sc);
+        __syncthreads();  // LDS reuse by the next segment
+    }
+}
+
 hipError_t launch_finalize(const SegLayout &L, const PointBufs &buf, const int32_t *ucnt,
                            const PointBufs &fin, int32_t *fcnt, int32_t *runcnt, uint8_t *flags,
-                           hipStream_t st)
+                           int32_t *lists, hipStream_t st)
 {
     if (L.n_seg == 0) return hipSuccess;
-    hipLaunchKernelGGL(finalize_kernel, dim3(L.n_seg), dim3(KR_BLOCK), 0, st, L, buf, ucnt, fin,
-                       fcnt, runcnt, flags);
+    const dim3 loop_grid(min(L.n_seg, 256));
+    hipLaunchKernelGGL(finalize_lists_init_kernel, dim3(1), dim3(64), 0, st, lists);
+    hipLaunchKernelGGL(finalize_small_kernel, dim3(L.n_seg), dim3(KR_FM_SMALL_NT), 0, st, L, buf,
+                       ucnt, fin, fcnt, lists);
+    hipLaunchKernelGGL(finalize_large_kernel, loop_grid, dim3(KR_FM_LARGE_NT), 0, st, L, buf,
+                       ucnt, fin, fcnt, lists);
+    hipLaunchKernelGGL(finalize_block_kernel, loop_grid, dim3(KR_BLOCK), 0, st, L, buf, ucnt,
+                       fin, fcnt, runcnt, flags, lists);
     return hipGetLastError();
 }
 
