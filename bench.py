@@ -13,6 +13,7 @@ the library's stream); `frontier_cells_per_s` is the composition's DP cells (sum
 partitions of the reachable bins) over step 2's time.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--skip-cpu]
+       python bench.py --part eval|compose   (one half only, no bench line: for profilers)
        python bench.py --copy-calibration   (plain 1 GiB device copy, for counters)
 """
 
@@ -87,6 +88,8 @@ def main():
     ap.add_argument("--skip-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--part", choices=["all", "eval", "compose"], default="all",
+                    help="profiling aid: run only one half of the step (prints no bench line)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         log("bench.py runs on exactly one GPU: the schedule search here is a single-GPU "
@@ -119,6 +122,17 @@ def main():
     cap = int(fr.off[-1].item())
     comp = kr.compose_frontiers(off4_d, T4_d, E4_d, B)
     torch.cuda.synchronize()
+
+    if args.part != "all":
+        for _ in range(args.warmup + args.steps):
+            if args.part == "eval":
+                kr.evaluate_and_filter(sp, *d, cap=cap, sync=False)
+            else:
+                kr.compose_frontiers(off4_d, T4_d, E4_d, B, out=comp)
+                kr.extract_schedule(comp, off4_d, T4_d, E4_d, comp.stair_bin[:1])
+        torch.cuda.synchronize()
+        log("ran %d passes of the %s half" % (args.warmup + args.steps, args.part))
+        return
 
     def step(ev, phase_ev):
         ev[0].record()

@@ -25,6 +25,7 @@
 // energy.  All of it runs on registers with wave reductions.
 #include "kr_filter.h"
 #include "kr_launch.h"
+#include "kr_wave.h"
 
 namespace kr {
 
@@ -40,15 +41,6 @@ __device__ __forceinline__ void wave_lds_fence()
 // Keeps the compiler from sinking the computation of x past this point (it would keep
 // the inputs of every unrolled round alive at once).
 __device__ __forceinline__ void pin(double &x) { asm volatile("" : "+v"(x)); }
-
-// Minimum of two non-NaN doubles in one instruction (the compiler's fmin adds operand
-// canonicalisation it cannot prove unnecessary here).
-__device__ __forceinline__ double vmin(double a, double b)
-{
-    double r;
-    asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-    return r;
-}
 
 // s_waitcnt encodings (gfx9): vmcnt [3:0]+[15:14], expcnt [6:4], lgkmcnt [11:8].
 #define KR_WAIT_VM0 0x0F70
@@ -82,43 +74,6 @@ __device__ __forceinline__ void emit(const Key &k, int n, double *oT, double *oE
         oE[n] = bitsd(k.e);
         oI[n] = k.i;
     }
-}
-
-// One DPP step of a wave minimum over doubles (rows not written keep their own value).
-template <int CTRL, int ROWS>
-__device__ __forceinline__ double dpp_min_f64(double x)
-{
-    const uint64_t b = dbits(x);
-    const uint32_t lo = (uint32_t)b, hi = (uint32_t)(b >> 32);
-    uint32_t ylo, yhi;
-    if constexpr (ROWS == 0xF) {  // every lane reads a lane of its own row
-        ylo = __builtin_amdgcn_mov_dpp(lo, CTRL, 0xF, 0xF, false);
-        yhi = __builtin_amdgcn_mov_dpp(hi, CTRL, 0xF, 0xF, false);
-    } else {  // rows outside ROWS keep their own value
-        ylo = __builtin_amdgcn_update_dpp(lo, lo, CTRL, ROWS, 0xF, false);
-        yhi = __builtin_amdgcn_update_dpp(hi, hi, CTRL, ROWS, 0xF, false);
-    }
-    return vmin(bitsd(((uint64_t)yhi << 32) | ylo), x);
-}
-
-// Minima over the wave of two non-negative doubles (same DPP pattern as wave_min_u64),
-// interleaved; results uniform.
-__device__ __forceinline__ void wave_min2_f64(double &x, double &y)
-{
-    x = dpp_min_f64<0xB1, 0xF>(x);
-    y = dpp_min_f64<0xB1, 0xF>(y);
-    x = dpp_min_f64<0x4E, 0xF>(x);
-    y = dpp_min_f64<0x4E, 0xF>(y);
-    x = dpp_min_f64<0x141, 0xF>(x);
-    y = dpp_min_f64<0x141, 0xF>(y);
-    x = dpp_min_f64<0x140, 0xF>(x);
-    y = dpp_min_f64<0x140, 0xF>(y);
-    x = dpp_min_f64<0x142, 0xA>(x);
-    y = dpp_min_f64<0x142, 0xA>(y);
-    x = dpp_min_f64<0x143, 0xC>(x);
-    y = dpp_min_f64<0x143, 0xC>(y);
-    x = bitsd(lane_u64(dbits(x), 63));
-    y = bitsd(lane_u64(dbits(y), 63));
 }
 
 // Least (T, E, index) candidate among those with pred(r) true.  Fast path when exactly
