@@ -69,8 +69,9 @@ bool wave_plan(EvalArgs *a)
     const int maxrun = std::max(std::min(a->span, a->n_pos), last);
     a->R = maxrun <= 2 ? 2 : maxrun <= 4 ? 4 : maxrun <= 8 ? 8 : 17;
     a->nch = (maxrun + a->R - 1) / a->R;
-    // filter scratch: pad rows of each table and the column-sum area below record N + 1
-    a->wcap = (int)std::min<int64_t>(64, std::min<int64_t>(KR_PAD * (a->S + 1), 4 * (a->N + 1)));
+    // filter scratch: the pad rows of each table
+    // (the power pad holds cap doubles of E, then cap ints of indices)
+    a->wcap = (int)std::min<int64_t>(64, KR_PAD * (a->S + 1) * 2 / 3);
     // a few times more one-wave blocks than fit on the chip at once, so the
     // dispatcher balances uneven slabs; within a block slab copies overlap the filter
     const int64_t resident = std::max<int64_t>(1, std::min<int64_t>(16, kLdsPerCu / (lds * 8)));

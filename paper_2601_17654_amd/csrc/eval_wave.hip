@@ -197,6 +197,7 @@ __device__ inline int wave_frontier(const double (&vT)[R], const double (&vE)[R]
             if (mine) {  // give the pad rows back
                 sc.T[lane] = INFINITY;
                 sc.E[lane] = 0.0;
+                sc.I[lane] = 0;  // the power pad's upper half holds the indices
             }
         } else if (tot > 0) {
             uint64_t bound = dbits(EA);
@@ -307,9 +308,11 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
     int count = 0;
     const double *Ct = Lt + sg;  // column sg of the time table; pw at + w_pw
     const int pwo = a.w_pw;
-    // filter scratch: the pad rows (restored after use) and the column sums (rewritten
-    // for every slab; record N + 1 is beyond the scratch)
-    const Scratch sc{Lt + slab, Lp + slab, (int32_t *)C0, a.wcap};
+    // filter scratch, all in the pad rows (restored after use): T in the time pad, E
+    // in the power pad, indices after E in the power pad (a power pad of zeros reads
+    // back the same whether as doubles or as pairs of zero ints).  The column sums
+    // are not touched: a run of several chunks reads them again after a filter.
+    const Scratch sc{Lt + slab, Lp + slab, (int32_t *)(Lp + slab + a.wcap), a.wcap};
 
     // pad rows and the zero record (never overwritten by the slab copies)
     for (int x = lane; x < K * S1; x += 64) {
@@ -325,7 +328,6 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
     }
     double tc_next = a.tc[((size_t)p * a.F + f0) * S + s];
     double pc_next = a.pc[((size_t)p * a.F + f0) * S + s];
-
     for (int f = f0; f < f1; ++f) {
         __builtin_amdgcn_s_waitcnt(KR_WAIT_VM0);  // slab f is in LDS
         wave_lds_fence();

@@ -74,10 +74,14 @@ def small_spaces():
     spaces.append(I.Space(2, 1, 2, 2, (8, 16), (1500.0,)))
     spaces.append(I.Space(2, 9, 1, 10, (1, 2, 3), (1005.0, 1980.0)))
     spaces.append(I.Space(2, 9, 2, 10, (1, 32), (1005.0, 1980.0)))
+    # more SM choices than half a wave: one run of 33 positions per lane, evaluated as
+    # two register chunks per frequency
+    spaces.append(I.Space(2, 32, 1, 33, tuple(range(1, 41)), (1005.0, 1500.0, 1980.0)))
+    spaces.append(I.Space(2, 32, 1, 33, tuple(range(2, 98, 2)), (1005.0, 1980.0)))
     return spaces
 
 
-@pytest.mark.parametrize("case", range(14))
+@pytest.mark.parametrize("case", range(16))
 @pytest.mark.parametrize("tc_scale", [1.0, 1e-3, 1e3])
 def test_evaluate_small_spaces(kr, oracle_lib, case, tc_scale):
     space = small_spaces()[case]
@@ -121,6 +125,23 @@ def test_evaluate_sampled_partitions(kr, oracle_lib, cfg, parts):
         Tr, Er = oracle_lib.evaluate_partition(w.space, w.t, w.pw, w.tc, w.pc, p)
         assert_close(T[p], Tr, RT_TE, "cfg%d T part %d" % (cfg, parts.start + p))
         assert_close(E[p], Er, RT_TE, "cfg%d E part %d" % (cfg, parts.start + p))
+
+
+def test_evaluate_and_filter_eval_stress_all(kr, oracle_lib):
+    """The fused kernel at the eval-stress batch size, in the benchmark's launch
+    configuration (several frequencies per block, so the staging of the next slab
+    during the current one runs), against the oracle on every partition."""
+    w = workload(3)
+    fr = kr.evaluate_and_filter(w.space, *dev_tables(w))
+    ref = oracle_lib.evaluate_and_filter(w.space, w.t, w.pw, w.tc, w.pc)
+    off = fr.off.cpu().numpy()
+    idx, T, E = fr.idx.cpu().numpy(), fr.T.cpu().numpy(), fr.E.cpu().numpy()
+    assert off[-1] == sum(len(r[0]) for r in ref), "total frontier points"
+    for p in range(w.space.n_parts):
+        lo, hi = int(off[p]), int(off[p + 1])
+        np.testing.assert_array_equal(idx[lo:hi], ref[p][0], err_msg="eval-stress part %d" % p)
+        assert_close(T[lo:hi], ref[p][1], RT_TE, "eval-stress part %d T" % p)
+        assert_close(E[lo:hi], ref[p][2], RT_TE, "eval-stress part %d E" % p)
 
 
 @pytest.mark.parametrize("cfg,sample", [(3, [0, 1, 333, 512, 1023]), (2, [0, 131, 255])])
