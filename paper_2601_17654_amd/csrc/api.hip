@@ -312,6 +312,8 @@ size_t kr_compose_frontiers_workspace(int32_t n_parts, int32_t n_bins)
     c.take<int32_t>(P);
     c.take<double>(B);
     c.take<double>(B);
+    c.take<double>(P * B);
+    c.take<int32_t>((B + 255) / 256);
     return c.used;
 }
 
@@ -343,6 +345,8 @@ kr_status kr_compose_frontiers(int32_t n_parts, const int64_t *off, const double
     w.occ = c.take<int32_t>(P);
     w.F0 = c.take<double>(B);
     w.F1 = c.take<double>(B);
+    w.Fh = c.take<double>(P * B);
+    w.done = c.take<int32_t>((B + 255) / 256);
     ComposeArgs a;
     a.P = n_parts;
     a.B = n_bins;

@@ -295,6 +295,187 @@ minplus_tile_kernel(ComposeArgs a, ComposeWs w, int k, const double *Fprev, doub
     }
 }
 
+// All min-plus steps in one launch, as a wavefront over (tile, step).  Block g owns
+// the KR_MP_W bins of tile g for every step: F_k of its own bins stays in LDS from one
+// step to the next, and the halo F_{k-1}[b0 - M_k, b0) comes from the tiles on its
+// left, which publish every step's values to the step history Fh[k][b] and then
+// raise done[tile] = k.  Tile g can run step k as soon as those tiles have finished
+// step k - 1, so the tiles advance as a diagonal front: a step costs one tile's
+// compute, and the latency of a hand-over is paid once per tile, not once per step.
+// The grid is launched cooperatively (every block resident), so a wait always ends;
+// a wait that still exceeds KR_WF_POLLS polls marks the result invalid and releases
+// the blocks waiting on this one.
+//
+// Hand-over: values and flags are written and read with device-scope relaxed atomic
+// accesses, which are coherent across the chip without cache maintenance; a block
+// waits for its value stores to complete before it raises its flag, and reads the
+// values only after it has seen the flag.
+#define KR_WF_POLLS (1 << 22)
+
+__device__ __forceinline__ void store_dev(double *p, double v)
+{
+    __hip_atomic_store((uint64_t *)p, dbits(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_dev(int32_t *p, int32_t v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+struct WavefrontLds {
+    double win[KR_MP_W + KR_MP_HCAP];  // F_{k-1}[b0 - M_k, b0 + KR_MP_W)
+    double cur[KR_MP_W];               // F of the tile's own bins, last finished step
+    double e[KR_MP_HCAP + 1];
+    int32_t off8[KR_MP_HCAP + 1];  // b2 * 8: byte offset into the window
+    int32_t arg[KR_MP_HCAP + 1];
+    double pbest[KR_MP_Q][KR_MP_W];
+    int32_t pwho[KR_MP_Q][KR_MP_W];
+    int32_t bad;  // a wait gave up
+};
+
+__global__ void wavefront_init_kernel(int32_t *done, int G)
+{
+    const int g = blockIdx.x * blockDim.x + threadIdx.x;
+    if (g < G) done[g] = -1;
+}
+
+__global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(ComposeArgs a, ComposeWs w)
+{
+    __shared__ WavefrontLds sm;
+    if (*a.status != KR_OK) return;  // the same for every block
+    const int tid = threadIdx.x, t = tid % KR_MP_W, qtr = tid / KR_MP_W;
+    const int g = blockIdx.x;
+    const int P = a.P, B = a.B;
+    const int64_t b0 = (int64_t)g * KR_MP_W, b = b0 + t;
+    double *const Fh = w.Fh;
+    int32_t *const done = w.done;
+    if (tid == 0) sm.bad = 0;
+
+    // Waits until tiles [lo, g) have finished step k; false if a wait gave up.
+    auto wait_left = [&](int lo, int k) {
+        if (tid == 0) {
+            for (int tt = lo; tt < g && !sm.bad; ++tt) {
+                int polls = 0;
+                while (load_l2(done + tt) < k) {
+                    if (++polls > KR_WF_POLLS) {
+                        sm.bad = 1;
+                        break;
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        return !sm.bad;
+    };
+    // Every thread's value stores are complete before the flag goes up.
+    auto publish = [&](int k) {
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);  // the stores stay before the wait
+        __builtin_amdgcn_s_waitcnt(0x0F70);       // vmcnt(0)
+        __syncthreads();
+        if (tid == 0) store_dev(done + g, k);
+    };
+
+    // step 0: F_1 = e_1
+    if (qtr == 0) {
+        double v = INFINITY;
+        int32_t who = -1;
+        if (b < B && b <= w.Mk[0]) {
+            const int32_t arg = w.earg[b];
+            if (arg != 0x7FFFFFFF) {
+                v = bitsd(w.ebits[b]);
+                who = arg;
+            }
+        }
+        sm.cur[t] = v;
+        if (b < B) {
+            a.bp[b] = who;
+            if (P == 1) a.F_out[b] = v;
+            else store_dev(Fh + b, v);
+        }
+    }
+    publish(0);
+
+    for (int k = 1; k < P; ++k) {
+        const int64_t Lprev = w.Lk[k - 1], Lcur = w.Lk[k];
+        const int64_t M = w.Mk[k];
+        const int cnt = w.occ[k];
+        const int64_t base = w.eoff[k];
+        const bool last = k == P - 1;
+        double best = INFINITY;
+        int32_t who = -1;
+        if (b0 < Lcur) {
+            const int lo = (int)(max((int64_t)0, b0 - M) / KR_MP_W);
+            if (!wait_left(lo, k - 1)) break;
+            const double *Fp = Fh + (int64_t)(k - 1) * B;
+            if (M <= KR_MP_HCAP) {
+                for (int i = tid; i < M; i += KR_MP_W * KR_MP_Q) {
+                    const int64_t src = b0 - M + i;
+                    sm.win[i] = src >= 0 && src < Lprev ? load_l2(Fp + src) : INFINITY;
+                }
+                for (int i = tid; i < KR_MP_W; i += KR_MP_W * KR_MP_Q) sm.win[M + i] = sm.cur[i];
+                for (int i = tid; i < cnt; i += KR_MP_W * KR_MP_Q) {
+                    sm.e[i] = w.oe[base + i];
+                    sm.off8[i] = w.ob2[base + i] * 8;
+                    sm.arg[i] = w.oarg[base + i];
+                }
+                __syncthreads();
+                const int x0 = cnt * qtr / KR_MP_Q, x1 = cnt * (qtr + 1) / KR_MP_Q;
+                const char *wl = (const char *)(sm.win + t + M);  // window entry of bin b
+                int bx = -1;
+#pragma unroll 4
+                for (int x = x0; x < x1; ++x) {
+                    const double v = *(const double *)(wl - sm.off8[x]) + sm.e[x];
+                    bx = v < best ? x : bx;
+                    best = v < best ? v : best;
+                }
+                sm.pbest[qtr][t] = best;
+                sm.pwho[qtr][t] = bx >= 0 ? sm.arg[bx] : -1;
+                __syncthreads();
+                if (qtr == 0) {
+                    who = sm.pwho[0][t];
+#pragma unroll
+                    for (int q = 1; q < KR_MP_Q; ++q) {
+                        const double v = sm.pbest[q][t];
+                        if (v < best) {
+                            best = v;
+                            who = sm.pwho[q][t];
+                        }
+                    }
+                }
+            } else if (qtr == 0) {
+                // offsets beyond the window: each bin walks the records itself, reading
+                // its own tile's F from LDS and the rest from the step history
+                for (int x = 0; x < cnt; ++x) {
+                    const int64_t src = b - w.ob2[base + x];
+                    if (src >= 0 && src < Lprev) {
+                        const double f = src >= b0 ? sm.cur[src - b0] : load_l2(Fp + src);
+                        const double v = f + w.oe[base + x];
+                        if (v < best) {
+                            best = v;
+                            who = w.oarg[base + x];
+                        }
+                    }
+                }
+            }
+        }
+        __syncthreads();  // every read of cur and of the window is done
+        if (qtr == 0) {
+            const bool live = b < Lcur;
+            const double v = live ? best : INFINITY;
+            sm.cur[t] = v;
+            if (b < B) {
+                a.bp[(int64_t)k * B + b] = live ? who : -1;
+                if (last) a.F_out[b] = v;
+                else if (b0 < Lcur) store_dev(Fh + (int64_t)k * B + b, v);
+            }
+        }
+        publish(k);
+    }
+    if (sm.bad && tid == 0) {
+        *a.status = KR_EHIP;
+        store_dev(done + g, P);  // release whoever waits on this tile
+    }
+}
+
 // Exclusive scan over a block of NT threads (NT / 64 waves); *total gets the aggregate.
 // Every thread must call.  lds holds NT / 64 values.
 template <int NT, typename T, typename Op>
@@ -362,6 +543,28 @@ __global__ void __launch_bounds__(KR_ST_NT) staircase_kernel(ComposeArgs a)
     if (threadIdx.x == 0) *a.n_stair = n;
 }
 
+// Whether G wavefront blocks can all be resident at once on the current device (a
+// cooperative launch needs it); asked once per device.
+static bool wavefront_fits(int G)
+{
+    static int cap[64];
+    static bool known[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
+    if (!known[dev]) {
+        int coop = 0, cus = 0, per_cu = 0;
+        cap[dev] = 0;
+        if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess &&
+            coop &&
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &per_cu, (const void *)minplus_wavefront_kernel, KR_MP_W * KR_MP_Q, 0) == hipSuccess)
+            cap[dev] = per_cu * cus;
+        known[dev] = true;
+    }
+    return G <= cap[dev];
+}
+
 hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipEvent_t *minplus_ev,
                           hipStream_t st)
 {
@@ -369,18 +572,31 @@ hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipEvent_t *
     hipLaunchKernelGGL(compose_range_kernel, dim3(a.P), dim3(KR_BLOCK), 0, st, a, w);
     hipLaunchKernelGGL(compose_setup_kernel, dim3(1), dim3(KR_BLOCK), 0, st, a, w);
     hipLaunchKernelGGL(compose_bin_kernel, dim3(a.P), dim3(KR_BLOCK), 0, st, a, w);
-    const dim3 grid((a.B + KR_BLOCK - 1) / KR_BLOCK);
-    double *buf[2] = {w.F0, w.F1};
-    double *prev = a.P == 1 ? a.F_out : buf[0];
-    hipLaunchKernelGGL(compose_first_kernel, grid, dim3(KR_BLOCK), 0, st, a, w, prev);
-    if (minplus_ev) (void)hipEventRecord(minplus_ev[0], st);
-    for (int k = 1; k < a.P; ++k) {
-        double *cur = (k == a.P - 1) ? a.F_out : buf[k % 2];
-        hipLaunchKernelGGL(minplus_tile_kernel, dim3((a.B + KR_MP_W - 1) / KR_MP_W),
-                           dim3(KR_MP_W * KR_MP_Q), 0, st, a, w, k, (const double *)prev, cur);
-        prev = cur;
+    const int G = (a.B + KR_MP_W - 1) / KR_MP_W;
+    if (w.Fh && wavefront_fits(G)) {
+        hipLaunchKernelGGL(wavefront_init_kernel, dim3((G + KR_BLOCK - 1) / KR_BLOCK),
+                           dim3(KR_BLOCK), 0, st, w.done, G);
+        if (minplus_ev) (void)hipEventRecord(minplus_ev[0], st);
+        void *args[] = {(void *)&a, (void *)&w};
+        const hipError_t e = hipLaunchCooperativeKernel((const void *)minplus_wavefront_kernel,
+                                                        dim3(G), dim3(KR_MP_W * KR_MP_Q), args,
+                                                        0, st);
+        if (e != hipSuccess) return e;
+        if (minplus_ev) (void)hipEventRecord(minplus_ev[1], st);
+    } else {
+        const dim3 grid((a.B + KR_BLOCK - 1) / KR_BLOCK);
+        double *buf[2] = {w.F0, w.F1};
+        double *prev = a.P == 1 ? a.F_out : buf[0];
+        hipLaunchKernelGGL(compose_first_kernel, grid, dim3(KR_BLOCK), 0, st, a, w, prev);
+        if (minplus_ev) (void)hipEventRecord(minplus_ev[0], st);
+        for (int k = 1; k < a.P; ++k) {
+            double *cur = (k == a.P - 1) ? a.F_out : buf[k % 2];
+            hipLaunchKernelGGL(minplus_tile_kernel, dim3(G), dim3(KR_MP_W * KR_MP_Q), 0, st, a, w,
+                               k, (const double *)prev, cur);
+            prev = cur;
+        }
+        if (minplus_ev) (void)hipEventRecord(minplus_ev[1], st);
     }
-    if (minplus_ev) (void)hipEventRecord(minplus_ev[1], st);
     hipLaunchKernelGGL(staircase_kernel, dim3(1), dim3(KR_ST_NT), 0, st, a);
     return hipGetLastError();
 }

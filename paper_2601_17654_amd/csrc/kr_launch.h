@@ -93,6 +93,8 @@ struct ComposeWs {
     double *oe;            // [B + P]
     int32_t *occ;          // [P]
     double *F0, *F1;       // [B]
+    double *Fh;            // [P][B] step history of the wavefront min-plus (or null)
+    int32_t *done;         // [ceil(B / 256)] last finished step of each tile
 };
 struct ComposeArgs {
     int P, B;
