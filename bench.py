@@ -34,7 +34,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 FP64_VECTOR_TFLOPS = 78.6
 COUNTERS = os.path.join(ROOT, "profiles", "eval_filter_counters_eval_stress.txt")
-KERNEL_SOURCES = ["eval_wave.hip", "kr_filter.h", "kr_device.h", "kr_launch.h", "api.hip"]
+KERNEL_SOURCES = ["eval_wave.hip", "kr_filter.h", "kr_device.h", "kr_wave.h", "kr_launch.h", "api.hip"]
 METRIC = "schedule candidates evaluated+filtered/sec and frontier cells/sec on 1 MI355X"
 
 
