@@ -304,16 +304,16 @@ size_t kr_compose_frontiers_workspace(int32_t n_parts, int32_t n_bins)
     c.take<int64_t>(P);
     c.take<int64_t>(P);
     c.take<int64_t>(P + 1);
-    c.take<uint64_t>(B + P);
-    c.take<int32_t>(B + P);
-    c.take<int32_t>(B + P);
-    c.take<int32_t>(B + P);
-    c.take<double>(B + P);
+    c.take<int64_t>(1);
+    c.take<uint64_t>(B + 8 * P);
+    c.take<int32_t>(B + 8 * P);
+    c.take<int32_t>(B + 8 * P);
+    c.take<int32_t>(B + 8 * P);
+    c.take<double>(B + 8 * P);
     c.take<int32_t>(P);
     c.take<double>(B);
     c.take<double>(B);
     c.take<double>(P * B);
-    c.take<int32_t>((B + 255) / 256);
     return c.used;
 }
 
@@ -337,16 +337,16 @@ kr_status kr_compose_frontiers(int32_t n_parts, const int64_t *off, const double
     w.Mk = c.take<int64_t>(P);
     w.Lk = c.take<int64_t>(P);
     w.eoff = c.take<int64_t>(P + 1);
-    w.ebits = c.take<uint64_t>(B + P);
-    w.earg = c.take<int32_t>(B + P);
-    w.ob2 = c.take<int32_t>(B + P);
-    w.oarg = c.take<int32_t>(B + P);
-    w.oe = c.take<double>(B + P);
+    w.mmax = c.take<int64_t>(1);
+    w.ebits = c.take<uint64_t>(B + 8 * P);
+    w.earg = c.take<int32_t>(B + 8 * P);
+    w.ob2 = c.take<int32_t>(B + 8 * P);
+    w.oarg = c.take<int32_t>(B + 8 * P);
+    w.oe = c.take<double>(B + 8 * P);
     w.occ = c.take<int32_t>(P);
     w.F0 = c.take<double>(B);
     w.F1 = c.take<double>(B);
     w.Fh = c.take<double>(P * B);
-    w.done = c.take<int32_t>((B + 255) / 256);
     ComposeArgs a;
     a.P = n_parts;
     a.B = n_bins;

@@ -12,6 +12,7 @@
 // min-plus keeps the smallest b2 (strict comparisons in ascending order).
 #include "kr_launch.h"
 #include "kr_device.h"
+#include "kr_wave.h"
 
 namespace kr {
 
@@ -20,6 +21,9 @@ struct MinF64 {
 };
 struct MaxF64 {
     __device__ __forceinline__ double operator()(double a, double b) const { return b > a ? b : a; }
+};
+struct MaxI64 {
+    __device__ __forceinline__ int64_t operator()(int64_t a, int64_t b) const { return b > a ? b : a; }
 };
 
 __device__ __forceinline__ uint64_t load_l2(const uint64_t *p)
@@ -108,19 +112,23 @@ __global__ void __launch_bounds__(KR_BLOCK) compose_setup_kernel(ComposeArgs a, 
     }
     __syncthreads();
     int64_t carry = 0;  // sum of M over earlier chunks
+    int64_t mx = 0;     // largest M seen by this thread
     for (int k0 = 0; k0 < P; k0 += KR_BLOCK) {
         const int k = k0 + threadIdx.x;
         const int64_t m = k < P ? w.Mk[k] : 0;
+        mx = m > mx ? m : mx;
         int64_t tot;
         const int64_t ex = block_exclusive(m, (int64_t)0, SumI64(), sc, &tot);
         if (k < P) {
             w.Lk[k] = 1 + carry + ex + m;  // 1 + sum_{j<=k} M_j
-            w.eoff[k] = carry + ex + k;    // sum_{j<k} (M_j + 1)
+            w.eoff[k] = carry + ex + 8 * (int64_t)k;  // sum_{j<k} (M_j + 8)
         }
         carry += tot;
     }
+    mx = block_reduce(mx, (int64_t)0, MaxI64(), sc);
     if (threadIdx.x == 0) {
-        w.eoff[P] = carry + P;
+        *w.mmax = mx;
+        w.eoff[P] = carry + 8 * (int64_t)P;
         a.info[0] = delta;
         a.info[1] = s_tsum;
         *a.L_out = (int32_t)(1 + carry);
@@ -175,6 +183,10 @@ __device__ __forceinline__ void bin_partition(const ComposeArgs &a, const Compos
         carry += tot;
     }
     if (threadIdx.x == 0) w.occ[k] = carry;
+    if (threadIdx.x < 7) {  // the table runs on to a multiple of 8 past M with empty offsets
+        w.ebits[eo + M + 1 + threadIdx.x] = KR_INF_BITS;
+        w.earg[eo + M + 1 + threadIdx.x] = 0x7FFFFFFF;
+    }
 }
 
 __global__ void __launch_bounds__(KR_BLOCK) compose_bin_kernel(ComposeArgs a, ComposeWs w)
@@ -298,181 +310,407 @@ minplus_tile_kernel(ComposeArgs a, ComposeWs w, int k, const double *Fprev, doub
 // All min-plus steps in one launch, as a wavefront over (tile, step).  Block g owns
 // the KR_MP_W bins of tile g for every step: F_k of its own bins stays in LDS from one
 // step to the next, and the halo F_{k-1}[b0 - M_k, b0) comes from the tiles on its
-// left, which publish every step's values to the step history Fh[k][b] and then
-// raise done[tile] = k.  Tile g can run step k as soon as those tiles have finished
-// step k - 1, so the tiles advance as a diagonal front: a step costs one tile's
-// compute, and the latency of a hand-over is paid once per tile, not once per step.
-// The grid is launched cooperatively (every block resident), so a wait always ends;
-// a wait that still exceeds KR_WF_POLLS polls marks the result invalid and releases
-// the blocks waiting on this one.
+// left through the step history Fh[k][b].  A tile publishes only what other tiles read:
+// row k, its bins within M_{k+1} of its right edge and below L_k.  Before the launch
+// those entries are set to KR_UNSET, a NaN pattern no step writes; a reader loads an
+// entry until it holds something else, so every value is its own ready flag and a
+// hand-over costs one store and one load.  Tile g runs step k as soon as the tiles on
+// its left have finished step k - 1, so the tiles advance as a diagonal front.  The
+// next step's halo and records are loaded while the current step computes.
 //
-// Hand-over: values and flags are written and read with device-scope relaxed atomic
-// accesses, which are coherent across the chip without cache maintenance; a block
-// waits for its value stores to complete before it raises its flag, and reads the
-// values only after it has seen the flag.
+// The grid is launched cooperatively (every block resident), so a wait always ends; a
+// wait that still exceeds KR_WF_POLLS polls sets the status to KR_EHIP, and every other
+// waiter gives up as soon as it sees that status.  Entries are written and read with
+// device-scope relaxed atomic accesses, which are coherent across the chip without
+// cache maintenance; each is written at most once per launch, after the fill kernel.
 #define KR_WF_POLLS (1 << 22)
+#define KR_UNSET 0x7FF4B1A5C0DE0000ull
 
-__device__ __forceinline__ void store_dev(double *p, double v)
+__device__ __forceinline__ void store_dev(uint64_t *p, uint64_t v)
 {
-    __hip_atomic_store((uint64_t *)p, dbits(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void store_dev(int32_t *p, int32_t v)
 {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-struct WavefrontLds {
-    double win[KR_MP_W + KR_MP_HCAP];  // F_{k-1}[b0 - M_k, b0 + KR_MP_W)
-    double cur[KR_MP_W];               // F of the tile's own bins, last finished step
-    double e[KR_MP_HCAP + 1];
-    int32_t off8[KR_MP_HCAP + 1];  // b2 * 8: byte offset into the window
-    int32_t arg[KR_MP_HCAP + 1];
-    double pbest[KR_MP_Q][KR_MP_W];
-    int32_t pwho[KR_MP_Q][KR_MP_W];
-    int32_t bad;  // a wait gave up
-};
-
-__global__ void wavefront_init_kernel(int32_t *done, int G)
+// Whether bin x of row k is read by another tile: within M_{k+1} of its tile's right
+// edge and below L_k (M1 = M_{k+1}, L = L_k).
+__device__ __forceinline__ bool exported(int64_t x, int64_t M1, int64_t L)
 {
-    const int g = blockIdx.x * blockDim.x + threadIdx.x;
-    if (g < G) done[g] = -1;
+    return x < L && (x % KR_MP_W) >= KR_MP_W - M1;
 }
 
+// Marks every entry of the step history that some tile will publish as unwritten.
+// One block per row k = 0 .. P-2.
+__global__ void __launch_bounds__(KR_BLOCK) wavefront_fill_kernel(ComposeArgs a, ComposeWs w)
+{
+    if (*a.status != KR_OK) return;
+    const int k = blockIdx.x;
+    const int64_t L = min(w.Lk[k], (int64_t)a.B), M1 = w.Mk[k + 1];
+    uint64_t *row = (uint64_t *)w.Fh + (int64_t)k * a.B;
+    for (int64_t x = threadIdx.x; x < L; x += KR_BLOCK)
+        if (exported(x, M1, L)) row[x] = KR_UNSET;
+}
+
+#define KR_WF_MC 512  // steps per chunk of the block's step-metadata ring
+#define KR_WF_LO 8    // window entries below offset H (read only by padding offsets)
+#define KR_WF_S 8     // offset slices of the dense scan (block = 128 bin pairs x 8 slices)
+
+struct WavefrontLds {
+    // Window of step k in buffer k & 1: win[LO + H + i] = F_{k-1}[b0 + i] for i in
+    // [-M_k, W), the halo and then the tile's own bins.
+    double win[2][KR_WF_LO + KR_MP_HCAP + KR_MP_W];
+    // Records of step k in buffer k & 1: the dense least-energy table e_k[0 .. 8
+    // ceil((M_k + 1) / 8)) (INFINITY past M_k) with its points, or the occupied offsets
+    // only (b2 * 8 in off8).
+    double e[2][KR_MP_HCAP + 8];
+    int32_t off8[2][KR_MP_HCAP + 8];
+    int32_t arg[2][KR_MP_HCAP + 8];
+    double pbest[KR_WF_S][KR_MP_W];  // partial minima per slice (or quarter) and bin
+    int32_t pidx[KR_WF_S][KR_MP_W];  // their 8-offset group (dense) or point (sparse)
+    int4 meta[2][KR_WF_MC];  // (M_k, L_k, first record, records) at [(k / MC) & 1][k % MC]
+    int32_t bad;             // a wait was given up
+};
+
+// Whether step k scans its dense offset table (about 2.25 instructions per pair) rather
+// than its occupied offsets (about 7 per pair).
+__device__ __forceinline__ bool dense_step(int4 m) { return 18 * ((m.x + 8) / 8) <= 7 * m.w; }
+
+typedef const __attribute__((address_space(4))) double const_f64;
+
+// Roles inside a block: the first KR_MP_W threads (four waves) combine the partial
+// minima and store the step's results; the other threads load the next step's records
+// and halo while the step computes and move them into LDS at its end.  The two never
+// mix, so a wave that stores never has to wait for its stores to complete, and a wave
+// that waits for its loads has no stores in flight (one in-order counter covers both).
 __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(ComposeArgs a, ComposeWs w)
 {
+    constexpr int NT = KR_MP_W * KR_MP_Q, H = KR_MP_HCAP, MC = KR_WF_MC, LO = KR_WF_LO;
+    constexpr int NS = NT - KR_MP_W;  // loader threads
     __shared__ WavefrontLds sm;
     if (*a.status != KR_OK) return;  // the same for every block
-    const int tid = threadIdx.x, t = tid % KR_MP_W, qtr = tid / KR_MP_W;
-    const int g = blockIdx.x;
+    const int tid = threadIdx.x, t = tid % KR_MP_W;
+    const int qtr = __builtin_amdgcn_readfirstlane(tid / KR_MP_W);
+    const bool loader = qtr != 0;
+    const int s = tid - KR_MP_W;  // loader index
     const int P = a.P, B = a.B;
-    const int64_t b0 = (int64_t)g * KR_MP_W, b = b0 + t;
-    double *const Fh = w.Fh;
-    int32_t *const done = w.done;
-    if (tid == 0) sm.bad = 0;
+    const int64_t b0 = (int64_t)blockIdx.x * KR_MP_W, b = b0 + t;
+    uint64_t *const Fh = (uint64_t *)w.Fh;
+    auto window = [&](int k) { return sm.win[k & 1] + LO + H; };  // window(k)[i] = F_{k-1}[b0 + i]
 
-    // Waits until tiles [lo, g) have finished step k; false if a wait gave up.
-    auto wait_left = [&](int lo, int k) {
-        if (tid == 0) {
-            for (int tt = lo; tt < g && !sm.bad; ++tt) {
-                int polls = 0;
-                while (load_l2(done + tt) < k) {
-                    if (++polls > KR_WF_POLLS) {
-                        sm.bad = 1;
-                        break;
-                    }
+    auto load_meta = [&](int c) {  // chunk c of the step metadata into its ring slot
+        for (int i = s; i < MC; i += NS) {
+            const int k = c * MC + i;
+            if (k < P)
+                sm.meta[c & 1][i] = make_int4((int)w.Mk[k], (int)w.Lk[k], (int)w.eoff[k], w.occ[k]);
+        }
+    };
+    auto meta = [&](int k) { return sm.meta[(k / MC) & 1][k % MC]; };  // x M, y L, z base, w count
+    if (tid == 0) sm.bad = 0;
+    for (int i = tid; i < 2 * (LO + H); i += NT)  // read by padding offsets only
+        sm.win[i / (LO + H)][i % (LO + H)] = INFINITY;
+    if (loader) {
+        load_meta(0);
+        load_meta(1);
+    }
+    __syncthreads();
+
+    auto gave_up = [&]() {
+        return __hip_atomic_load(&sm.bad, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) != 0;
+    };
+    // Value of the published entry *p, first loaded as v: loads it again until it has
+    // been written.  INFINITY once waiting has been given up.
+    auto fetch = [&](const uint64_t *p, uint64_t v) -> double {
+        for (int polls = 1; v == KR_UNSET; ++polls) {
+            if (gave_up()) return INFINITY;
+            if (polls % 1024 == 0) {
+                const bool over = polls > KR_WF_POLLS;
+                if (over) store_dev(a.status, (int32_t)KR_EHIP);
+                if (over || load_l2(a.status) != KR_OK) {
+                    __hip_atomic_store(&sm.bad, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                    return INFINITY;
+                }
+            }
+            __builtin_amdgcn_s_sleep(1);
+            v = load_l2(p);
+        }
+        return bitsd(v);
+    };
+
+    // Loader registers: the next step's records and halo entries.  The loads are
+    // unconditional (a thread with nothing to load reads a valid dummy address).
+    uint64_t hv[2], re[2];
+    int32_t ro[2], ra[2];
+    auto halo_src = [&](int4 m, int Lprev, int h, int64_t &src) {
+        const int i = s + h * NS;
+        src = b0 - m.x + i;
+        return m.x <= H && i < m.x && src >= 0 && src < Lprev;
+    };
+    auto issue = [&](int k, int4 m, int Lprev) {  // loads for step k
+        const bool dense = dense_step(m);
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            const int i = s + r * NS;
+            const int64_t xd = m.z + max(0, min(i, m.x + 7)), xs = m.z + max(0, min(i, m.w - 1));
+            re[r] = dense ? w.ebits[xd] : *(const uint64_t *)(w.oe + xs);
+            ra[r] = *(dense ? w.earg + xd : w.oarg + xs);
+            ro[r] = w.ob2[xs];
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            int64_t src;
+            const bool need = halo_src(m, Lprev, h, src);
+            hv[h] = load_l2(Fh + (int64_t)(k - 1) * B + (need ? src : 0));
+        }
+    };
+    auto stage = [&](int k, int4 m, int Lprev) {  // the loads of issue(k) into LDS
+        const int buf = k & 1;
+        const int n = dense_step(m) ? 8 * ((m.x + 8) / 8) : m.w;
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            const int i = s + r * NS;
+            if (i < n) {
+                sm.e[buf][i] = bitsd(re[r]);
+                sm.off8[buf][i] = ro[r] * 8;
+                sm.arg[buf][i] = ra[r];
+            }
+        }
+        if (b0 < m.y) {
+            double *const wn = window(k);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                int64_t src;
+                const int i = s + h * NS;
+                if (i < m.x) {
+                    const bool need = halo_src(m, Lprev, h, src);
+                    wn[i - m.x] = need ? fetch(Fh + (int64_t)(k - 1) * B + src, hv[h]) : INFINITY;
                 }
             }
         }
-        __syncthreads();
-        return !sm.bad;
+        asm volatile("" ::"v"(hv[0]), "v"(hv[1]), "v"(re[0]), "v"(re[1]), "v"(ro[0]), "v"(ro[1]),
+                     "v"(ra[0]), "v"(ra[1]));
     };
-    // Every thread's value stores are complete before the flag goes up.
-    auto publish = [&](int k) {
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);  // the stores stay before the wait
-        __builtin_amdgcn_s_waitcnt(0x0F70);       // vmcnt(0)
-        __syncthreads();
-        if (tid == 0) store_dev(done + g, k);
+    // Whether this loader wave has records or halo entries of step k to move (most
+    // loader waves have none when the offset range is short).
+    const int ws = __builtin_amdgcn_readfirstlane(s & ~63);
+    auto busy = [&](int4 m) { return ws < max(dense_step(m) ? 8 * ((m.x + 8) / 8) : m.w, m.x); };
+    auto publish = [&](int k, double v, int M1, int L) {
+        uint64_t bits = dbits(v);
+        if (bits == KR_UNSET) bits = 0x7FF8000000000000ull;  // keep the marker unique
+        if (exported(b, M1, L)) store_dev(Fh + (int64_t)k * B + b, bits);
     };
 
-    // step 0: F_1 = e_1
-    if (qtr == 0) {
+    // step 0: F_1 = e_1, into the window of step 1
+    const int4 m0 = meta(0);
+    if (!loader) {
         double v = INFINITY;
         int32_t who = -1;
-        if (b < B && b <= w.Mk[0]) {
+        if (b < B && b <= m0.x) {
             const int32_t arg = w.earg[b];
             if (arg != 0x7FFFFFFF) {
                 v = bitsd(w.ebits[b]);
                 who = arg;
             }
         }
-        sm.cur[t] = v;
+        window(1)[t] = v;
         if (b < B) {
             a.bp[b] = who;
             if (P == 1) a.F_out[b] = v;
-            else store_dev(Fh + b, v);
+            else publish(0, v, meta(1).x, m0.y);
         }
     }
-    publish(0);
 
+    if (*w.mmax > H) {
+        // Some partition's offsets do not fit the window: every combining thread walks
+        // all records of its bin, reading its own tile's F from LDS and the rest from
+        // the step history.  The loops of the two modes share no code.
+        int4 mc = m0;
+        for (int k = 1; k < P; ++k) {
+            __syncthreads();  // F_{k-1} of the tile and the metadata of step k are in LDS
+            const int4 mp = mc;
+            mc = meta(k);
+            const bool last = k == P - 1;
+            const int M1 = last ? 0 : meta(k + 1).x;
+            const double *const wc = window(k);
+            double best = INFINITY;
+            int32_t who = -1;
+            if (!loader && b0 < mc.y) {
+                for (int x = 0; x < mc.w; ++x) {
+                    const int64_t src = b - w.ob2[mc.z + x];
+                    if (src >= 0 && src < mp.y) {
+                        const uint64_t *p = Fh + (int64_t)(k - 1) * B + src;
+                        const double f = src >= b0 ? wc[src - b0] : fetch(p, load_l2(p));
+                        const double v = f + w.oe[mc.z + x];
+                        if (v < best) {
+                            best = v;
+                            who = w.oarg[mc.z + x];
+                        }
+                    }
+                }
+            }
+            __syncthreads();  // the metadata of step k has been read
+            if (!loader) {
+                const bool live = b < mc.y;
+                const double v = live ? best : INFINITY;
+                window(k + 1)[t] = v;
+                if (b < B) {
+                    a.bp[(int64_t)k * B + b] = live ? who : -1;
+                    if (last) a.F_out[b] = v;
+                    else publish(k, v, M1, mc.y);
+                }
+            } else if ((k + 1) % MC == 0) {
+                load_meta((k + 1) / MC + 1);  // replaces chunk (k + 1) / MC - 1
+            }
+        }
+        return;
+    }
+
+    if (loader && P > 1 && busy(meta(1))) {
+        issue(1, meta(1), m0.y);
+        stage(1, meta(1), m0.y);
+    }
+    // The point behind bin b0 + u's least value best of step k: the part's point (sparse)
+    // or the first offset of 8-offset group idx that reaches best (dense).
+    auto point = [&](int k, double best, int idx, bool dense, int u) -> int32_t {
+        if (!dense || idx < 0) return idx;
+        const double *const wp = window(k);
+        const double *const ep = sm.e[k & 1];
+        const int i8 = 8 * idx;
+        int o = 7;
+#pragma unroll
+        for (int d = 7; d >= 0; --d) o = wp[u - i8 - d] + ep[i8 + d] == best ? d : o;
+        return sm.arg[k & 1][i8 + o];
+    };
+    // Least value and its part's index for bin b0 + u from the partial minima.
+    auto combine = [&](bool dense, int u, double &best, int32_t &idx) {
+        double pv[KR_WF_S];
+        int32_t pi[KR_WF_S];
+#pragma unroll
+        for (int q = 0; q < KR_WF_S; ++q) {  // all read at once; a sparse step fills KR_MP_Q
+            pv[q] = sm.pbest[q][u];
+            pi[q] = sm.pidx[q][u];
+        }
+        best = INFINITY;
+        idx = -1;
+#pragma unroll
+        for (int q = 0; q < KR_WF_S; ++q) {  // the first part (in offset order) with the least
+            if ((dense || q < KR_MP_Q) && pv[q] < best) {
+                best = pv[q];
+                idx = pi[q];
+            }
+        }
+    };
     for (int k = 1; k < P; ++k) {
-        const int64_t Lprev = w.Lk[k - 1], Lcur = w.Lk[k];
-        const int64_t M = w.Mk[k];
-        const int cnt = w.occ[k];
-        const int64_t base = w.eoff[k];
+        __syncthreads();  // window and records of step k are in LDS
+        const int4 mc = meta(k);
         const bool last = k == P - 1;
-        double best = INFINITY;
-        int32_t who = -1;
-        if (b0 < Lcur) {
-            const int lo = (int)(max((int64_t)0, b0 - M) / KR_MP_W);
-            if (!wait_left(lo, k - 1)) break;
-            const double *Fp = Fh + (int64_t)(k - 1) * B;
-            if (M <= KR_MP_HCAP) {
-                for (int i = tid; i < M; i += KR_MP_W * KR_MP_Q) {
-                    const int64_t src = b0 - M + i;
-                    sm.win[i] = src >= 0 && src < Lprev ? load_l2(Fp + src) : INFINITY;
+        const bool active = b0 < mc.y;
+        const bool dense = dense_step(mc);
+        const int4 mn = meta(last ? k : k + 1);
+        const bool moves = loader && !last && busy(mn);
+        if (moves) issue(k + 1, mn, mc.y);
+        const int buf = k & 1;
+        const double *const wc = window(k);
+        if (active) {
+            if (dense) {
+                // Thread (pair j, slice q): bins 2j and 2j + 1 over the slice's groups of
+                // 8 offsets.  A group needs 9 window entries and 8 table entries, which
+                // come from memory through the scalar cache (the table does not change
+                // during the launch).  The running minimum takes one v_min per pair; the
+                // group where it last fell is kept and rescanned when combining.
+                const int j = tid % (KR_MP_W / 2);
+                const int q = __builtin_amdgcn_readfirstlane(tid / (KR_MP_W / 2));
+                const int ng = (mc.x + 8) / 8;
+                const int g0 = ng * q / KR_WF_S, g1 = ng * (q + 1) / KR_WF_S;
+                const_f64 *et = (const_f64 *)(w.ebits + mc.z);
+                double best0 = INFINITY, best1 = INFINITY;
+                int bg0 = -1, bg1 = -1;
+                // one group of 8 offsets: updates the two running minima
+                auto group = [&](int g, const double *x, const double *e) {
+                    double v0[8], v1[8];  // offset 8g + o for bins 2j and 2j + 1
+#pragma unroll
+                    for (int o = 0; o < 8; ++o) {
+                        v0[o] = x[7 - o] + e[o];
+                        v1[o] = x[8 - o] + e[o];
+                    }
+                    const double m0v = vmin(vmin(vmin(v0[0], v0[1]), vmin(v0[2], v0[3])),
+                                            vmin(vmin(v0[4], v0[5]), vmin(v0[6], v0[7])));
+                    const double m1v = vmin(vmin(vmin(v1[0], v1[1]), vmin(v1[2], v1[3])),
+                                            vmin(vmin(v1[4], v1[5]), vmin(v1[6], v1[7])));
+                    bg0 = m0v < best0 ? g : bg0;
+                    bg1 = m1v < best1 ? g : bg1;
+                    best0 = vmin(best0, m0v);
+                    best1 = vmin(best1, m1v);
+                };
+                // Two groups a round, their loads issued together; an odd last round
+                // repeats its group, which cannot lower a minimum twice.
+                for (int g = g0; g < g1; g += 2) {
+                    const int h = min(g + 1, g1 - 1);
+                    const double *wa = wc + 2 * j - 8 * g - 7, *wb = wc + 2 * j - 8 * h - 7;
+                    double xa[9], xb[9], ea[8], eb[8];  // xa[d]: F at bin 2j + d - 7 - 8g
+#pragma unroll
+                    for (int d = 0; d < 9; ++d) {
+                        xa[d] = wa[d];
+                        xb[d] = wb[d];
+                    }
+#pragma unroll
+                    for (int o = 0; o < 8; ++o) {
+                        ea[o] = et[8 * g + o];
+                        eb[o] = et[8 * h + o];
+                    }
+                    group(g, xa, ea);
+                    group(h, xb, eb);
                 }
-                for (int i = tid; i < KR_MP_W; i += KR_MP_W * KR_MP_Q) sm.win[M + i] = sm.cur[i];
-                for (int i = tid; i < cnt; i += KR_MP_W * KR_MP_Q) {
-                    sm.e[i] = w.oe[base + i];
-                    sm.off8[i] = w.ob2[base + i] * 8;
-                    sm.arg[i] = w.oarg[base + i];
-                }
-                __syncthreads();
-                const int x0 = cnt * qtr / KR_MP_Q, x1 = cnt * (qtr + 1) / KR_MP_Q;
-                const char *wl = (const char *)(sm.win + t + M);  // window entry of bin b
+                sm.pbest[q][2 * j] = best0;
+                sm.pbest[q][2 * j + 1] = best1;
+                sm.pidx[q][2 * j] = bg0;
+                sm.pidx[q][2 * j + 1] = bg1;
+            } else {
+                const int x0 = mc.w * qtr / KR_MP_Q, x1 = mc.w * (qtr + 1) / KR_MP_Q;
+                const char *wl = (const char *)(wc + t);
+                double best = INFINITY;
                 int bx = -1;
 #pragma unroll 4
                 for (int x = x0; x < x1; ++x) {
-                    const double v = *(const double *)(wl - sm.off8[x]) + sm.e[x];
+                    const double v = *(const double *)(wl - sm.off8[buf][x]) + sm.e[buf][x];
                     bx = v < best ? x : bx;
                     best = v < best ? v : best;
                 }
                 sm.pbest[qtr][t] = best;
-                sm.pwho[qtr][t] = bx >= 0 ? sm.arg[bx] : -1;
-                __syncthreads();
-                if (qtr == 0) {
-                    who = sm.pwho[0][t];
-#pragma unroll
-                    for (int q = 1; q < KR_MP_Q; ++q) {
-                        const double v = sm.pbest[q][t];
-                        if (v < best) {
-                            best = v;
-                            who = sm.pwho[q][t];
-                        }
-                    }
-                }
-            } else if (qtr == 0) {
-                // offsets beyond the window: each bin walks the records itself, reading
-                // its own tile's F from LDS and the rest from the step history
-                for (int x = 0; x < cnt; ++x) {
-                    const int64_t src = b - w.ob2[base + x];
-                    if (src >= 0 && src < Lprev) {
-                        const double f = src >= b0 ? sm.cur[src - b0] : load_l2(Fp + src);
-                        const double v = f + w.oe[base + x];
-                        if (v < best) {
-                            best = v;
-                            who = w.oarg[base + x];
-                        }
-                    }
-                }
+                sm.pidx[qtr][t] = bx >= 0 ? sm.arg[buf][bx] : -1;
             }
         }
-        __syncthreads();  // every read of cur and of the window is done
-        if (qtr == 0) {
-            const bool live = b < Lcur;
+        __syncthreads();  // every partial minimum is in LDS
+        if (!loader) {
+            double best = INFINITY;
+            int32_t idx = -1;
+            if (active) combine(dense, t, best, idx);
+            const bool live = b < mc.y;
             const double v = live ? best : INFINITY;
-            sm.cur[t] = v;
+            window(k + 1)[t] = v;
             if (b < B) {
-                a.bp[(int64_t)k * B + b] = live ? who : -1;
                 if (last) a.F_out[b] = v;
-                else if (b0 < Lcur) store_dev(Fh + (int64_t)k * B + b, v);
+                else publish(k, v, mn.x, mc.y);
+            }
+            const int32_t who = active ? point(k, best, idx, dense, t) : -1;
+            if (b < B) a.bp[(int64_t)k * B + b] = live ? who : -1;
+        } else if (!last) {
+            // chunk c + 1 replaces chunk c - 1 once step cMC - 1 has read its metadata
+            if ((k + 1) % MC == 0) load_meta((k + 1) / MC + 1);
+            if (moves) stage(k + 1, mn, mc.y);
+            if (dense_step(mn) && b0 < mn.y) {
+                // bring the next step's table into the scalar cache, where the dense
+                // scan reads it: the first and last entry of each group of 8
+                const_f64 *et = (const_f64 *)(w.ebits + mn.z);
+                const int ng = (mn.x + 8) / 8;
+                for (int g = ws / 64; g < ng; g += NS / 64) {
+                    const double e0 = et[8 * g], e7 = et[8 * g + 7];
+                    asm volatile("" ::"s"(e0), "s"(e7));
+                }
             }
         }
-        publish(k);
-    }
-    if (sm.bad && tid == 0) {
-        *a.status = KR_EHIP;
-        store_dev(done + g, P);  // release whoever waits on this tile
     }
 }
 
@@ -574,8 +812,8 @@ hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipEvent_t *
     hipLaunchKernelGGL(compose_bin_kernel, dim3(a.P), dim3(KR_BLOCK), 0, st, a, w);
     const int G = (a.B + KR_MP_W - 1) / KR_MP_W;
     if (w.Fh && wavefront_fits(G)) {
-        hipLaunchKernelGGL(wavefront_init_kernel, dim3((G + KR_BLOCK - 1) / KR_BLOCK),
-                           dim3(KR_BLOCK), 0, st, w.done, G);
+        if (a.P > 1)
+            hipLaunchKernelGGL(wavefront_fill_kernel, dim3(a.P - 1), dim3(KR_BLOCK), 0, st, a, w);
         if (minplus_ev) (void)hipEventRecord(minplus_ev[0], st);
         void *args[] = {(void *)&a, (void *)&w};
         const hipError_t e = hipLaunchCooperativeKernel((const void *)minplus_wavefront_kernel,

@@ -87,14 +87,16 @@ hipError_t launch_output(const SegLayout &L, const PointBufs &fin, const int32_t
 struct ComposeWs {
     double *tmin, *range;  // [P]
     int64_t *Mk, *Lk, *eoff;  // [P], [P], [P+1]
-    uint64_t *ebits;       // [B + P]
-    int32_t *earg;         // [B + P]
-    int32_t *ob2, *oarg;   // [B + P] occupied offsets / point index
-    double *oe;            // [B + P]
+    int64_t *mmax;            // [1] largest M
+    // Per partition k from eoff[k]: the least-energy table over offsets 0 .. M_k + 7
+    // (empty past M_k) and the compact list of its occupied offsets.
+    uint64_t *ebits;       // [B + 8P]
+    int32_t *earg;         // [B + 8P]
+    int32_t *ob2, *oarg;   // [B + 8P] occupied offsets / point index
+    double *oe;            // [B + 8P]
     int32_t *occ;          // [P]
     double *F0, *F1;       // [B]
     double *Fh;            // [P][B] step history of the wavefront min-plus (or null)
-    int32_t *done;         // [ceil(B / 256)] last finished step of each tile
 };
 struct ComposeArgs {
     int P, B;

@@ -233,3 +233,28 @@ def compose_frontiers(seed: int = 4, n_parts: int = 512, n_min: int = 256, n_max
     off = np.zeros(n_parts + 1, dtype=np.int64)
     off[1:] = np.cumsum([len(x) for x in T_parts])
     return off, np.concatenate(T_parts), np.concatenate(E_parts)
+
+
+def frontier_batch(seed: int, n_points: Sequence[int], t_span: Sequence[float],
+                   t0: float = 1e-3) -> tuple:
+    """Frontier-shaped partitions of chosen sizes and time spans.
+
+    Partition k has n_points[k] times t0 + t_span[k] * u (u uniform, sorted, the first
+    pinned to 0 and the last to 1 when there are two or more) and energies falling from
+    2 J by uniform decrements.  Returns (off int64[P+1], T float64[n], E float64[n]).
+    """
+    T_parts: List[np.ndarray] = []
+    E_parts: List[np.ndarray] = []
+    cursor = 0
+    for n, span in zip(n_points, t_span):
+        u = np.sort(splitmix64_uniform(seed, cursor, n))
+        cursor += n
+        if n >= 2:
+            u[0], u[-1] = 0.0, 1.0
+        d = splitmix64_uniform(seed, cursor, n)
+        cursor += n
+        T_parts.append(t0 + span * u)
+        E_parts.append(2.0 - np.cumsum(d) / n)
+    off = np.zeros(len(T_parts) + 1, dtype=np.int64)
+    off[1:] = np.cumsum([len(x) for x in T_parts])
+    return off, np.concatenate(T_parts), np.concatenate(E_parts)

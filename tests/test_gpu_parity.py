@@ -314,6 +314,30 @@ def test_end_to_end_path(kr, oracle_lib, cfg):
             assert (f[x], tuple(pos[x]), tuple(sm[x])) == (rf, rpos, rsm)
 
 
+def test_compose_wavefront_modes(kr, oracle_lib):
+    """The min-plus wavefront's record formats and modes against the oracle: occupied
+    offsets only (few points over wide spans), a partition wider than the on-chip window,
+    and more steps than two chunks of the per-block step metadata."""
+    rng = np.random.default_rng(17)
+    cases = []
+    n = rng.integers(2, 7, 48)
+    cases.append(("sparse", n, rng.uniform(1e-3, 1e-2, 48), 16384))
+    n = rng.integers(20, 60, 6)
+    n[2] = 400
+    span = rng.uniform(1e-3, 2e-3, 6)
+    span[2] = 0.08
+    cases.append(("wide", n, span, 8192))
+    n = rng.integers(10, 31, 1300)
+    cases.append(("long", n, rng.uniform(0.5e-3, 1.5e-3, 1300), 32768))
+    for i, (what, n, span, B) in enumerate(cases):
+        off, T, E = I.frontier_batch(100 + i, n.tolist(), span.tolist())
+        print("compose wavefront case", what, flush=True)
+        comp = kr.compose_frontiers(torch.from_numpy(off).cuda(), torch.from_numpy(T).cuda(),
+                                    torch.from_numpy(E).cuda(), B)
+        ref = oracle_lib.compose(off, T, E, B)
+        compare_composed(kr, comp, ref, off, T, E, what)
+
+
 def test_compose_edge_cases(kr, oracle_lib):
     cases = []
     rng = np.random.default_rng(11)
