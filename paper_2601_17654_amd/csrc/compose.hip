@@ -846,8 +846,12 @@ hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipEvent_t *
 // one while the offset is in flight, so a step costs one memory latency when the offset
 // is below KR_EX_SPEC (else one more load).
 #define KR_EX_SPEC 128
+#define KR_EX_RS 2048  // partitions per pass of the final sums
+
 __global__ void __launch_bounds__(64) extract_kernel(ExtractArgs a)
 {
+    __shared__ double sT[KR_EX_RS], sE[KR_EX_RS];
+    const int P = a.P;
     const int q = blockIdx.x, lane = threadIdx.x;
     int32_t *choice = a.choice + (int64_t)q * a.P;
     int64_t b = a.bins[q];
@@ -884,24 +888,38 @@ __global__ void __launch_bounds__(64) extract_kernel(ExtractArgs a)
         }
     }
     ok = ok && b == 0;
-    if (lane != 0) return;
+    // Exact T and E of the choice: the lanes gather the chosen points' values into LDS,
+    // one lane adds them in partition order.
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's choice stores are done
     double Ts = 0.0, Es = 0.0;
-    if (ok) {
-        for (int k = 0; k < a.P; ++k) {
-            const int64_t x = a.off[k] + choice[k];
-            Ts = Ts + a.T[x];
-            Es = Es + a.E[x];
-            if (a.cand_idx) a.choice_cand[(int64_t)q * a.P + k] = a.cand_idx[x];
+    for (int k0 = 0; k0 < P; k0 += KR_EX_RS) {
+        const int kn = min(P - k0, KR_EX_RS);
+        for (int i = lane; i < kn; i += 64) {
+            const int kk = k0 + i;
+            if (ok) {
+                const int32_t c = load_l2(choice + kk);
+                const int64_t x = a.off[kk] + c;
+                sT[i] = a.T[x];
+                sE[i] = a.E[x];
+                if (a.cand_idx) a.choice_cand[(int64_t)q * P + kk] = a.cand_idx[x];
+            } else {
+                choice[kk] = -1;
+                if (a.cand_idx) a.choice_cand[(int64_t)q * P + kk] = -1;
+            }
         }
-    } else {
-        for (int k = 0; k < a.P; ++k) {
-            choice[k] = -1;
-            if (a.cand_idx) a.choice_cand[(int64_t)q * a.P + k] = -1;
-        }
-        Ts = Es = NAN;
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        if (ok && lane == 0)
+            for (int i = 0; i < kn; ++i) {
+                Ts = Ts + sT[i];
+                Es = Es + sE[i];
+            }
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
+        __builtin_amdgcn_s_waitcnt(0xC07F);
     }
-    a.T_out[q] = Ts;
-    a.E_out[q] = Es;
+    if (lane != 0) return;
+    a.T_out[q] = ok ? Ts : NAN;
+    a.E_out[q] = ok ? Es : NAN;
     a.ok[q] = ok;
 }
 

@@ -323,9 +323,9 @@ def test_compose_wavefront_modes(kr, oracle_lib):
     n = rng.integers(2, 7, 48)
     cases.append(("sparse", n, rng.uniform(1e-3, 1e-2, 48), 16384))
     n = rng.integers(20, 60, 6)
-    n[2] = 400
+    n[2] = 3000  # more points than the walk stages per partition
     span = rng.uniform(1e-3, 2e-3, 6)
-    span[2] = 0.08
+    span[2] = 0.08  # offsets wider than the window and than the walk's look-ahead
     cases.append(("wide", n, span, 8192))
     n = rng.integers(10, 31, 1300)
     cases.append(("long", n, rng.uniform(0.5e-3, 1.5e-3, 1300), 32768))
@@ -336,6 +336,22 @@ def test_compose_wavefront_modes(kr, oracle_lib):
                                     torch.from_numpy(E).cuda(), B)
         ref = oracle_lib.compose(off, T, E, B)
         compare_composed(kr, comp, ref, off, T, E, what)
+        # schedules behind the staircase and some other reachable bins
+        sb, _, _ = comp.staircase()
+        reach = np.flatnonzero(np.isfinite(ref.F))
+        bins = np.concatenate([sb.cpu().numpy(), rng.choice(reach, size=8, replace=False),
+                               [B - 1]]).astype(np.int32)
+        ch, _, Ts, Es, ok = kr.extract_schedule(comp, off, T, E, torch.from_numpy(bins).cuda())
+        ch, Ts, Es, ok = ch.cpu().numpy(), Ts.cpu().numpy(), Es.cpu().numpy(), ok.cpu().numpy()
+        for q, bq in enumerate(bins):
+            if bq >= ref.L or not np.isfinite(ref.F[bq]):
+                assert ok[q] == 0
+                continue
+            rc, rts, res = oracle_lib.extract(off, T, E, ref, int(bq))
+            assert ok[q] == 1, (what, int(bq))
+            np.testing.assert_array_equal(ch[q], rc)
+            assert_close(Ts[q], rts, RT_TE, "%s extract T bin %d" % (what, bq))
+            assert_close(Es[q], res, RT_TE, "%s extract E bin %d" % (what, bq))
 
 
 def test_compose_edge_cases(kr, oracle_lib):
