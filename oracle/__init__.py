@@ -49,8 +49,10 @@ def _load():
         lib.oracle_compose.argtypes = [i, lp, dp, dp, i, d, dp, ip, ip, dp, ip]
         lib.oracle_staircase.argtypes = [i, dp, d, d, ip, dp, dp, ip]
         lib.oracle_extract.argtypes = [i, i, lp, dp, dp, ip, ip, ctypes.c_int32, ip, dp, dp]
+        lib.oracle_microbatch.argtypes = [i, i, lp, dp, dp, i, ip, i, dp, dp, i,
+                                          ctypes.c_int64, dp, dp, ip, ip, lp]
         for fn in ("oracle_evaluate", "oracle_pareto", "oracle_compose", "oracle_staircase",
-                   "oracle_extract"):
+                   "oracle_extract", "oracle_microbatch"):
             getattr(lib, fn).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -169,6 +171,38 @@ def extract(off, T, E, comp: Composed, bin_: int):
     if rc != 0:
         raise OracleError("oracle_extract failed for bin %d: %d" % (bin_, rc))
     return choice, ts.value, es.value
+
+
+def microbatch(seg_off, T, E, n_types: int, n_freq: int, seq, comp_T=None, comp_E=None,
+               n_bins: int = 4096):
+    """Microbatch frontier (Algorithm 2 with one frequency per microbatch and one choice
+    per partition type).  seg_off [K*F+1]: segment t*F+f holds type t's points at
+    frequency f.  comp_T, comp_E [n_comp][F] or None.
+    Returns (T, E, f int32, choice int32[n][K]) in ascending time."""
+    lib = _load()
+    seg_off = np.ascontiguousarray(seg_off, dtype=np.int64)
+    T, E = _f64(T), _f64(E)
+    seq = np.ascontiguousarray(seq, dtype=np.int32)
+    if comp_T is None:
+        cT = np.zeros((0, n_freq))
+        cE = np.zeros((0, n_freq))
+    else:
+        cT, cE = _f64(comp_T).reshape(-1, n_freq), _f64(comp_E).reshape(-1, n_freq)
+    cap = n_freq * n_bins
+    oT, oE = np.empty(cap), np.empty(cap)
+    of = np.empty(cap, dtype=np.int32)
+    och = np.empty((cap, n_types), dtype=np.int32)
+    n = ctypes.c_int64(0)
+    rc = lib.oracle_microbatch(n_types, n_freq, _p(seg_off, ctypes.c_int64),
+                               _p(T, ctypes.c_double), _p(E, ctypes.c_double), len(seq),
+                               _p(seq, ctypes.c_int32), cT.shape[0], _p(cT, ctypes.c_double),
+                               _p(cE, ctypes.c_double), n_bins, cap, _p(oT, ctypes.c_double),
+                               _p(oE, ctypes.c_double), _p(of, ctypes.c_int32),
+                               _p(och, ctypes.c_int32), ctypes.byref(n))
+    if rc != 0:
+        raise OracleError("oracle_microbatch failed: %d" % rc)
+    k = min(n.value, cap)
+    return oT[:k].copy(), oE[:k].copy(), of[:k].copy(), och[:k].copy()
 
 
 def decode(space, idx: int):

@@ -22,6 +22,10 @@
  *   oracle_staircase  the non-dominated points of the composed array.
  *   oracle_extract    the per-partition choice behind a composed point (schedule
  *                     selection for a target latency, Section 5.1).
+ *   oracle_microbatch the microbatch frontier of Algorithm 2 with its two rules: one
+ *                     GPU frequency for the whole microbatch, and one shared SM
+ *                     allocation and launch timing per partition type (Section 4.4),
+ *                     plus the non-partition components.
  *
  * Every floating-point line is one IEEE fp64 rounding in the written order; the file
  * must be compiled without FMA contraction and without fast-math.
@@ -455,4 +459,143 @@ int oracle_extract(int P, int B, const int64_t *off, const double *T, const doub
     *T_out = Ts;
     *E_out = Es;
     return OR_OK;
+}
+
+/* ------------------------------------------------------------------------------
+ * Microbatch frontier (Section 4.4, Algorithm 2).
+ *
+ * A microbatch runs n_seq partitions in order; partition i is of type seq[i].  For a
+ * GPU frequency f, every partition of type t uses the same (SM allocation, launch
+ * timing) choice, so a configuration is one point of each type's frontier at f.  Its
+ * time is the sum of its partitions' times in execution order followed by the
+ * non-partition components' times at f (likewise energy); the microbatch frontier is
+ * GetFrontier over every configuration of every frequency.
+ *
+ * Per frequency the configurations are composed on a discretised time axis as in
+ * oracle_compose: type t, used n_t > 0 times, contributes its points scaled to
+ * (n_t * T, n_t * E) (one rounding each), and the used types are composed in type
+ * order.  Every non-dominated bin of that composition (oracle_staircase) is walked
+ * back to its choice (oracle_extract); that configuration's time and energy are then
+ * summed exactly in execution order, components last.  The union over frequencies of
+ * these configurations, in order (frequency, staircase bin), goes through GetFrontier.
+ * A frequency at which some used type has no point contributes nothing.
+ *
+ * seg_off [K*F+1]: points of type t at frequency f are seg_off[t*F+f] ..
+ * seg_off[t*F+f+1]-1 of T, E (each such segment a frontier or any point set).
+ * cT, cE [n_comp][F].  Outputs up to cap points in ascending time: oT, oE, of
+ * (frequency), ochoice [cap][K] (point index within its (type, f) segment; -1 for
+ * unused types); *n_out = number of frontier points (may exceed cap).
+ * ---------------------------------------------------------------------------- */
+int oracle_microbatch(int K, int F, const int64_t *seg_off, const double *T, const double *E,
+                      int n_seq, const int32_t *seq, int n_comp, const double *cT,
+                      const double *cE, int B, int64_t cap, double *oT, double *oE,
+                      int32_t *of, int32_t *ochoice, int64_t *n_out)
+{
+    if (K < 1 || F < 1 || n_seq < 1 || n_comp < 0 || B < 2 || cap < 0) return OR_EINVAL;
+    int32_t *cnt = (int32_t *)calloc((size_t)K, sizeof(int32_t));
+    int32_t *used = (int32_t *)malloc(sizeof(int32_t) * (size_t)K);
+    if (!cnt || !used) { free(cnt); free(used); return OR_EINVAL; }
+    for (int i = 0; i < n_seq; i++) {
+        if (seq[i] < 0 || seq[i] >= K) { free(cnt); free(used); return OR_EINVAL; }
+        cnt[seq[i]]++;
+    }
+    int Ku = 0;
+    for (int t = 0; t < K; t++)
+        if (cnt[t] > 0) used[Ku++] = t;
+    int64_t maxpts = 0;
+    for (int t = 0; t < K; t++)
+        for (int f = 0; f < F; f++) {
+            int64_t n = seg_off[t * F + f + 1] - seg_off[t * F + f];
+            if (n < 0) { free(cnt); free(used); return OR_EINVAL; }
+            if (n > maxpts) maxpts = n;
+        }
+    int64_t ncand_cap = (int64_t)F * B;
+    int64_t *off = (int64_t *)malloc(sizeof(int64_t) * (size_t)(Ku + 1));
+    double *Ts = (double *)malloc(sizeof(double) * (size_t)(Ku * maxpts + 1));
+    double *Es = (double *)malloc(sizeof(double) * (size_t)(Ku * maxpts + 1));
+    double *Fb = (double *)malloc(sizeof(double) * (size_t)B);
+    int32_t *bp = (int32_t *)malloc(sizeof(int32_t) * (size_t)Ku * B);
+    int32_t *pt = (int32_t *)malloc(sizeof(int32_t) * (size_t)(Ku * maxpts + 1));
+    int32_t *sb = (int32_t *)malloc(sizeof(int32_t) * (size_t)B);
+    double *stl = (double *)malloc(sizeof(double) * (size_t)B);
+    double *se = (double *)malloc(sizeof(double) * (size_t)B);
+    int32_t *ch = (int32_t *)malloc(sizeof(int32_t) * (size_t)(Ku + 1));
+    double *cTm = (double *)malloc(sizeof(double) * (size_t)ncand_cap);
+    double *cEm = (double *)malloc(sizeof(double) * (size_t)ncand_cap);
+    int32_t *cf = (int32_t *)malloc(sizeof(int32_t) * (size_t)ncand_cap);
+    int32_t *cch = (int32_t *)malloc(sizeof(int32_t) * (size_t)ncand_cap * K);
+    int32_t *keep = (int32_t *)malloc(sizeof(int32_t) * (size_t)(ncand_cap + 1));
+    int rc = OR_OK;
+    int64_t nc = 0;
+    if (!off || !Ts || !Es || !Fb || !bp || !pt || !sb || !stl || !se || !ch || !cTm || !cEm ||
+        !cf || !cch || !keep) {
+        rc = OR_EINVAL;
+        goto done;
+    }
+    for (int f = 0; f < F; f++) {
+        /* scaled points of the used types, in type order */
+        int64_t w = 0;
+        int empty = 0;
+        off[0] = 0;
+        for (int u = 0; u < Ku; u++) {
+            int t = used[u];
+            int64_t lo = seg_off[t * F + f], hi = seg_off[t * F + f + 1];
+            if (hi <= lo) empty = 1;
+            for (int64_t j = lo; j < hi; j++) {
+                Ts[w] = (double)cnt[t] * T[j];
+                Es[w] = (double)cnt[t] * E[j];
+                w++;
+            }
+            off[u + 1] = w;
+        }
+        if (empty) continue;
+        double info[2];
+        int32_t L;
+        rc = oracle_compose(Ku, off, Ts, Es, B, 0.0, Fb, bp, pt, info, &L);
+        if (rc != OR_OK) goto done;
+        int32_t ns = 0;
+        oracle_staircase(B, Fb, info[0], info[1], sb, stl, se, &ns);
+        for (int32_t q = 0; q < ns; q++) {
+            double tsum, esum;
+            rc = oracle_extract(Ku, B, off, Ts, Es, bp, pt, sb[q], ch, &tsum, &esum);
+            if (rc != OR_OK) goto done;
+            /* exact time and energy: partitions in execution order, then components */
+            double Tm = 0.0, Em = 0.0;
+            for (int i = 0; i < n_seq; i++) {
+                int t = seq[i], u = 0;
+                while (used[u] != t) u++;
+                int64_t x = seg_off[t * F + f] + ch[u];
+                Tm = Tm + T[x];
+                Em = Em + E[x];
+            }
+            for (int c = 0; c < n_comp; c++) {
+                Tm = Tm + cT[(int64_t)c * F + f];
+                Em = Em + cE[(int64_t)c * F + f];
+            }
+            cTm[nc] = Tm;
+            cEm[nc] = Em;
+            cf[nc] = f;
+            for (int t = 0; t < K; t++) cch[nc * K + t] = -1;
+            for (int u = 0; u < Ku; u++) cch[nc * K + used[u]] = ch[u];
+            nc++;
+        }
+    }
+    {
+        int64_t nk = 0;
+        rc = oracle_pareto(nc, cTm, cEm, keep, &nk);
+        if (rc != OR_OK) goto done;
+        for (int64_t r = 0; r < nk && r < cap; r++) {
+            int32_t c = keep[r];
+            oT[r] = cTm[c];
+            oE[r] = cEm[c];
+            of[r] = cf[c];
+            for (int t = 0; t < K; t++) ochoice[r * K + t] = cch[(int64_t)c * K + t];
+        }
+        *n_out = nk;
+    }
+done:
+    free(cnt); free(used); free(off); free(Ts); free(Es); free(Fb); free(bp); free(pt);
+    free(sb); free(stl); free(se); free(ch); free(cTm); free(cEm); free(cf); free(cch);
+    free(keep);
+    return rc;
 }
