@@ -210,6 +210,47 @@ kr_status kr_extract_schedule(int32_t n_parts, int32_t n_bins, const int32_t *bp
                               int32_t *ok_out, void *stream);
 
 /*
+ * kr_microbatch_frontier -- the microbatch frontier of Algorithm 2 with its two rules
+ * (Section 4.4): one GPU frequency for the whole microbatch, and one shared SM
+ * allocation and launch timing for all partitions of a type; the non-partition
+ * components are added per frequency.  A configuration's time is the sum of its
+ * partitions' times in execution order, then the components' times at its frequency in
+ * their order (energy alike).  Per frequency, the used types are composed as in
+ * kr_compose_frontiers with type t's points scaled to (n_t T, n_t E), n_t = its count
+ * in seq; each non-dominated bin is walked back to its configuration, whose exact sums
+ * enter GetFrontier over all frequencies (ties in order (frequency, bin)).  A frequency
+ * at which a used type has no point contributes nothing.
+ *   n_types K <= KR_MB_MAX_TYPES, n_freq F      host
+ *   seg_off   device [K*F+1]: type t's points at frequency f are seg_off[t*F+f] ..
+ *             seg_off[t*F+f+1]-1 of T, E (for instance per-(type, frequency) frontiers
+ *             from kr_pareto_filter); n_points host = seg_off[K*F]
+ *   n_seq, seq      host [n_seq] type of each partition, in execution order
+ *                   (1 <= n_seq <= KR_MB_MAX_SEQ)
+ *   n_comp          host >= 0; comp_T, comp_E device [n_comp][F] (NULL when 0)
+ *   n_bins          host B >= 2, bins of each frequency's composition
+ *   cap             host: capacity of the outputs
+ *   out_T, out_E    device [cap] frontier points in ascending time
+ *   out_f           device [cap] frequency index of each point
+ *   out_choice      device [cap][K] point index within its (type, frequency)
+ *                   segment, -1 for types not in seq
+ *   n_out           device [1] number of frontier points (the first cap are written)
+ * Returns KR_EINVAL for bad arguments (a type out of range in seq, ...), KR_ECAPACITY
+ * if ws_bytes is below kr_microbatch_frontier_workspace(...).  Stream-ordered; the host
+ * array seq may be reused as soon as the call returns.
+ */
+#define KR_MB_MAX_TYPES 32
+#define KR_MB_MAX_SEQ 2048 /* partitions per microbatch */
+size_t kr_microbatch_frontier_workspace(int32_t n_types, int32_t n_freq, int64_t n_points,
+                                        int32_t n_seq, int32_t n_bins);
+kr_status kr_microbatch_frontier(int32_t n_types, int32_t n_freq, const int64_t *seg_off,
+                                 const double *T, const double *E, int64_t n_points,
+                                 int32_t n_seq, const int32_t *seq, int32_t n_comp,
+                                 const double *comp_T, const double *comp_E, int32_t n_bins,
+                                 int64_t cap, double *out_T, double *out_E, int32_t *out_f,
+                                 int32_t *out_choice, int64_t *n_out, void *ws, size_t ws_bytes,
+                                 void *stream);
+
+/*
  * kr_decode_candidates -- candidate index -> (frequency index, launch positions, SM
  * choices) under the index order above.
  *   idx [n] device; f_out [n]; pos_out [n][M]; sm_out [n][M] (device)

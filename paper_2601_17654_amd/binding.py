@@ -50,6 +50,9 @@ _SIGS = {
     "kr_extract_schedule": (_i32, [_i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
                                    _vp, _vp, _vp, _vp]),
     "kr_decode_candidates": (_i32, [_SP, _vp, _i64, _vp, _vp, _vp, _vp]),
+    "kr_microbatch_frontier": (_i32, [_i32, _i32, _vp, _vp, _vp, _i64, _i32, _vp, _i32, _vp, _vp,
+                                      _i32, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "kr_microbatch_frontier_workspace": (_sz, [_i32, _i32, _i64, _i32, _i32]),
     "kr_status_string": (ctypes.c_char_p, [_i32]),
     "kr_set_phase_events": (_i32, [_i32, _vp, _vp]),
 }
@@ -291,6 +294,52 @@ def extract_schedule(comp: Composed, off, T, E, bins, cand_idx=None):
                                     _ptr(E), _ptr(bins), nq, _ptr(cand_idx), _ptr(choice), _ptr(cc),
                                     _ptr(Ts), _ptr(Es), _ptr(ok), _stream()))
     return choice, cc, Ts, Es, ok
+
+
+class Microbatch:
+    """Microbatch frontier: T, E [n], f int32 [n] frequency index, choice int32 [n][K]."""
+
+    def __init__(self, T, E, f, choice):
+        self.T, self.E, self.f, self.choice = T, E, f, choice
+
+
+def microbatch_frontier(seg_off, T, E, n_types: int, n_freq: int, seq, comp_T=None, comp_E=None,
+                        n_bins: int = 4096, cap: Optional[int] = None) -> Microbatch:
+    """Microbatch frontier of Algorithm 2 (one frequency per microbatch, one configuration
+    per partition type).  seg_off [K*F+1] (segment t*F+f = type t's points at frequency f),
+    seq: host list of partition types in execution order, comp_T/comp_E [n_comp][F]."""
+    seg_host = np.asarray(seg_off.cpu() if isinstance(seg_off, torch.Tensor) else seg_off,
+                          dtype=np.int64)
+    if len(seg_host) != n_types * n_freq + 1:
+        raise ValueError("seg_off must have n_types * n_freq + 1 entries")
+    n_points = int(seg_host[-1])
+    seg_dev = torch.from_numpy(seg_host).cuda()
+    T = _dev(T, torch.float64, "T").reshape(-1)
+    E = _dev(E, torch.float64, "E").reshape(-1)
+    seq_h = np.ascontiguousarray(np.asarray(seq, dtype=np.int32))
+    if comp_T is None:
+        n_comp, cT, cE = 0, None, None
+    else:
+        cT = _dev(comp_T, torch.float64, "comp_T").reshape(-1, n_freq)
+        cE = _dev(comp_E, torch.float64, "comp_E").reshape(-1, n_freq)
+        n_comp = cT.shape[0]
+    c = int(cap) if cap is not None else n_freq * n_bins
+    oT = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
+    oE = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
+    of = torch.empty(max(c, 1), dtype=torch.int32, device="cuda")
+    och = torch.empty((max(c, 1), n_types), dtype=torch.int32, device="cuda")
+    n = torch.empty(1, dtype=torch.int64, device="cuda")
+    wsb = _lib.kr_microbatch_frontier_workspace(n_types, n_freq, n_points, len(seq_h), n_bins)
+    if wsb == 0:
+        raise ValueError("unsupported microbatch shape")
+    ws = _workspace(wsb)
+    _check("kr_microbatch_frontier",
+           _lib.kr_microbatch_frontier(n_types, n_freq, _ptr(seg_dev), _ptr(T), _ptr(E), n_points,
+                                       len(seq_h), seq_h.ctypes.data_as(ctypes.c_void_p), n_comp,
+                                       _ptr(cT), _ptr(cE), n_bins, c, _ptr(oT), _ptr(oE), _ptr(of),
+                                       _ptr(och), _ptr(n), _ptr(ws), wsb, _stream()))
+    k = min(int(n.item()), c)
+    return Microbatch(oT[:k], oE[:k], of[:k], och[:k])
 
 
 def decode_candidates(space, idx):

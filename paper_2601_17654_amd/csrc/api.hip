@@ -400,6 +400,124 @@ kr_status kr_extract_schedule(int32_t n_parts, int32_t n_bins, const int32_t *bp
     return launch_extract(a, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
 }
 
+// Workspace of the microbatch frontier; every pointer is null when base is null.
+struct MbWs {
+    int64_t *off_f, *seg, *front_off;
+    double *Ts, *Es, *F, *info, *stair_Tlo, *stair_E, *slot_T, *slot_E, *front_T, *front_E;
+    int32_t *bp, *pt_bin, *L, *stair_bin, *n_stair, *status, *slot_choice, *front_idx;
+    void *cws, *pws;
+    size_t cws_bytes, pws_bytes;
+};
+
+static MbWs carve_mb(Carve &c, int K, int F, int64_t n_points, int B)
+{
+    MbWs w;
+    const int64_t S = (int64_t)F * B;
+    w.off_f = c.take<int64_t>(K + 1);
+    w.seg = c.take<int64_t>(2);
+    w.front_off = c.take<int64_t>(2);
+    w.Ts = c.take<double>(n_points + 1);
+    w.Es = c.take<double>(n_points + 1);
+    w.F = c.take<double>(B);
+    w.info = c.take<double>(2);
+    w.stair_Tlo = c.take<double>(B);
+    w.stair_E = c.take<double>(B);
+    w.slot_T = c.take<double>(S);
+    w.slot_E = c.take<double>(S);
+    w.front_T = c.take<double>(S);
+    w.front_E = c.take<double>(S);
+    w.bp = c.take<int32_t>((size_t)K * B);
+    w.pt_bin = c.take<int32_t>(n_points + 1);
+    w.L = c.take<int32_t>(1);
+    w.stair_bin = c.take<int32_t>(B);
+    w.n_stair = c.take<int32_t>(1);
+    w.status = c.take<int32_t>(1);
+    w.slot_choice = c.take<int32_t>((size_t)S * K);
+    w.front_idx = c.take<int32_t>(S);
+    w.cws_bytes = kr_compose_frontiers_workspace(K, B);
+    w.cws = c.take<char>(w.cws_bytes);
+    w.pws_bytes = kr_pareto_filter_workspace(S, 1);
+    w.pws = c.take<char>(w.pws_bytes);
+    return w;
+}
+
+size_t kr_microbatch_frontier_workspace(int32_t n_types, int32_t n_freq, int64_t n_points,
+                                        int32_t n_seq, int32_t n_bins)
+{
+    if (n_types < 1 || n_types > KR_MB_MAX_TYPES || n_freq < 1 || n_points < 0 || n_seq < 1 ||
+        n_seq > KR_MB_MAX_SEQ || n_bins < 2)
+        return 0;
+    Carve c(nullptr);
+    carve_mb(c, n_types, n_freq, n_points, n_bins);
+    return c.used;
+}
+
+kr_status kr_microbatch_frontier(int32_t n_types, int32_t n_freq, const int64_t *seg_off,
+                                 const double *T, const double *E, int64_t n_points,
+                                 int32_t n_seq, const int32_t *seq, int32_t n_comp,
+                                 const double *comp_T, const double *comp_E, int32_t n_bins,
+                                 int64_t cap, double *out_T, double *out_E, int32_t *out_f,
+                                 int32_t *out_choice, int64_t *n_out, void *ws, size_t ws_bytes,
+                                 void *stream)
+{
+    const size_t need = kr_microbatch_frontier_workspace(n_types, n_freq, n_points, n_seq, n_bins);
+    if (need == 0 || !seg_off || (n_points > 0 && (!T || !E)) || !seq || n_comp < 0 ||
+        (n_comp > 0 && (!comp_T || !comp_E)) || cap < 0 ||
+        (cap > 0 && (!out_T || !out_E || !out_f || !out_choice)) || !n_out || !ws)
+        return KR_EINVAL;
+    if (ws_bytes < need) return KR_ECAPACITY;
+    MbArgs a;
+    a.K = n_types;
+    a.F = n_freq;
+    a.B = n_bins;
+    a.n_seq = n_seq;
+    a.n_comp = n_comp;
+    a.seg_off = seg_off;
+    a.T = T;
+    a.E = E;
+    a.comp_T = comp_T;
+    a.comp_E = comp_E;
+    int32_t cnt[KR_MB_MAX_TYPES] = {0}, uidx[KR_MB_MAX_TYPES];
+    for (int i = 0; i < n_seq; ++i) {
+        if (seq[i] < 0 || seq[i] >= n_types) return KR_EINVAL;
+        ++cnt[seq[i]];
+    }
+    a.Ku = 0;
+    for (int t = 0; t < n_types; ++t)
+        if (cnt[t] > 0) {
+            uidx[t] = a.Ku;
+            a.used[a.Ku] = t;
+            a.count[a.Ku] = cnt[t];
+            ++a.Ku;
+        }
+    for (int i = 0; i < n_seq; ++i) a.seq_u[i] = (uint8_t)uidx[seq[i]];
+    hipStream_t st = (hipStream_t)stream;
+    Carve c(ws);
+    MbWs w = carve_mb(c, n_types, n_freq, n_points, n_bins);
+    a.slot_T = w.slot_T;
+    a.slot_E = w.slot_E;
+    a.slot_choice = w.slot_choice;
+    for (int f = 0; f < n_freq; ++f) {
+        if (launch_mb_scale(a, f, w.off_f, w.Ts, w.Es, st) != hipSuccess) return KR_EHIP;
+        const kr_status rc = kr_compose_frontiers(
+            a.Ku, w.off_f, w.Ts, w.Es, n_bins, 0.0, w.F, w.bp, w.pt_bin, w.info, w.L, w.stair_bin,
+            w.stair_Tlo, w.stair_E, w.n_stair, w.status, w.cws, w.cws_bytes, stream);
+        if (rc != KR_OK) return rc;
+        MbComp mc{w.off_f, w.bp, w.pt_bin, w.stair_bin, w.n_stair, w.status};
+        if (launch_mb_walk(a, f, mc, st) != hipSuccess) return KR_EHIP;
+    }
+    const int64_t S = (int64_t)n_freq * n_bins;
+    if (launch_mb_seg(w.seg, S, st) != hipSuccess) return KR_EHIP;
+    const kr_status rc = kr_pareto_filter(S, w.slot_T, w.slot_E, w.seg, 1, S, w.front_off,
+                                          w.front_idx, w.front_T, w.front_E, w.pws, w.pws_bytes,
+                                          stream);
+    if (rc != KR_OK) return rc;
+    return launch_mb_gather(a, w.front_off, w.front_idx, cap, out_T, out_E, out_f, out_choice,
+                            n_out, st) == hipSuccess
+               ? KR_OK
+               : KR_EHIP;
+}
+
 kr_status kr_decode_candidates(const kr_space *space, const int32_t *idx, int64_t n,
                                int32_t *f_out, int32_t *pos_out, int32_t *sm_out, void *stream)
 {

@@ -122,4 +122,31 @@ struct ExtractArgs {
 };
 hipError_t launch_extract(const ExtractArgs &a, hipStream_t st);
 
+// microbatch.hip
+#define KR_MB_MAX_TYPES 32
+#define KR_MB_MAX_SEQ 2048
+struct MbArgs {
+    int K, F, B, Ku, n_seq, n_comp;
+    const int64_t *seg_off;
+    const double *T, *E;
+    const double *comp_T, *comp_E;
+    int32_t used[KR_MB_MAX_TYPES];   // used types, in type order
+    int32_t count[KR_MB_MAX_TYPES];  // their repeat counts
+    uint8_t seq_u[KR_MB_MAX_SEQ];    // used-type index of each partition
+    double *slot_T, *slot_E;         // [F * B]
+    int32_t *slot_choice;            // [F * B][K]
+};
+// One frequency's composition outputs.
+struct MbComp {
+    const int64_t *off;  // [Ku + 1]
+    const int32_t *bp, *pt_bin, *stair_bin, *n_stair, *status;
+};
+hipError_t launch_mb_scale(const MbArgs &a, int f, int64_t *off_f, double *Ts, double *Es,
+                           hipStream_t st);
+hipError_t launch_mb_walk(const MbArgs &a, int f, const MbComp &c, hipStream_t st);
+hipError_t launch_mb_seg(int64_t *seg, int64_t n, hipStream_t st);
+hipError_t launch_mb_gather(const MbArgs &a, const int64_t *front_off, const int32_t *front_idx,
+                            int64_t cap, double *out_T, double *out_E, int32_t *out_f,
+                            int32_t *out_choice, int64_t *n_out, hipStream_t st);
+
 }  // namespace kr

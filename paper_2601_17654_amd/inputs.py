@@ -258,3 +258,21 @@ def frontier_batch(seed: int, n_points: Sequence[int], t_span: Sequence[float],
     off = np.zeros(len(T_parts) + 1, dtype=np.int64)
     off[1:] = np.cumsum([len(x) for x in T_parts])
     return off, np.concatenate(T_parts), np.concatenate(E_parts)
+
+
+def microbatch_components(seed: int, n_comp: int, freqs: Sequence[float]) -> tuple:
+    """Non-partition components of a microbatch (kernels outside any partition, such as
+    an embedding or a loss), each like a compute kernel running alone: per component
+    t0 ~ logU(20 us, 2 ms), alpha ~ U(0.3, 1), P0 ~ U(300, 700) W, gamma ~ U(1.5, 2.5);
+    T_c(f) = t0 (alpha fmax / f + 1 - alpha), E_c(f) = P0 (f / fmax)^gamma T_c(f).
+    Returns (T [n_comp][F], E [n_comp][F])."""
+    f = np.asarray(freqs, dtype=np.float64)
+    fmax = f.max()
+    u = splitmix64_uniform(seed, 0, 4 * n_comp).reshape(n_comp, 4) if n_comp else np.zeros((0, 4))
+    t0 = _log_uniform(u[:, 0], 20e-6, 2e-3)
+    alpha = 0.3 + 0.7 * u[:, 1]
+    P0 = 300.0 + 400.0 * u[:, 2]
+    gamma = 1.5 + u[:, 3]
+    T = t0[:, None] * (alpha[:, None] * fmax / f[None, :] + 1.0 - alpha[:, None])
+    E = P0[:, None] * (f[None, :] / fmax) ** gamma[:, None] * T
+    return T, E

@@ -1,0 +1,106 @@
+"""GPU parity of the microbatch frontier (Algorithm 2 with one frequency per microbatch
+and one configuration per partition type) against the oracle: points, frequencies and
+per-type choices bit-exact, on random point sets, on per-(type, frequency) frontiers of
+evaluated llama-layer tables, and on the degenerate cases (a used type without points at a
+frequency, types not in the sequence, one type repeated)."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2601_17654_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def kr():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    from paper_2601_17654_amd import binding
+
+    return binding
+
+
+def _random_case(rng, K, F, nmax, empty=None):
+    segs, T, E = [], [], []
+    for t in range(K):
+        for f in range(F):
+            n = 0 if empty == (t, f) else int(rng.integers(1, nmax + 1))
+            T.extend(rng.uniform(1e-3, 5e-3, n) * (1.0 + 0.1 * f))
+            E.extend(rng.uniform(0.5, 2.0, n) / (1.0 + 0.05 * f))
+            segs.append(n)
+    seg_off = np.zeros(K * F + 1, dtype=np.int64)
+    seg_off[1:] = np.cumsum(segs)
+    return seg_off, np.array(T), np.array(E)
+
+
+def _compare(kr, seg_off, T, E, K, F, seq, cT, cE, B, what):
+    print("microbatch case", what, flush=True)
+    got = kr.microbatch_frontier(seg_off, torch.from_numpy(T).cuda(), torch.from_numpy(E).cuda(),
+                                 K, F, seq, None if cT is None else torch.from_numpy(cT).cuda(),
+                                 None if cE is None else torch.from_numpy(cE).cuda(), n_bins=B)
+    rT, rE, rf, rch = oracle.microbatch(seg_off, T, E, K, F, seq, cT, cE, n_bins=B)
+    gT, gE = got.T.cpu().numpy(), got.E.cpu().numpy()
+    gf, gch = got.f.cpu().numpy(), got.choice.cpu().numpy()
+    assert len(gT) == len(rT), what
+    np.testing.assert_array_equal(gf, rf, err_msg=what)
+    np.testing.assert_array_equal(gch, rch, err_msg=what)
+    np.testing.assert_array_equal(gT, rT, err_msg=what)
+    np.testing.assert_array_equal(gE, rE, err_msg=what)
+    return len(gT)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_microbatch_random(kr, seed):
+    rng = np.random.default_rng(300 + seed)
+    K, F = int(rng.integers(1, 5)), int(rng.integers(1, 6))
+    seg_off, T, E = _random_case(rng, K, F, 12)
+    seq = [int(x) for x in rng.integers(0, K, int(rng.integers(1, 9)))]
+    nc = int(rng.integers(0, 3))
+    cT = rng.uniform(1e-4, 1e-3, (nc, F)) if nc else None
+    cE = rng.uniform(0.01, 0.1, (nc, F)) if nc else None
+    B = int(rng.choice([64, 512, 4096]))
+    _compare(kr, seg_off, T, E, K, F, seq, cT, cE, B, "random %d" % seed)
+
+
+def test_microbatch_degenerate(kr):
+    rng = np.random.default_rng(17)
+    K, F = 3, 4
+    seg_off, T, E = _random_case(rng, K, F, 6, empty=(1, 2))
+    # a used type without points at frequency 2, an unused type
+    _compare(kr, seg_off, T, E, K, F, [0, 1, 0], None, None, 256, "empty segment")
+    # one type, repeated, with components
+    cT, cE = I.microbatch_components(5, 2, [1005.0, 1200.0, 1500.0, 1980.0])
+    _compare(kr, seg_off, T, E, K, F, [2] * 5, cT, cE, 1024, "one type repeated")
+
+
+def test_microbatch_llama_layers(kr):
+    """Types = the first four partitions of the llama-layer tables; per-(type, frequency)
+    frontiers by the library's filter and by the oracle's; a sequence of 8 layers of
+    (type 0, type 1) plus one of each other type; two components."""
+    w = I.config_workload(1, parts=range(0, 4))
+    sp = w.space
+    K, F = sp.n_parts, sp.n_freq
+    Cf = sp.cand_per_freq
+    d = [torch.from_numpy(getattr(w, k)).cuda() for k in ("t", "pw", "tc", "pc")]
+    Tg, Eg = kr.evaluate_partition(sp, *d)
+    seg = np.arange(K * F + 1, dtype=np.int64) * Cf
+    fr = kr.pareto_filter(Tg.reshape(-1), Eg.reshape(-1), seg)
+    # the oracle's per-(type, frequency) frontiers
+    rT, rE, rsegs = [], [], [0]
+    for t in range(K):
+        Tt, Et = oracle.evaluate_partition(sp, w.t, w.pw, w.tc, w.pc, t)
+        for f in range(F):
+            idx = oracle.pareto(Tt[f * Cf:(f + 1) * Cf], Et[f * Cf:(f + 1) * Cf])
+            rT.extend(Tt[f * Cf + idx])
+            rE.extend(Et[f * Cf + idx])
+            rsegs.append(rsegs[-1] + len(idx))
+    rseg = np.array(rsegs, dtype=np.int64)
+    np.testing.assert_array_equal(fr.off.cpu().numpy(), rseg)
+    np.testing.assert_array_equal(fr.T.cpu().numpy(), np.array(rT))
+    np.testing.assert_array_equal(fr.E.cpu().numpy(), np.array(rE))
+    seq = [0, 1] * 8 + [2, 3]
+    cT, cE = I.microbatch_components(1, 2, sp.freqs_mhz)
+    n = _compare(kr, rseg, np.array(rT), np.array(rE), K, F, seq, cT, cE, 2048, "llama layers")
+    assert n > 10
