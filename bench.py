@@ -34,7 +34,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 FP64_VECTOR_TFLOPS = 78.6
 COUNTERS = os.path.join(ROOT, "profiles", "eval_filter_counters_eval_stress.txt")
-KERNEL_SOURCES = ["eval_wave.hip", "kr_filter.h", "kr_device.h", "kr_wave.h", "kr_launch.h", "api.hip"]
+KERNEL_SOURCES = ["eval_wave.hip", "kr_filter.h", "kr_device.h", "kr_wave.h"]
 METRIC = "schedule candidates evaluated+filtered/sec and frontier cells/sec on 1 MI355X"
 
 
@@ -42,11 +42,26 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def _between(text: str, start: str, end: str) -> str:
+    i = text.index(start)
+    return text[i:text.index(end, i) + len(end)]
+
+
 def kernel_source_hash() -> str:
+    """sha256 (first 16 hex) of what the fused eval kernel is built from: its source files,
+    its argument struct, and the host code that plans its launch."""
+    csrc = os.path.join(ROOT, "paper_2601_17654_amd", "csrc")
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2601_17654_amd", "csrc", f), "rb") as fh:
+        with open(os.path.join(csrc, f), "rb") as fh:
             h.update(fh.read())
+    with open(os.path.join(csrc, "kr_launch.h")) as fh:
+        h.update(_between(fh.read(), "struct EvalArgs {", "\n};\n").encode())
+    with open(os.path.join(csrc, "api.hip")) as fh:
+        api = fh.read()
+    h.update(_between(api, "bool wave_plan(EvalArgs *a)", "\n}\n").encode())
+    h.update(_between(api, "bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)",
+                      "\n}\n").encode())
     return h.hexdigest()[:16]
 
 
@@ -215,6 +230,38 @@ def main():
         "roofline": roof,
     }
 
+    # Microbatch frontier (Algorithm 2 with one frequency per microbatch and one
+    # configuration per partition type): two llama-layer partition types, a 32-layer
+    # microbatch, two non-partition components, every frequency.  Timed on its own.
+    mb_w = I.config_workload(1, parts=range(0, 2))
+    msp = mb_w.space
+    mK, mF, mCf = msp.n_parts, msp.n_freq, msp.cand_per_freq
+    md = [torch.from_numpy(getattr(mb_w, k)).cuda() for k in ("t", "pw", "tc", "pc")]
+    mT, mE = kr.evaluate_partition(msp, *md)
+    mfr = kr.pareto_filter(mT.reshape(-1), mE.reshape(-1), np.arange(mK * mF + 1) * mCf)
+    mseg = mfr.off.cpu().numpy()
+    mseq = [0, 1] * 32
+    mcT, mcE = I.microbatch_components(1, 2, msp.freqs_mhz)
+    mcT_d, mcE_d = torch.from_numpy(mcT).cuda(), torch.from_numpy(mcE).cuda()
+    MB_BINS = 4096
+    kr.microbatch_frontier(mseg, mfr.T, mfr.E, mK, mF, mseq, mcT_d, mcE_d, n_bins=MB_BINS)
+    torch.cuda.synchronize()
+    mev = mk(2 * args.steps)
+    for k in range(args.steps):
+        mev[2 * k].record()
+        mres = kr.microbatch_frontier(mseg, mfr.T, mfr.E, mK, mF, mseq, mcT_d, mcE_d,
+                                      n_bins=MB_BINS)
+        mev[2 * k + 1].record()
+    torch.cuda.synchronize()
+    mb_ms = float(np.mean([mev[2 * k].elapsed_time(mev[2 * k + 1]) for k in range(args.steps)]))
+    sizes = np.diff(mseg).reshape(mK, mF)
+    n_configs = int(np.sum(np.prod(sizes, axis=0)))
+    out["microbatch"] = {
+        "workload": "microbatch-llama: 2 partition types (llama-layer tables), 32 layers "
+                    "(64 partitions), 64 frequencies, 2 components, 4096 bins",
+        "ms": round(mb_ms, 4), "frontier_points": int(mres.T.numel()),
+        "configurations": n_configs, "configurations_per_s": n_configs / (mb_ms * 1e-3)}
+
     if not args.skip_cpu:
         import oracle
 
@@ -241,6 +288,15 @@ def main():
         out["cpu_baseline_compose"] = {"value": cells / el, "unit": "cells/s", "cores": 1,
                                        "kind": "oracle", "sample": "full compose-stress batch, "
                                        "%.1f s" % el}
+        mT_h, mE_h = mfr.T.cpu().numpy(), mfr.E.cpu().numpy()
+        t0 = time.perf_counter()
+        ro = oracle.microbatch(mseg, mT_h, mE_h, mK, mF, mseq, mcT, mcE, n_bins=MB_BINS)
+        el = time.perf_counter() - t0
+        out["microbatch"]["cpu_baseline"] = {
+            "value": n_configs / el, "unit": "configurations/s", "cores": 1, "kind": "oracle",
+            "sample": "the same microbatch, %.2f s" % el,
+            "parity": bool(np.array_equal(ro[0], mres.T.cpu().numpy()) and
+                           np.array_equal(ro[3], mres.choice.cpu().numpy()))}
     print(json.dumps(out))
 
 
