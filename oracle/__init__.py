@@ -51,8 +51,10 @@ def _load():
         lib.oracle_extract.argtypes = [i, i, lp, dp, dp, ip, ip, ctypes.c_int32, ip, dp, dp]
         lib.oracle_microbatch.argtypes = [i, i, lp, dp, dp, i, ip, i, dp, dp, i,
                                           ctypes.c_int64, dp, dp, ip, ip, lp]
+        lib.oracle_microbatch_exact.argtypes = [i, i, lp, dp, dp, i, ip, i, dp, dp,
+                                                ctypes.c_int64, dp, dp, ip, ip, lp]
         for fn in ("oracle_evaluate", "oracle_pareto", "oracle_compose", "oracle_staircase",
-                   "oracle_extract", "oracle_microbatch"):
+                   "oracle_extract", "oracle_microbatch", "oracle_microbatch_exact"):
             getattr(lib, fn).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -201,6 +203,38 @@ def microbatch(seg_off, T, E, n_types: int, n_freq: int, seq, comp_T=None, comp_
                                _p(och, ctypes.c_int32), ctypes.byref(n))
     if rc != 0:
         raise OracleError("oracle_microbatch failed: %d" % rc)
+    k = min(n.value, cap)
+    return oT[:k].copy(), oE[:k].copy(), of[:k].copy(), och[:k].copy()
+
+
+def microbatch_exact(seg_off, T, E, n_types: int, n_freq: int, seq, comp_T=None, comp_E=None):
+    """Microbatch frontier by enumerating every configuration (Algorithm 2 as written).
+    Returns (T, E, f int32, choice int32[n][K]) in ascending time."""
+    lib = _load()
+    seg_off = np.ascontiguousarray(seg_off, dtype=np.int64)
+    T, E = _f64(T), _f64(E)
+    seq = np.ascontiguousarray(seq, dtype=np.int32)
+    if comp_T is None:
+        cT = np.zeros((0, n_freq))
+        cE = np.zeros((0, n_freq))
+    else:
+        cT, cE = _f64(comp_T).reshape(-1, n_freq), _f64(comp_E).reshape(-1, n_freq)
+    sizes = np.diff(seg_off).reshape(n_types, n_freq)
+    used = sorted(set(seq.tolist()))
+    cap = max(int(np.sum(np.prod(sizes[used], axis=0))), 1)
+    oT, oE = np.empty(cap), np.empty(cap)
+    of = np.empty(cap, dtype=np.int32)
+    och = np.empty((cap, n_types), dtype=np.int32)
+    n = ctypes.c_int64(0)
+    rc = lib.oracle_microbatch_exact(n_types, n_freq, _p(seg_off, ctypes.c_int64),
+                                     _p(T, ctypes.c_double), _p(E, ctypes.c_double), len(seq),
+                                     _p(seq, ctypes.c_int32), cT.shape[0],
+                                     _p(cT, ctypes.c_double), _p(cE, ctypes.c_double), cap,
+                                     _p(oT, ctypes.c_double), _p(oE, ctypes.c_double),
+                                     _p(of, ctypes.c_int32), _p(och, ctypes.c_int32),
+                                     ctypes.byref(n))
+    if rc != 0:
+        raise OracleError("oracle_microbatch_exact failed: %d" % rc)
     k = min(n.value, cap)
     return oT[:k].copy(), oE[:k].copy(), of[:k].copy(), och[:k].copy()
 

@@ -25,7 +25,9 @@
  *   oracle_microbatch the microbatch frontier of Algorithm 2 with its two rules: one
  *                     GPU frequency for the whole microbatch, and one shared SM
  *                     allocation and launch timing per partition type (Section 4.4),
- *                     plus the non-partition components.
+ *                     plus the non-partition components, composed on a time grid.
+ *   oracle_microbatch_exact  the same frontier by enumerating every configuration, as
+ *                     Algorithm 2 is written.
  *
  * Every floating-point line is one IEEE fp64 rounding in the written order; the file
  * must be compiled without FMA contraction and without fast-math.
@@ -597,5 +599,93 @@ done:
     free(cnt); free(used); free(off); free(Ts); free(Es); free(Fb); free(bp); free(pt);
     free(sb); free(stl); free(se); free(ch); free(cTm); free(cEm); free(cf); free(cch);
     free(keep);
+    return rc;
+}
+
+/* ------------------------------------------------------------------------------
+ * Microbatch frontier by enumeration (Section 4.4, Algorithm 2 as written): for every
+ * frequency f, every configuration (one point of each used type's set at f), its time
+ * and energy summed in execution order and then over the components, and GetFrontier
+ * over all of them.  Configurations of one frequency are taken in mixed-radix order
+ * with the first used type (in type order) slowest; the union is in order (f, that
+ * index), which decides exact ties.  Same arguments and outputs as oracle_microbatch.
+ * ---------------------------------------------------------------------------- */
+int oracle_microbatch_exact(int K, int F, const int64_t *seg_off, const double *T,
+                            const double *E, int n_seq, const int32_t *seq, int n_comp,
+                            const double *cT, const double *cE, int64_t cap, double *oT,
+                            double *oE, int32_t *of, int32_t *ochoice, int64_t *n_out)
+{
+    if (K < 1 || F < 1 || n_seq < 1 || n_comp < 0 || cap < 0) return OR_EINVAL;
+    int32_t cnt[64], used[64];
+    if (K > 64) return OR_EINVAL;
+    for (int t = 0; t < K; t++) cnt[t] = 0;
+    for (int i = 0; i < n_seq; i++) {
+        if (seq[i] < 0 || seq[i] >= K) return OR_EINVAL;
+        cnt[seq[i]]++;
+    }
+    int Ku = 0;
+    for (int t = 0; t < K; t++)
+        if (cnt[t] > 0) used[Ku++] = t;
+    int64_t total = 0;
+    for (int f = 0; f < F; f++) {
+        int64_t n = 1;
+        for (int u = 0; u < Ku; u++) n *= seg_off[used[u] * F + f + 1] - seg_off[used[u] * F + f];
+        total += n;
+    }
+    double *cTm = (double *)malloc(sizeof(double) * (size_t)(total + 1));
+    double *cEm = (double *)malloc(sizeof(double) * (size_t)(total + 1));
+    int32_t *cf = (int32_t *)malloc(sizeof(int32_t) * (size_t)(total + 1));
+    int32_t *cch = (int32_t *)malloc(sizeof(int32_t) * (size_t)(total + 1) * K);
+    int32_t *keep = (int32_t *)malloc(sizeof(int32_t) * (size_t)(total + 1));
+    int rc = OR_OK;
+    if (!cTm || !cEm || !cf || !cch || !keep) { rc = OR_EINVAL; goto done; }
+    {
+        int64_t nc = 0;
+        int32_t j[64];
+        for (int f = 0; f < F; f++) {
+            int64_t n = 1;
+            for (int u = 0; u < Ku; u++)
+                n *= seg_off[used[u] * F + f + 1] - seg_off[used[u] * F + f];
+            for (int u = 0; u < Ku; u++) j[u] = 0;
+            for (int64_t c = 0; c < n; c++) {
+                double Tm = 0.0, Em = 0.0;
+                for (int i = 0; i < n_seq; i++) {
+                    int u = 0;
+                    while (used[u] != seq[i]) u++;
+                    int64_t x = seg_off[used[u] * F + f] + j[u];
+                    Tm = Tm + T[x];
+                    Em = Em + E[x];
+                }
+                for (int k = 0; k < n_comp; k++) {
+                    Tm = Tm + cT[(int64_t)k * F + f];
+                    Em = Em + cE[(int64_t)k * F + f];
+                }
+                cTm[nc] = Tm;
+                cEm[nc] = Em;
+                cf[nc] = f;
+                for (int t = 0; t < K; t++) cch[nc * K + t] = -1;
+                for (int u = 0; u < Ku; u++) cch[nc * K + used[u]] = j[u];
+                nc++;
+                /* next configuration: the last used type fastest */
+                for (int u = Ku - 1; u >= 0; u--) {
+                    if (++j[u] < seg_off[used[u] * F + f + 1] - seg_off[used[u] * F + f]) break;
+                    j[u] = 0;
+                }
+            }
+        }
+        int64_t nk = 0;
+        rc = oracle_pareto(nc, cTm, cEm, keep, &nk);
+        if (rc != OR_OK) goto done;
+        for (int64_t r = 0; r < nk && r < cap; r++) {
+            int32_t c = keep[r];
+            oT[r] = cTm[c];
+            oE[r] = cEm[c];
+            of[r] = cf[c];
+            for (int t = 0; t < K; t++) ochoice[r * K + t] = cch[(int64_t)c * K + t];
+        }
+        *n_out = nk;
+    }
+done:
+    free(cTm); free(cEm); free(cf); free(cch); free(keep);
     return rc;
 }

@@ -202,3 +202,72 @@ def test_repeat_count_weights_the_choice():
     assert len(want) == 4
     assert [(t, e) for (t, e, _) in want] == list(zip(oT.tolist(), oE.tolist()))
     assert [tuple(c) for c in och.tolist()] == [(0, 0), (0, 1), (1, 0), (1, 1)]
+
+
+# ---- the enumerating oracle -------------------------------------------------------
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_exact_against_brute_force(seed):
+    """Enumeration against the brute-force non-dominated set (pairwise dominance, not
+    sort-and-scan), with every reported choice re-summed."""
+    rng = np.random.default_rng(400 + seed)
+    K, F = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+    seg_off, T, E = _case(rng, K, F, 4, empty=(0, 0) if seed == 3 else None)
+    seq = [int(x) for x in rng.integers(0, K, int(rng.integers(1, 6)))]
+    nc = int(rng.integers(0, 3))
+    cT = rng.uniform(1e-4, 1e-3, (nc, F))
+    cE = rng.uniform(0.01, 0.1, (nc, F))
+    oT, oE, of, och = oracle.microbatch_exact(seg_off, T, E, K, F, seq, cT if nc else None,
+                                              cE if nc else None)
+    want = sorted(_nondominated(_exact(seg_off, T, E, K, F, seq, cT, cE)))
+    assert [(t, e, f) for (t, e, f) in want] == list(zip(oT.tolist(), oE.tolist(), of.tolist()))
+    for r in range(len(oT)):
+        choice = {t: int(och[r][t]) for t in range(K)}
+        assert _config_sums(seg_off, T, E, F, int(of[r]), seq, choice, cT, cE) == (oT[r], oE[r])
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_exact_equals_grid_with_fine_bins(seed):
+    """The enumeration and the grid composition (pinned above) agree once the bins are
+    finer than every gap between configuration times."""
+    rng = np.random.default_rng(500 + seed)
+    K, F = 2, 2
+    segs, T, E = [], [], []
+    for t in range(K):
+        for f in range(F):
+            n = int(rng.integers(2, 5))
+            T.extend((1.0 + np.arange(n) * 16.0 ** t) * 1e-3 * (1.0 + 0.1 * f))
+            E.extend(rng.uniform(0.5, 2.0, n))
+            segs.append(n)
+    seg_off = np.zeros(K * F + 1, dtype=np.int64)
+    seg_off[1:] = np.cumsum(segs)
+    T, E = np.array(T), np.array(E)
+    seq = [0, 1, 0, 0]
+    a = oracle.microbatch_exact(seg_off, T, E, K, F, seq)
+    b = oracle.microbatch(seg_off, T, E, K, F, seq, n_bins=1 << 14)
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x, y)
+
+
+def test_exact_dominated_points_change_nothing():
+    """Adding dominated points to a type's set leaves the frontier unchanged (fp64
+    rounding is monotone, so a dominated choice never helps a sum)."""
+    rng = np.random.default_rng(9)
+    K, F = 2, 2
+    seg_off, T, E = _case(rng, K, F, 4)
+    seq = [0, 1, 1]
+    a = oracle.microbatch_exact(seg_off, T, E, K, F, seq)
+    # each segment gets a copy of its points, 1% slower and 1% more energy, appended
+    segs, T2, E2 = [], [], []
+    for g in range(K * F):
+        x, y = T[seg_off[g]:seg_off[g + 1]], E[seg_off[g]:seg_off[g + 1]]
+        T2.extend(list(x) + list(x * 1.01))
+        E2.extend(list(y) + list(y * 1.01))
+        segs.append(2 * len(x))
+    seg2 = np.zeros(K * F + 1, dtype=np.int64)
+    seg2[1:] = np.cumsum(segs)
+    b = oracle.microbatch_exact(seg2, np.array(T2), np.array(E2), K, F, seq)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+    np.testing.assert_array_equal(a[2], b[2])
