@@ -231,16 +231,17 @@ def main():
     }
 
     # Microbatch frontier (Algorithm 2 with one frequency per microbatch and one
-    # configuration per partition type): two llama-layer partition types, a 32-layer
-    # microbatch, two non-partition components, every frequency.  Timed on its own.
-    mb_w = I.config_workload(1, parts=range(0, 2))
+    # configuration per partition type): four llama-layer partition types, a 16-layer
+    # microbatch of all four, two non-partition components, every frequency.  Timed on
+    # its own.
+    mb_w = I.config_workload(1, parts=range(0, 4))
     msp = mb_w.space
     mK, mF, mCf = msp.n_parts, msp.n_freq, msp.cand_per_freq
     md = [torch.from_numpy(getattr(mb_w, k)).cuda() for k in ("t", "pw", "tc", "pc")]
     mT, mE = kr.evaluate_partition(msp, *md)
     mfr = kr.pareto_filter(mT.reshape(-1), mE.reshape(-1), np.arange(mK * mF + 1) * mCf)
     mseg = mfr.off.cpu().numpy()
-    mseq = [0, 1] * 32
+    mseq = [0, 1, 2, 3] * 16
     mcT, mcE = I.microbatch_components(1, 2, msp.freqs_mhz)
     mcT_d, mcE_d = torch.from_numpy(mcT).cuda(), torch.from_numpy(mcE).cuda()
     MB_BINS = 4096
@@ -254,13 +255,23 @@ def main():
         mev[2 * k + 1].record()
     torch.cuda.synchronize()
     mb_ms = float(np.mean([mev[2 * k].elapsed_time(mev[2 * k + 1]) for k in range(args.steps)]))
+    kr.microbatch_enumerate(mseg, mfr.T, mfr.E, mK, mF, mseq, mcT_d, mcE_d)
+    torch.cuda.synchronize()
+    for k in range(args.steps):
+        mev[2 * k].record()
+        mexa = kr.microbatch_enumerate(mseg, mfr.T, mfr.E, mK, mF, mseq, mcT_d, mcE_d)
+        mev[2 * k + 1].record()
+    torch.cuda.synchronize()
+    mx_ms = float(np.mean([mev[2 * k].elapsed_time(mev[2 * k + 1]) for k in range(args.steps)]))
     sizes = np.diff(mseg).reshape(mK, mF)
     n_configs = int(np.sum(np.prod(sizes, axis=0)))
     out["microbatch"] = {
-        "workload": "microbatch-llama: 2 partition types (llama-layer tables), 32 layers "
-                    "(64 partitions), 64 frequencies, 2 components, 4096 bins",
-        "ms": round(mb_ms, 4), "frontier_points": int(mres.T.numel()),
-        "configurations": n_configs, "configurations_per_s": n_configs / (mb_ms * 1e-3)}
+        "workload": "microbatch-llama: 4 partition types (llama-layer tables), 16 layers of "
+                    "all four (64 partitions), 64 frequencies, 2 components",
+        "configurations": n_configs,
+        "enumerate_ms": round(mx_ms, 4), "enumerate_points": int(mexa.T.numel()),
+        "configurations_per_s": n_configs / (mx_ms * 1e-3),
+        "grid_ms": round(mb_ms, 4), "grid_bins": MB_BINS, "grid_points": int(mres.T.numel())}
 
     if not args.skip_cpu:
         import oracle
@@ -290,12 +301,18 @@ def main():
                                        "%.1f s" % el}
         mT_h, mE_h = mfr.T.cpu().numpy(), mfr.E.cpu().numpy()
         t0 = time.perf_counter()
-        ro = oracle.microbatch(mseg, mT_h, mE_h, mK, mF, mseq, mcT, mcE, n_bins=MB_BINS)
+        rx = oracle.microbatch_exact(mseg, mT_h, mE_h, mK, mF, mseq, mcT, mcE)
         el = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        ro = oracle.microbatch(mseg, mT_h, mE_h, mK, mF, mseq, mcT, mcE, n_bins=MB_BINS)
+        elg = time.perf_counter() - t0
         out["microbatch"]["cpu_baseline"] = {
             "value": n_configs / el, "unit": "configurations/s", "cores": 1, "kind": "oracle",
-            "sample": "the same microbatch, %.2f s" % el,
-            "parity": bool(np.array_equal(ro[0], mres.T.cpu().numpy()) and
+            "sample": "the same microbatch by enumeration, %.4f s (grid composition %.2f s)"
+                      % (el, elg),
+            "parity": bool(np.array_equal(rx[0], mexa.T.cpu().numpy()) and
+                           np.array_equal(rx[3], mexa.choice.cpu().numpy()) and
+                           np.array_equal(ro[0], mres.T.cpu().numpy()) and
                            np.array_equal(ro[3], mres.choice.cpu().numpy()))}
     print(json.dumps(out))
 

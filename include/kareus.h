@@ -251,6 +251,28 @@ kr_status kr_microbatch_frontier(int32_t n_types, int32_t n_freq, const int64_t 
                                  void *stream);
 
 /*
+ * kr_microbatch_enumerate -- the same microbatch frontier (Section 4.4, Algorithm 2) by
+ * enumerating every configuration, as the algorithm is written, with no time grid: for
+ * every frequency, every choice of one point per type in seq, summed in execution order
+ * and then over the components; GetFrontier over all of them.  Configurations of one
+ * frequency are ordered mixed-radix with the first type in seq (in type order) slowest;
+ * exact ties go to the order (frequency, that index).  Arguments as for
+ * kr_microbatch_frontier, and:
+ *   n_configs  host: configurations to reserve, >= the sum over frequencies of the product
+ *              of the used types' point counts (<= 2^31 - 1)
+ *   status_out device [1]: KR_OK, or KR_ECAPACITY if the configurations exceed n_configs
+ *              (then *n_out = 0)
+ */
+size_t kr_microbatch_enumerate_workspace(int32_t n_types, int32_t n_freq, int64_t n_configs);
+kr_status kr_microbatch_enumerate(int32_t n_types, int32_t n_freq, const int64_t *seg_off,
+                                  const double *T, const double *E, int32_t n_seq,
+                                  const int32_t *seq, int32_t n_comp, const double *comp_T,
+                                  const double *comp_E, int64_t n_configs, int64_t cap,
+                                  double *out_T, double *out_E, int32_t *out_f,
+                                  int32_t *out_choice, int64_t *n_out, int32_t *status_out,
+                                  void *ws, size_t ws_bytes, void *stream);
+
+/*
  * kr_decode_candidates -- candidate index -> (frequency index, launch positions, SM
  * choices) under the index order above.
  *   idx [n] device; f_out [n]; pos_out [n][M]; sm_out [n][M] (device)

@@ -53,6 +53,9 @@ _SIGS = {
     "kr_microbatch_frontier": (_i32, [_i32, _i32, _vp, _vp, _vp, _i64, _i32, _vp, _i32, _vp, _vp,
                                       _i32, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "kr_microbatch_frontier_workspace": (_sz, [_i32, _i32, _i64, _i32, _i32]),
+    "kr_microbatch_enumerate": (_i32, [_i32, _i32, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i64,
+                                       _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "kr_microbatch_enumerate_workspace": (_sz, [_i32, _i32, _i64]),
     "kr_status_string": (ctypes.c_char_p, [_i32]),
     "kr_set_phase_events": (_i32, [_i32, _vp, _vp]),
 }
@@ -338,6 +341,50 @@ def microbatch_frontier(seg_off, T, E, n_types: int, n_freq: int, seq, comp_T=No
                                        len(seq_h), seq_h.ctypes.data_as(ctypes.c_void_p), n_comp,
                                        _ptr(cT), _ptr(cE), n_bins, c, _ptr(oT), _ptr(oE), _ptr(of),
                                        _ptr(och), _ptr(n), _ptr(ws), wsb, _stream()))
+    k = min(int(n.item()), c)
+    return Microbatch(oT[:k], oE[:k], of[:k], och[:k])
+
+
+def microbatch_enumerate(seg_off, T, E, n_types: int, n_freq: int, seq, comp_T=None,
+                         comp_E=None, cap: Optional[int] = None) -> Microbatch:
+    """Microbatch frontier by enumerating every configuration (Algorithm 2 as written)."""
+    seg_host = np.asarray(seg_off.cpu() if isinstance(seg_off, torch.Tensor) else seg_off,
+                          dtype=np.int64)
+    if len(seg_host) != n_types * n_freq + 1:
+        raise ValueError("seg_off must have n_types * n_freq + 1 entries")
+    seq_h = np.ascontiguousarray(np.asarray(seq, dtype=np.int32))
+    sizes = np.diff(seg_host).reshape(n_types, n_freq)
+    used = sorted(set(seq_h.tolist()))
+    n_configs = max(int(np.sum(np.prod(sizes[used], axis=0))), 1)
+    seg_dev = torch.from_numpy(seg_host).cuda()
+    T = _dev(T, torch.float64, "T").reshape(-1)
+    E = _dev(E, torch.float64, "E").reshape(-1)
+    if comp_T is None:
+        n_comp, cT, cE = 0, None, None
+    else:
+        cT = _dev(comp_T, torch.float64, "comp_T").reshape(-1, n_freq)
+        cE = _dev(comp_E, torch.float64, "comp_E").reshape(-1, n_freq)
+        n_comp = cT.shape[0]
+    c = int(cap) if cap is not None else n_configs
+    oT = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
+    oE = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
+    of = torch.empty(max(c, 1), dtype=torch.int32, device="cuda")
+    och = torch.empty((max(c, 1), n_types), dtype=torch.int32, device="cuda")
+    n = torch.empty(1, dtype=torch.int64, device="cuda")
+    status = torch.empty(1, dtype=torch.int32, device="cuda")
+    wsb = _lib.kr_microbatch_enumerate_workspace(n_types, n_freq, n_configs)
+    if wsb == 0:
+        raise ValueError("unsupported microbatch shape")
+    ws = _workspace(wsb)
+    _check("kr_microbatch_enumerate",
+           _lib.kr_microbatch_enumerate(n_types, n_freq, _ptr(seg_dev), _ptr(T), _ptr(E),
+                                        len(seq_h), seq_h.ctypes.data_as(ctypes.c_void_p),
+                                        n_comp, _ptr(cT), _ptr(cE), n_configs, c, _ptr(oT),
+                                        _ptr(oE), _ptr(of), _ptr(och), _ptr(n), _ptr(status),
+                                        _ptr(ws), wsb, _stream()))
+    st = int(status.item())
+    if st != KR_OK:
+        raise KrError("kr_microbatch_enumerate", st)
     k = min(int(n.item()), c)
     return Microbatch(oT[:k], oE[:k], of[:k], och[:k])
 

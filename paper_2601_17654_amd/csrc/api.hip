@@ -518,6 +518,102 @@ kr_status kr_microbatch_frontier(int32_t n_types, int32_t n_freq, const int64_t 
                : KR_EHIP;
 }
 
+// Workspace of the enumerating microbatch frontier.
+struct MbEnumWs {
+    int64_t *base, *seg, *front_off;
+    int32_t *status, *front_idx;
+    double *slot_T, *slot_E, *front_T, *front_E;
+    void *pws;
+    size_t pws_bytes;
+};
+
+static MbEnumWs carve_mb_enum(Carve &c, int F, int64_t slots)
+{
+    MbEnumWs w;
+    w.base = c.take<int64_t>(F + 1);
+    w.seg = c.take<int64_t>(2);
+    w.front_off = c.take<int64_t>(2);
+    w.status = c.take<int32_t>(1);
+    w.front_idx = c.take<int32_t>(slots);
+    w.slot_T = c.take<double>(slots);
+    w.slot_E = c.take<double>(slots);
+    w.front_T = c.take<double>(slots);
+    w.front_E = c.take<double>(slots);
+    w.pws_bytes = kr_pareto_filter_workspace(slots, 1);
+    w.pws = c.take<char>(w.pws_bytes);
+    return w;
+}
+
+size_t kr_microbatch_enumerate_workspace(int32_t n_types, int32_t n_freq, int64_t n_configs)
+{
+    if (n_types < 1 || n_types > KR_MB_MAX_TYPES || n_freq < 1 || n_configs < 1 ||
+        n_configs > INT32_MAX)
+        return 0;
+    Carve c(nullptr);
+    carve_mb_enum(c, n_freq, n_configs);
+    return c.used;
+}
+
+kr_status kr_microbatch_enumerate(int32_t n_types, int32_t n_freq, const int64_t *seg_off,
+                                  const double *T, const double *E, int32_t n_seq,
+                                  const int32_t *seq, int32_t n_comp, const double *comp_T,
+                                  const double *comp_E, int64_t n_configs, int64_t cap,
+                                  double *out_T, double *out_E, int32_t *out_f,
+                                  int32_t *out_choice, int64_t *n_out, int32_t *status_out,
+                                  void *ws, size_t ws_bytes, void *stream)
+{
+    const size_t need = kr_microbatch_enumerate_workspace(n_types, n_freq, n_configs);
+    if (need == 0 || !seg_off || !T || !E || !seq || n_seq < 1 || n_seq > KR_MB_MAX_SEQ ||
+        n_comp < 0 || (n_comp > 0 && (!comp_T || !comp_E)) || cap < 0 ||
+        (cap > 0 && (!out_T || !out_E || !out_f || !out_choice)) || !n_out || !status_out || !ws)
+        return KR_EINVAL;
+    if (ws_bytes < need) return KR_ECAPACITY;
+    MbArgs a;
+    a.K = n_types;
+    a.F = n_freq;
+    a.B = 0;
+    a.n_seq = n_seq;
+    a.n_comp = n_comp;
+    a.seg_off = seg_off;
+    a.T = T;
+    a.E = E;
+    a.comp_T = comp_T;
+    a.comp_E = comp_E;
+    int32_t cnt[KR_MB_MAX_TYPES] = {0}, uidx[KR_MB_MAX_TYPES];
+    for (int i = 0; i < n_seq; ++i) {
+        if (seq[i] < 0 || seq[i] >= n_types) return KR_EINVAL;
+        ++cnt[seq[i]];
+    }
+    a.Ku = 0;
+    for (int t = 0; t < n_types; ++t)
+        if (cnt[t] > 0) {
+            uidx[t] = a.Ku;
+            a.used[a.Ku] = t;
+            a.count[a.Ku] = cnt[t];
+            ++a.Ku;
+        }
+    for (int i = 0; i < n_seq; ++i) a.seq_u[i] = (uint8_t)uidx[seq[i]];
+    hipStream_t st = (hipStream_t)stream;
+    Carve c(ws);
+    MbEnumWs w = carve_mb_enum(c, n_freq, n_configs);
+    a.slot_T = w.slot_T;
+    a.slot_E = w.slot_E;
+    a.slot_choice = nullptr;
+    if (launch_mb_enum(a, w.base, n_configs, w.status, st) != hipSuccess) return KR_EHIP;
+    if (launch_mb_seg(w.seg, n_configs, st) != hipSuccess) return KR_EHIP;
+    const kr_status rc = kr_pareto_filter(n_configs, w.slot_T, w.slot_E, w.seg, 1, n_configs,
+                                          w.front_off, w.front_idx, w.front_T, w.front_E, w.pws,
+                                          w.pws_bytes, stream);
+    if (rc != KR_OK) return rc;
+    if (launch_mb_enum_gather(a, w.base, w.status, w.front_off, w.front_idx, cap, out_T, out_E,
+                              out_f, out_choice, n_out, n_configs, st) != hipSuccess)
+        return KR_EHIP;
+    return hipMemcpyAsync(status_out, w.status, sizeof(int32_t), hipMemcpyDeviceToDevice, st) ==
+                   hipSuccess
+               ? KR_OK
+               : KR_EHIP;
+}
+
 kr_status kr_decode_candidates(const kr_space *space, const int32_t *idx, int64_t n,
                                int32_t *f_out, int32_t *pos_out, int32_t *sm_out, void *stream)
 {

@@ -148,5 +148,12 @@ hipError_t launch_mb_seg(int64_t *seg, int64_t n, hipStream_t st);
 hipError_t launch_mb_gather(const MbArgs &a, const int64_t *front_off, const int32_t *front_idx,
                             int64_t cap, double *out_T, double *out_E, int32_t *out_f,
                             int32_t *out_choice, int64_t *n_out, hipStream_t st);
+// Enumeration: base [F + 1] configuration totals, status [1]; slot_T / slot_E [slots].
+hipError_t launch_mb_enum(const MbArgs &a, int64_t *base, int64_t slots, int32_t *status,
+                          hipStream_t st);
+hipError_t launch_mb_enum_gather(const MbArgs &a, const int64_t *base, const int32_t *status,
+                                 const int64_t *front_off, const int32_t *front_idx, int64_t cap,
+                                 double *out_T, double *out_E, int32_t *out_f, int32_t *out_choice,
+                                 int64_t *n_out, int64_t slots, hipStream_t st);
 
 }  // namespace kr

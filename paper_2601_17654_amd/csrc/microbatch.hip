@@ -139,4 +139,122 @@ hipError_t launch_mb_gather(const MbArgs &a, const int64_t *front_off, const int
     return hipGetLastError();
 }
 
+// ---- enumeration of every configuration (Algorithm 2 as written) ----------------------
+
+// Configurations per frequency (product of the used types' point counts) and their
+// running totals: base[f] .. base[f+1]-1 are frequency f's slots.  One thread; fails
+// with KR_ECAPACITY past the slots reserved.
+__global__ void mb_count_kernel(MbArgs a, int64_t *base, int64_t slots, int32_t *status)
+{
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    int64_t tot = 0;
+    for (int f = 0; f < a.F; ++f) {
+        base[f] = tot;
+        int64_t n = 1;
+        for (int u = 0; u < a.Ku; ++u) {
+            const int t = a.used[u];
+            n *= a.seg_off[t * a.F + f + 1] - a.seg_off[t * a.F + f];
+        }
+        tot += n;
+    }
+    base[a.F] = tot;
+    *status = tot <= slots ? KR_OK : KR_ECAPACITY;
+}
+
+// Frequency and per-used-type point of slot x (first used type slowest).
+__device__ __forceinline__ int mb_decode(const MbArgs &a, const int64_t *base, int64_t x,
+                                         int32_t *choice)
+{
+    int lo = 0, hi = a.F - 1;  // last f with base[f] <= x
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (base[mid] <= x) lo = mid;
+        else hi = mid - 1;
+    }
+    const int f = lo;
+    int64_t c = x - base[f];
+    for (int u = a.Ku - 1; u >= 0; --u) {
+        const int t = a.used[u];
+        const int64_t n = a.seg_off[t * a.F + f + 1] - a.seg_off[t * a.F + f];
+        choice[u] = (int32_t)(c % n);
+        c /= n;
+    }
+    return f;
+}
+
+// Time and energy of every configuration: partitions in execution order, then the
+// components.  Slots past the total hold +inf.
+__global__ void __launch_bounds__(KR_BLOCK) mb_enum_kernel(MbArgs a, const int64_t *base,
+                                                         int64_t slots, const int32_t *status)
+{
+    const int64_t total = *status == KR_OK ? base[a.F] : 0;
+    for (int64_t x = (int64_t)blockIdx.x * KR_BLOCK + threadIdx.x; x < slots;
+         x += (int64_t)gridDim.x * KR_BLOCK) {
+        if (x >= total) {
+            a.slot_T[x] = INFINITY;
+            a.slot_E[x] = INFINITY;
+            continue;
+        }
+        int32_t choice[KR_MB_MAX_TYPES];
+        const int f = mb_decode(a, base, x, choice);
+        double Tm = 0.0, Em = 0.0;
+        for (int i = 0; i < a.n_seq; ++i) {
+            const int u = a.seq_u[i];
+            const int64_t p = a.seg_off[a.used[u] * a.F + f] + choice[u];
+            Tm = Tm + a.T[p];
+            Em = Em + a.E[p];
+        }
+        for (int k = 0; k < a.n_comp; ++k) {
+            Tm = Tm + a.comp_T[(int64_t)k * a.F + f];
+            Em = Em + a.comp_E[(int64_t)k * a.F + f];
+        }
+        a.slot_T[x] = Tm;
+        a.slot_E[x] = Em;
+    }
+}
+
+// Frontier slots into the caller's outputs, decoding each slot's configuration.
+__global__ void __launch_bounds__(KR_BLOCK) mb_enum_gather_kernel(
+    MbArgs a, const int64_t *base, const int32_t *status, const int64_t *front_off,
+    const int32_t *front_idx, int64_t cap, double *out_T, double *out_E, int32_t *out_f,
+    int32_t *out_choice, int64_t *n_out)
+{
+    const int64_t n = *status == KR_OK ? front_off[1] : 0;
+    const int64_t r = (int64_t)blockIdx.x * KR_BLOCK + threadIdx.x;
+    if (r == 0) *n_out = n;
+    if (r >= n || r >= cap) return;
+    const int64_t x = front_idx[r];
+    int32_t choice[KR_MB_MAX_TYPES];
+    const int f = mb_decode(a, base, x, choice);
+    out_T[r] = a.slot_T[x];
+    out_E[r] = a.slot_E[x];
+    out_f[r] = f;
+    for (int t = 0; t < a.K; ++t) out_choice[r * a.K + t] = -1;
+    for (int u = 0; u < a.Ku; ++u) out_choice[r * a.K + a.used[u]] = choice[u];
+}
+
+hipError_t launch_mb_enum(const MbArgs &a, int64_t *base, int64_t slots, int32_t *status,
+                          hipStream_t st)
+{
+    hipLaunchKernelGGL(mb_count_kernel, dim3(1), dim3(64), 0, st, a, base, slots, status);
+    const int64_t blocks = (slots + KR_BLOCK - 1) / KR_BLOCK;
+    const unsigned grid = (unsigned)(blocks < 4096 ? (blocks > 0 ? blocks : 1) : 4096);
+    hipLaunchKernelGGL(mb_enum_kernel, dim3(grid), dim3(KR_BLOCK), 0, st, a, base, slots,
+                       (const int32_t *)status);
+    return hipGetLastError();
+}
+
+hipError_t launch_mb_enum_gather(const MbArgs &a, const int64_t *base, const int32_t *status,
+                                 const int64_t *front_off, const int32_t *front_idx, int64_t cap,
+                                 double *out_T, double *out_E, int32_t *out_f, int32_t *out_choice,
+                                 int64_t *n_out, int64_t slots, hipStream_t st)
+{
+    const int64_t m = cap < slots ? cap : slots;
+    const int64_t blocks = ((m > 0 ? m : 1) + KR_BLOCK - 1) / KR_BLOCK;
+    hipLaunchKernelGGL(mb_enum_gather_kernel, dim3((unsigned)blocks), dim3(KR_BLOCK), 0, st, a,
+                       base, status, front_off, front_idx, cap, out_T, out_E, out_f, out_choice,
+                       n_out);
+    return hipGetLastError();
+}
+
 }  // namespace kr

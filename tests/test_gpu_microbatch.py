@@ -35,6 +35,21 @@ def _random_case(rng, K, F, nmax, empty=None):
     return seg_off, np.array(T), np.array(E)
 
 
+def _compare_exact(kr, seg_off, T, E, K, F, seq, cT, cE, what):
+    print("microbatch enumeration case", what, flush=True)
+    got = kr.microbatch_enumerate(seg_off, torch.from_numpy(T).cuda(),
+                                  torch.from_numpy(E).cuda(), K, F, seq,
+                                  None if cT is None else torch.from_numpy(cT).cuda(),
+                                  None if cE is None else torch.from_numpy(cE).cuda())
+    rT, rE, rf, rch = oracle.microbatch_exact(seg_off, T, E, K, F, seq, cT, cE)
+    assert got.T.numel() == len(rT), what
+    np.testing.assert_array_equal(got.f.cpu().numpy(), rf, err_msg=what)
+    np.testing.assert_array_equal(got.choice.cpu().numpy(), rch, err_msg=what)
+    np.testing.assert_array_equal(got.T.cpu().numpy(), rT, err_msg=what)
+    np.testing.assert_array_equal(got.E.cpu().numpy(), rE, err_msg=what)
+    return len(rT)
+
+
 def _compare(kr, seg_off, T, E, K, F, seq, cT, cE, B, what):
     print("microbatch case", what, flush=True)
     got = kr.microbatch_frontier(seg_off, torch.from_numpy(T).cuda(), torch.from_numpy(E).cuda(),
@@ -62,6 +77,7 @@ def test_microbatch_random(kr, seed):
     cE = rng.uniform(0.01, 0.1, (nc, F)) if nc else None
     B = int(rng.choice([64, 512, 4096]))
     _compare(kr, seg_off, T, E, K, F, seq, cT, cE, B, "random %d" % seed)
+    _compare_exact(kr, seg_off, T, E, K, F, seq, cT, cE, "random %d" % seed)
 
 
 def test_microbatch_degenerate(kr):
@@ -70,9 +86,11 @@ def test_microbatch_degenerate(kr):
     seg_off, T, E = _random_case(rng, K, F, 6, empty=(1, 2))
     # a used type without points at frequency 2, an unused type
     _compare(kr, seg_off, T, E, K, F, [0, 1, 0], None, None, 256, "empty segment")
+    _compare_exact(kr, seg_off, T, E, K, F, [0, 1, 0], None, None, "empty segment")
     # one type, repeated, with components
     cT, cE = I.microbatch_components(5, 2, [1005.0, 1200.0, 1500.0, 1980.0])
     _compare(kr, seg_off, T, E, K, F, [2] * 5, cT, cE, 1024, "one type repeated")
+    _compare_exact(kr, seg_off, T, E, K, F, [2] * 5, cT, cE, "one type repeated")
 
 
 def test_microbatch_llama_layers(kr):
@@ -104,3 +122,5 @@ def test_microbatch_llama_layers(kr):
     cT, cE = I.microbatch_components(1, 2, sp.freqs_mhz)
     n = _compare(kr, rseg, np.array(rT), np.array(rE), K, F, seq, cT, cE, 2048, "llama layers")
     assert n > 10
+    assert _compare_exact(kr, rseg, np.array(rT), np.array(rE), K, F, seq, cT, cE,
+                          "llama layers") > 10
