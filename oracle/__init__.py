@@ -53,8 +53,15 @@ def _load():
                                           ctypes.c_int64, dp, dp, ip, ip, lp]
         lib.oracle_microbatch_exact.argtypes = [i, i, lp, dp, dp, i, ip, i, dp, dp,
                                                 ctypes.c_int64, dp, dp, ip, ip, lp]
+        lib.oracle_hypervolume.argtypes = [ctypes.c_int64, dp, dp, d, d, dp]
+        lib.oracle_hvi.argtypes = [i, lp, dp, dp, lp, dp, dp, d, dp, dp, dp]
+        lib.oracle_uncertainty.argtypes = [i, ctypes.c_int64, dp, dp, dp]
+        lib.oracle_select.argtypes = [i, lp, dp, dp, lp, lp, i, i, i, i, lp, ip]
+        lib.oracle_hv_converged.argtypes = [i, dp, i, d]
         for fn in ("oracle_evaluate", "oracle_pareto", "oracle_compose", "oracle_staircase",
-                   "oracle_extract", "oracle_microbatch", "oracle_microbatch_exact"):
+                   "oracle_extract", "oracle_microbatch", "oracle_microbatch_exact",
+                   "oracle_hypervolume", "oracle_hvi", "oracle_uncertainty", "oracle_select",
+                   "oracle_hv_converged"):
             getattr(lib, fn).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -237,6 +244,82 @@ def microbatch_exact(seg_off, T, E, n_types: int, n_freq: int, seq, comp_T=None,
         raise OracleError("oracle_microbatch_exact failed: %d" % rc)
     k = min(n.value, cap)
     return oT[:k].copy(), oE[:k].copy(), of[:k].copy(), och[:k].copy()
+
+
+def hypervolume(T, E, rT: float, rE: float) -> float:
+    """HV of the points (T, E) against the reference point (rT, rE) (Section 4.3)."""
+    lib = _load()
+    T, E = _f64(T), _f64(E)
+    out = ctypes.c_double(0.0)
+    rc = lib.oracle_hypervolume(T.shape[0], _p(T, ctypes.c_double), _p(E, ctypes.c_double),
+                                float(rT), float(rE), ctypes.byref(out))
+    if rc != 0:
+        raise OracleError("oracle_hypervolume failed: %d" % rc)
+    return out.value
+
+
+def hvi(cand_off, T_hat, E_hat, obs_off, T_obs, E_obs, p_static: float):
+    """Exploitation scores of Algorithm 1 (total, dynamic, static energy).
+    Returns (hvi float64[3][n_cand], hv float64[n_seg][3], ref float64[n_seg][4])."""
+    lib = _load()
+    cand_off = np.ascontiguousarray(cand_off, dtype=np.int64)
+    obs_off = np.ascontiguousarray(obs_off, dtype=np.int64)
+    T_hat, E_hat, T_obs, E_obs = _f64(T_hat), _f64(E_hat), _f64(T_obs), _f64(E_obs)
+    n_seg = cand_off.shape[0] - 1
+    n = int(cand_off[-1]) if n_seg > 0 else 0
+    out = np.empty((3, n))
+    hv = np.empty((max(n_seg, 0), 3))
+    ref = np.empty((max(n_seg, 0), 4))
+    rc = lib.oracle_hvi(n_seg, _p(cand_off, ctypes.c_int64), _p(T_hat, ctypes.c_double),
+                        _p(E_hat, ctypes.c_double), _p(obs_off, ctypes.c_int64),
+                        _p(T_obs, ctypes.c_double), _p(E_obs, ctypes.c_double),
+                        float(p_static), _p(out, ctypes.c_double), _p(hv, ctypes.c_double),
+                        _p(ref, ctypes.c_double))
+    if rc != 0:
+        raise OracleError("oracle_hvi failed: %d" % rc)
+    return out, hv, ref
+
+
+def uncertainty(Tm, Em):
+    """Exploration score: population std over ensemble members of T plus that of E.
+    Tm, Em: [M][n]."""
+    lib = _load()
+    Tm, Em = _f64(Tm), _f64(Em)
+    M, n = Tm.shape
+    out = np.empty(n)
+    rc = lib.oracle_uncertainty(M, n, _p(Tm, ctypes.c_double), _p(Em, ctypes.c_double),
+                                _p(out, ctypes.c_double))
+    if rc != 0:
+        raise OracleError("oracle_uncertainty failed: %d" % rc)
+    return out
+
+
+def select(cand_off, score, unc, obs_off, obs_idx, k1: int, k2: int, k3: int, k: int):
+    """Multi-pass candidate selection of Algorithm 1.  score [3][n_cand], unc [n_cand] or
+    None, obs_idx local indices.  Returns a list of int64 arrays, one per partition."""
+    lib = _load()
+    cand_off = np.ascontiguousarray(cand_off, dtype=np.int64)
+    obs_off = np.ascontiguousarray(obs_off, dtype=np.int64)
+    obs_idx = np.ascontiguousarray(obs_idx, dtype=np.int64)
+    score = _f64(score)
+    n_seg = cand_off.shape[0] - 1
+    uncp = None if unc is None else _f64(unc)
+    sel = np.full((max(n_seg, 1), max(k, 1)), -1, dtype=np.int64)
+    cnt = np.zeros(max(n_seg, 1), dtype=np.int32)
+    rc = lib.oracle_select(n_seg, _p(cand_off, ctypes.c_int64), _p(score, ctypes.c_double),
+                           None if uncp is None else _p(uncp, ctypes.c_double),
+                           _p(obs_off, ctypes.c_int64), _p(obs_idx, ctypes.c_int64),
+                           k1, k2, k3, k, _p(sel, ctypes.c_int64), _p(cnt, ctypes.c_int32))
+    if rc != 0:
+        raise OracleError("oracle_select failed: %d" % rc)
+    return [sel[g, :cnt[g]].copy() for g in range(n_seg)]
+
+
+def hv_converged(hv_history, R: int = 2, eps: float = 1e-3) -> bool:
+    """Stopping rule of Algorithm 1 (Appendix C)."""
+    lib = _load()
+    h = _f64(hv_history)
+    return bool(lib.oracle_hv_converged(h.shape[0], _p(h, ctypes.c_double), R, float(eps)))
 
 
 def decode(space, idx: int):

@@ -28,6 +28,10 @@
  *                     plus the non-partition components, composed on a time grid.
  *   oracle_microbatch_exact  the same frontier by enumerating every configuration, as
  *                     Algorithm 2 is written.
+ *   oracle_hypervolume, oracle_hvi, oracle_uncertainty, oracle_select,
+ *   oracle_hv_converged  the scores, candidate selection and stopping rule of the
+ *                     multi-pass Bayesian optimisation (Section 4.3, Algorithm 1,
+ *                     Appendix C).
  *
  * Every floating-point line is one IEEE fp64 rounding in the written order; the file
  * must be compiled without FMA contraction and without fast-math.
@@ -688,4 +692,258 @@ int oracle_microbatch_exact(int K, int F, const int64_t *seg_off, const double *
 done:
     free(cTm); free(cEm); free(cf); free(cch); free(keep);
     return rc;
+}
+
+/* ------------------------------------------------------------------------------
+ * Hypervolume and hypervolume improvement (Section 4.3, exploitation passes of
+ * Algorithm 1; reference point from Appendix C).
+ *
+ * HV(S; r) is the area of the part of the box below r = (rT, rE) that some point of S
+ * weakly dominates, i.e. the area of the union over s in S of [s.T, rT] x [s.E, rE]
+ * (empty unless s.T < rT and s.E < rE).  Measured in vertical strips: visit the
+ * points in ascending (T, E); a point inside the box whose energy is below every
+ * energy seen so far opens a new step of the staircase, and the previous step's strip
+ * (this T - previous T) * (rE - previous E) is added; the last step's strip ends at
+ * rT.  The strips are added in ascending time.
+ *
+ * HVI(y) = HV(S u {y}; r) - HV(S; r), both computed as above.
+ * ---------------------------------------------------------------------------- */
+typedef struct { double t, e; } or_pt;
+
+static int cmp_pt(const void *a, const void *b)
+{
+    const or_pt *x = (const or_pt *)a, *y = (const or_pt *)b;
+    if (x->t < y->t) return -1;
+    if (x->t > y->t) return 1;
+    if (x->e < y->e) return -1;
+    if (x->e > y->e) return 1;
+    return 0;
+}
+
+/* pts is sorted in place. */
+static double hv_of(or_pt *pts, int64_t n, double rT, double rE)
+{
+    qsort(pts, (size_t)n, sizeof(or_pt), cmp_pt);
+    double hv = 0.0, run = rE, pt = 0.0, pe = 0.0;
+    int have = 0;
+    for (int64_t i = 0; i < n; i++) {
+        if (!(pts[i].t < rT) || !(pts[i].e < rE)) continue;
+        if (pts[i].e < run) {
+            if (have) hv = hv + (pts[i].t - pt) * (rE - pe);
+            pt = pts[i].t;
+            pe = pts[i].e;
+            run = pe;
+            have = 1;
+        }
+    }
+    if (have) hv = hv + (rT - pt) * (rE - pe);
+    return hv;
+}
+
+int oracle_hypervolume(int64_t n, const double *T, const double *E, double rT, double rE,
+                       double *hv_out)
+{
+    if (n < 0) return OR_EINVAL;
+    or_pt *p = (or_pt *)malloc(sizeof(or_pt) * (size_t)(n > 0 ? n : 1));
+    if (!p) return OR_EINVAL;
+    for (int64_t i = 0; i < n; i++) {
+        p[i].t = T[i];
+        p[i].e = E[i];
+    }
+    *hv_out = hv_of(p, n, rT, rE);
+    free(p);
+    return OR_OK;
+}
+
+/*
+ * The three exploitation scores of Algorithm 1 for every unmeasured candidate of every
+ * partition.  Energy variants (Sections 2.1 and 4.3): static energy is static power
+ * times time, dynamic energy is total minus static:
+ *     v = 0 total   E
+ *     v = 1 dynamic E - p_static * T
+ *     v = 2 static  p_static * T
+ * Readings: for variant v, the current frontier is that of the measured points in the
+ * (T, energy_v) plane, and the reference point is r_v = (1.1 * max T, 1.1 * max
+ * energy_v) over the measured points (Appendix C).  Candidate y is (T_hat, energy_v of
+ * (T_hat, E_hat)).
+ *
+ * Partition g owns candidates [cand_off[g], cand_off[g+1]) and measured points
+ * [obs_off[g], obs_off[g+1]) (at least one).  Outputs: hvi[v * n_cand + x],
+ * hv[g * 3 + v] = HV of the measured points, ref[g * 4 + 0] = rT and
+ * ref[g * 4 + 1 + v] = rE_v.
+ */
+static double energy_variant(int v, double t, double e, double ps)
+{
+    if (v == 0) return e;
+    if (v == 1) return e - ps * t;
+    return ps * t;
+}
+
+int oracle_hvi(int n_seg, const int64_t *cand_off, const double *T_hat, const double *E_hat,
+               const int64_t *obs_off, const double *T_obs, const double *E_obs,
+               double p_static, double *hvi, double *hv, double *ref)
+{
+    if (n_seg < 0) return OR_EINVAL;
+    int64_t n_cand = n_seg > 0 ? cand_off[n_seg] : 0;
+    for (int g = 0; g < n_seg; g++)
+        if (obs_off[g + 1] - obs_off[g] < 1 || cand_off[g + 1] < cand_off[g]) return OR_EINVAL;
+    int64_t max_obs = 0;
+    for (int g = 0; g < n_seg; g++)
+        if (obs_off[g + 1] - obs_off[g] > max_obs) max_obs = obs_off[g + 1] - obs_off[g];
+    or_pt *p = (or_pt *)malloc(sizeof(or_pt) * (size_t)(max_obs + 1));
+    if (!p) return OR_EINVAL;
+    for (int g = 0; g < n_seg; g++) {
+        int64_t o0 = obs_off[g], no = obs_off[g + 1] - o0;
+        double mt = T_obs[o0];
+        for (int64_t i = 1; i < no; i++)
+            if (T_obs[o0 + i] > mt) mt = T_obs[o0 + i];
+        double rT = 1.1 * mt;
+        ref[g * 4] = rT;
+        for (int v = 0; v < 3; v++) {
+            double me = energy_variant(v, T_obs[o0], E_obs[o0], p_static);
+            for (int64_t i = 1; i < no; i++) {
+                double ev = energy_variant(v, T_obs[o0 + i], E_obs[o0 + i], p_static);
+                if (ev > me) me = ev;
+            }
+            double rE = 1.1 * me;
+            ref[g * 4 + 1 + v] = rE;
+            for (int64_t i = 0; i < no; i++) {
+                p[i].t = T_obs[o0 + i];
+                p[i].e = energy_variant(v, T_obs[o0 + i], E_obs[o0 + i], p_static);
+            }
+            double base = hv_of(p, no, rT, rE);
+            hv[g * 3 + v] = base;
+            for (int64_t x = cand_off[g]; x < cand_off[g + 1]; x++) {
+                for (int64_t i = 0; i < no; i++) {
+                    p[i].t = T_obs[o0 + i];
+                    p[i].e = energy_variant(v, T_obs[o0 + i], E_obs[o0 + i], p_static);
+                }
+                p[no].t = T_hat[x];
+                p[no].e = energy_variant(v, T_hat[x], E_hat[x], p_static);
+                hvi[(int64_t)v * n_cand + x] = hv_of(p, no + 1, rT, rE) - base;
+            }
+        }
+    }
+    free(p);
+    return OR_OK;
+}
+
+/*
+ * Exploration score of Algorithm 1: the standard deviation of the M ensemble
+ * predictions of time plus that of energy.  Reading: population standard deviation
+ * (divide by M), mean and squared deviations summed in member order.
+ * Tm, Em [M][n] (member-major); unc [n].
+ */
+int oracle_uncertainty(int M, int64_t n, const double *Tm, const double *Em, double *unc)
+{
+    if (M < 1 || n < 0) return OR_EINVAL;
+    for (int64_t x = 0; x < n; x++) {
+        double st = 0.0, se = 0.0;
+        for (int m = 0; m < M; m++) {
+            st = st + Tm[(int64_t)m * n + x];
+            se = se + Em[(int64_t)m * n + x];
+        }
+        double mt = st / M, me = se / M;
+        double vt = 0.0, ve = 0.0;
+        for (int m = 0; m < M; m++) {
+            double dt = Tm[(int64_t)m * n + x] - mt, de = Em[(int64_t)m * n + x] - me;
+            vt = vt + dt * dt;
+            ve = ve + de * de;
+        }
+        unc[x] = sqrt(vt / M) + sqrt(ve / M);
+    }
+    return OR_OK;
+}
+
+/* ------------------------------------------------------------------------------
+ * Multi-pass candidate selection of Algorithm 1, per partition:
+ *     C = TopK(score_0 over X \ D, k1)
+ *     C = C u TopK(score_1 over X \ D, k2)
+ *     C = C u TopK(score_2 over X \ D, k3)
+ *     C = C u TopK(unc over X \ D \ C, k - |C|)        (skipped when unc is NULL)
+ * TopK(s over A, m) takes the m members of A with the largest s, ties to the smaller
+ * index (all of A if it has fewer than m).  X is the partition's candidates (local
+ * indices 0..n_g-1), D the measured ones: obs_idx[obs_off[g] .. obs_off[g+1]) hold
+ * local indices; entries outside [0, n_g) name no candidate and are ignored.  C is
+ * written in the order the passes add it (each pass by rank, members already in C
+ * skipped) to sel[g * k ...], its size to count[g].  score [3][n_cand], unc [n_cand].
+ * Needs 0 <= k1, k2, k3, k1 + k2 + k3 <= k; any NaN score is an error.
+ * ---------------------------------------------------------------------------- */
+static const double *g_s;
+
+static int cmp_score(const void *a, const void *b)
+{
+    int64_t x = *(const int64_t *)a, y = *(const int64_t *)b;
+    if (g_s[x] > g_s[y]) return -1;
+    if (g_s[x] < g_s[y]) return 1;
+    return (x > y) - (x < y);
+}
+
+int oracle_select(int n_seg, const int64_t *cand_off, const double *score, const double *unc,
+                  const int64_t *obs_off, const int64_t *obs_idx, int k1, int k2, int k3, int k,
+                  int64_t *sel, int32_t *count)
+{
+    if (n_seg < 0 || k1 < 0 || k2 < 0 || k3 < 0 || k1 + k2 + k3 > k) return OR_EINVAL;
+    int64_t n_cand = n_seg > 0 ? cand_off[n_seg] : 0;
+    for (int64_t x = 0; x < n_cand; x++) {
+        if (score[x] != score[x] || score[n_cand + x] != score[n_cand + x] ||
+            score[2 * n_cand + x] != score[2 * n_cand + x])
+            return OR_EINVAL;
+        if (unc && unc[x] != unc[x]) return OR_EINVAL;
+    }
+    for (int g = 0; g < n_seg; g++) {
+        int64_t c0 = cand_off[g], ng = cand_off[g + 1] - c0;
+        char *in_d = (char *)calloc((size_t)(ng > 0 ? ng : 1), 1);
+        char *in_c = (char *)calloc((size_t)(ng > 0 ? ng : 1), 1);
+        int64_t *a = (int64_t *)malloc(sizeof(int64_t) * (size_t)(ng > 0 ? ng : 1));
+        if (!in_d || !in_c || !a) {
+            free(in_d);
+            free(in_c);
+            free(a);
+            return OR_EINVAL;
+        }
+        for (int64_t i = obs_off[g]; i < obs_off[g + 1]; i++)
+            if (obs_idx[i] >= 0 && obs_idx[i] < ng) in_d[obs_idx[i]] = 1;
+        int32_t cnt = 0;
+        int want[3] = {k1, k2, k3};
+        for (int pass = 0; pass < 4; pass++) {
+            if (pass == 3 && !unc) break;
+            const double *s = pass < 3 ? score + (int64_t)pass * n_cand + c0 : unc + c0;
+            int64_t na = 0;
+            for (int64_t x = 0; x < ng; x++)
+                if (!in_d[x] && !(pass == 3 && in_c[x])) a[na++] = x;
+            g_s = s;
+            qsort(a, (size_t)na, sizeof(int64_t), cmp_score);
+            int64_t m = pass < 3 ? want[pass] : k - cnt;
+            if (m > na) m = na;
+            for (int64_t r = 0; r < m; r++) {
+                if (in_c[a[r]]) continue;
+                in_c[a[r]] = 1;
+                sel[(int64_t)g * k + cnt++] = a[r];
+            }
+        }
+        count[g] = cnt;
+        free(in_d);
+        free(in_c);
+        free(a);
+    }
+    return OR_OK;
+}
+
+/* ------------------------------------------------------------------------------
+ * Stopping rule of Algorithm 1 (Appendix C): after batch b the relative HV improvement
+ * is (hv[b] - hv[b-1]) / hv[b-1]; stop once the mean of the last R of them is below
+ * eps.  hv[0] is the HV after the initial sample, hv[1..n-1] after each batch.
+ * Reading: with hv[b-1] = 0 the relative improvement is +inf (never converged).
+ * Returns 1 to stop after the last batch, 0 to go on.
+ * ---------------------------------------------------------------------------- */
+int oracle_hv_converged(int n, const double *hv, int R, double eps)
+{
+    if (R < 1 || n - 1 < R) return 0;
+    double s = 0.0;
+    for (int b = n - R; b < n; b++) {
+        if (!(hv[b - 1] != 0.0)) return 0;
+        s = s + (hv[b] - hv[b - 1]) / hv[b - 1];
+    }
+    return s / R < eps;
 }
