@@ -273,6 +273,95 @@ kr_status kr_microbatch_enumerate(int32_t n_types, int32_t n_freq, const int64_t
                                   void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * kr_hvi_scores -- the three exploitation scores of the multi-pass Bayesian optimisation
+ * (Section 4.3, Algorithm 1) for every candidate of every partition: the hypervolume
+ * improvement HVI(y) = HV(P u {y}; r) - HV(P; r) of the candidate's predicted point y
+ * over the current frontier P, with energy taken as
+ *     v = 0 total E,   v = 1 dynamic E - p_static * T,   v = 2 static p_static * T
+ * (static energy is static power times time, dynamic is the rest: Sections 2.1, 4.3).
+ * For variant v, P is the frontier of the partition's measured points in the
+ * (T, energy_v) plane and r = (1.1 * max T, 1.1 * max energy_v) over those points
+ * (Appendix C).  HV(S; r) is the area of the part of the box below r that S weakly
+ * dominates.
+ *   n_seg            host >= 1 partitions
+ *   n_cand           host = cand_off[n_seg]; cand_off device [n_seg + 1] non-decreasing
+ *                    from 0 (trusted: the host does not read it)
+ *   T_hat, E_hat     device [n_cand] predicted time and total energy of each candidate
+ *   n_obs            host = obs_off[n_seg]; obs_off device [n_seg + 1] non-decreasing
+ *                    from 0, every partition with 1 .. KR_HVI_MAX_OBS measured points
+ *   T_obs, E_obs     device [n_obs] measured time and total energy
+ *   p_static         host, static power (same unit as energy / time)
+ *   hvi_out          device [3][n_cand]: hvi_out[v * n_cand + x]
+ *   hv_out           device [n_seg][3]: HV of the measured points per variant (the
+ *                    stopping rule's quantity for v = 0)
+ *   ref_out          device [n_seg][4]: rT, then rE for v = 0, 1, 2
+ *   status_out       device [1]: KR_OK, or KR_EINVAL when a partition has no or more than
+ *                    KR_HVI_MAX_OBS measured points (its scores, HV and r are then NaN)
+ * HV and r are exact to the oracle's rounding (staircase strips summed in ascending
+ * time); HVI is the area y adds, summed strip by strip, so it differs from the
+ * difference of two hypervolumes only by rounding (a few ulps of HV(P u {y})).
+ * Dominated candidates and candidates outside the box score exactly 0.
+ */
+#define KR_HVI_MAX_OBS 512
+size_t kr_hvi_scores_workspace(int32_t n_seg, int64_t n_obs);
+kr_status kr_hvi_scores(int32_t n_seg, int64_t n_cand, const int64_t *cand_off,
+                        const double *T_hat, const double *E_hat, int64_t n_obs,
+                        const int64_t *obs_off, const double *T_obs, const double *E_obs,
+                        double p_static, double *hvi_out, double *hv_out, double *ref_out,
+                        int32_t *status_out, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * kr_uncertainty -- the exploration score of Algorithm 1 (Section 4.3): the standard
+ * deviation of the ensemble members' predicted time plus that of their predicted
+ * energy, per candidate.  Population standard deviation (divide by M); the mean and the
+ * squared deviations are summed in member order.
+ *   n_members  host M, 1 .. 64
+ *   n          host candidates
+ *   T_m, E_m   device [M][n] member-major predictions
+ *   unc_out    device [n]
+ */
+kr_status kr_uncertainty(int32_t n_members, int64_t n, const double *T_m, const double *E_m,
+                         double *unc_out, void *stream);
+
+/*
+ * kr_select_batch -- the multi-pass candidate selection of Algorithm 1 (Section 4.3),
+ * per partition g with candidates X (local indices 0 .. n_g - 1) and measured set D:
+ *     C = TopK(score_0 over X \ D, k1) u TopK(score_1 over X \ D, k2)
+ *         u TopK(score_2 over X \ D, k3)
+ *     C = C u TopK(unc over X \ D \ C, k - |C|)           (skipped when unc is NULL)
+ * TopK takes the largest scores, ties to the smaller index (all of the set if it is
+ * smaller); -0 and +0 tie.  C is written in the order the passes add it (each pass in
+ * rank order, members already in C skipped).
+ *   n_seg, n_cand, cand_off   as for kr_hvi_scores; every partition < 2^31 candidates
+ *   score            device [3][n_cand] (e.g. hvi_out of kr_hvi_scores)
+ *   unc              device [n_cand] or NULL
+ *   obs_off          device [n_seg + 1]; obs_idx device [obs_off[n_seg]]: the measured
+ *                    candidates' local indices (entries outside [0, n_g) are ignored)
+ *   k1, k2, k3, k    host: 0 <= k1, k2, k3; k1 + k2 + k3 <= k <= KR_SELECT_MAX_K
+ *   sel_out          device [n_seg][k]: the first count_out[g] entries of row g are C
+ *   count_out        device [n_seg]
+ *   status_out       device [1]: KR_OK, or KR_EINVAL if any score (or unc) is NaN (then
+ *                    every count is 0)
+ * Selections are exact: the same inputs give the oracle's selection bit for bit.
+ */
+#define KR_SELECT_MAX_K 64
+size_t kr_select_batch_workspace(int32_t n_seg, int64_t n_cand);
+kr_status kr_select_batch(int32_t n_seg, int64_t n_cand, const int64_t *cand_off,
+                          const double *score, const double *unc, const int64_t *obs_off,
+                          const int64_t *obs_idx, int32_t k1, int32_t k2, int32_t k3, int32_t k,
+                          int64_t *sel_out, int32_t *count_out, int32_t *status_out, void *ws,
+                          size_t ws_bytes, void *stream);
+
+/*
+ * kr_hv_converged -- the stopping rule of Algorithm 1 (Appendix C), on the host: after
+ * batch b the relative HV improvement is (hv[b] - hv[b-1]) / hv[b-1]; stop once the mean
+ * of the last R of them is below eps.  hv_history host [n]: hv[0] after the initial
+ * sample, hv[b] after batch b.  A zero hv[b-1] in the window never converges.
+ * Returns 1 to stop, 0 to go on (also when fewer than R batches have run or R < 1).
+ */
+int32_t kr_hv_converged(int32_t n, const double *hv_history, int32_t R, double eps);
+
+/*
  * kr_decode_candidates -- candidate index -> (frequency index, launch positions, SM
  * choices) under the index order above.
  *   idx [n] device; f_out [n]; pos_out [n][M]; sm_out [n][M] (device)

@@ -56,6 +56,14 @@ _SIGS = {
     "kr_microbatch_enumerate": (_i32, [_i32, _i32, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i64,
                                        _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "kr_microbatch_enumerate_workspace": (_sz, [_i32, _i32, _i64]),
+    "kr_hvi_scores": (_i32, [_i32, _i64, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _f64, _vp, _vp, _vp,
+                             _vp, _vp, _sz, _vp]),
+    "kr_hvi_scores_workspace": (_sz, [_i32, _i64]),
+    "kr_uncertainty": (_i32, [_i32, _i64, _vp, _vp, _vp, _vp]),
+    "kr_select_batch": (_i32, [_i32, _i64, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp,
+                               _vp, _vp, _vp, _sz, _vp]),
+    "kr_select_batch_workspace": (_sz, [_i32, _i64]),
+    "kr_hv_converged": (_i32, [_i32, _vp, _i32, _f64]),
     "kr_status_string": (ctypes.c_char_p, [_i32]),
     "kr_set_phase_events": (_i32, [_i32, _vp, _vp]),
 }
@@ -401,3 +409,113 @@ def decode_candidates(space, idx):
            _lib.kr_decode_candidates(ctypes.byref(sp), _ptr(idx), n, _ptr(f), _ptr(pos), _ptr(sm),
                                      _stream()))
     return f, pos, sm
+
+
+@dataclasses.dataclass
+class HviScores:
+    hvi: torch.Tensor     # [3][n_cand]: total, dynamic, static energy
+    hv: torch.Tensor      # [n_seg][3]
+    ref: torch.Tensor     # [n_seg][4]: rT, rE per variant
+    status: torch.Tensor  # [1]
+
+
+def _offsets(off, name: str) -> torch.Tensor:
+    return _dev(np.asarray(off.cpu() if isinstance(off, torch.Tensor) else off, dtype=np.int64),
+                torch.int64, name).reshape(-1)
+
+
+def hvi_scores(cand_off, T_hat, E_hat, obs_off, T_obs, E_obs, p_static: float,
+               check: bool = True, out: Optional[HviScores] = None) -> HviScores:
+    """Exploitation scores of Algorithm 1 (kr_hvi_scores).  With check=False the device
+    status is left for the caller (no synchronisation)."""
+    co = cand_off if isinstance(cand_off, torch.Tensor) and cand_off.is_cuda else \
+        _offsets(cand_off, "cand_off")
+    oo = obs_off if isinstance(obs_off, torch.Tensor) and obs_off.is_cuda else \
+        _offsets(obs_off, "obs_off")
+    n_seg = co.numel() - 1
+    T_hat = _dev(T_hat, torch.float64, "T_hat").reshape(-1)
+    E_hat = _dev(E_hat, torch.float64, "E_hat").reshape(-1)
+    T_obs = _dev(T_obs, torch.float64, "T_obs").reshape(-1)
+    E_obs = _dev(E_obs, torch.float64, "E_obs").reshape(-1)
+    n, no = T_hat.numel(), T_obs.numel()
+    if out is None:
+        out = HviScores(torch.empty((3, n), dtype=torch.float64, device="cuda"),
+                        torch.empty((n_seg, 3), dtype=torch.float64, device="cuda"),
+                        torch.empty((n_seg, 4), dtype=torch.float64, device="cuda"),
+                        torch.empty(1, dtype=torch.int32, device="cuda"))
+    wsb = _lib.kr_hvi_scores_workspace(n_seg, no)
+    if wsb == 0:
+        raise ValueError("hvi_scores needs at least one partition and one measured point")
+    ws = _workspace(wsb)
+    _check("kr_hvi_scores",
+           _lib.kr_hvi_scores(n_seg, n, _ptr(co), _ptr(T_hat), _ptr(E_hat), no, _ptr(oo),
+                              _ptr(T_obs), _ptr(E_obs), float(p_static), _ptr(out.hvi),
+                              _ptr(out.hv), _ptr(out.ref), _ptr(out.status), _ptr(ws), wsb,
+                              _stream()))
+    if check and int(out.status.item()) != KR_OK:
+        raise KrError("kr_hvi_scores", int(out.status.item()))
+    return out
+
+
+def uncertainty(T_m, E_m, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Exploration score of Algorithm 1 (kr_uncertainty); T_m, E_m [M][n]."""
+    T_m = _dev(T_m, torch.float64, "T_m")
+    E_m = _dev(E_m, torch.float64, "E_m")
+    if T_m.dim() != 2 or T_m.shape != E_m.shape:
+        raise ValueError("T_m and E_m must both be [M][n]")
+    M, n = T_m.shape
+    if out is None:
+        out = torch.empty(n, dtype=torch.float64, device="cuda")
+    _check("kr_uncertainty",
+           _lib.kr_uncertainty(M, n, _ptr(T_m), _ptr(E_m), _ptr(out), _stream()))
+    return out
+
+
+@dataclasses.dataclass
+class Batch:
+    sel: torch.Tensor     # [n_seg][k] int64 local indices
+    count: torch.Tensor   # [n_seg] int32
+    status: torch.Tensor  # [1]
+
+    def lists(self):
+        c = self.count.cpu().numpy()
+        s = self.sel.cpu().numpy()
+        return [s[g, :c[g]].copy() for g in range(len(c))]
+
+
+def select_batch(cand_off, score, unc, obs_off, obs_idx, k1: int, k2: int, k3: int, k: int,
+                 check: bool = True, out: Optional[Batch] = None) -> Batch:
+    """Multi-pass candidate selection of Algorithm 1 (kr_select_batch)."""
+    co = cand_off if isinstance(cand_off, torch.Tensor) and cand_off.is_cuda else \
+        _offsets(cand_off, "cand_off")
+    oo = obs_off if isinstance(obs_off, torch.Tensor) and obs_off.is_cuda else \
+        _offsets(obs_off, "obs_off")
+    oi = _dev(np.asarray(obs_idx, dtype=np.int64) if not isinstance(obs_idx, torch.Tensor)
+              else obs_idx, torch.int64, "obs_idx").reshape(-1)
+    if oi.numel() == 0:
+        oi = torch.zeros(1, dtype=torch.int64, device="cuda")
+    n_seg = co.numel() - 1
+    score = _dev(score, torch.float64, "score").reshape(3, -1)
+    n = score.shape[1]
+    u = None if unc is None else _dev(unc, torch.float64, "unc").reshape(-1)
+    if out is None:
+        out = Batch(torch.full((n_seg, max(k, 1)), -1, dtype=torch.int64, device="cuda"),
+                    torch.empty(n_seg, dtype=torch.int32, device="cuda"),
+                    torch.empty(1, dtype=torch.int32, device="cuda"))
+    wsb = _lib.kr_select_batch_workspace(n_seg, n)
+    if wsb == 0:
+        raise ValueError("select_batch needs at least one partition")
+    ws = _workspace(wsb)
+    _check("kr_select_batch",
+           _lib.kr_select_batch(n_seg, n, _ptr(co), _ptr(score), _ptr(u), _ptr(oo), _ptr(oi),
+                                k1, k2, k3, k, _ptr(out.sel), _ptr(out.count), _ptr(out.status),
+                                _ptr(ws), wsb, _stream()))
+    if check and int(out.status.item()) != KR_OK:
+        raise KrError("kr_select_batch", int(out.status.item()))
+    return out
+
+
+def hv_converged(hv_history, R: int = 2, eps: float = 1e-3) -> bool:
+    """Stopping rule of Algorithm 1 (kr_hv_converged, host)."""
+    h = np.ascontiguousarray(np.asarray(hv_history, dtype=np.float64))
+    return bool(_lib.kr_hv_converged(h.shape[0], h.ctypes.data_as(ctypes.c_void_p), R, float(eps)))

@@ -635,6 +635,121 @@ kr_status kr_decode_candidates(const kr_space *space, const int32_t *idx, int64_
     return launch_decode(d, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
 }
 
+size_t kr_hvi_scores_workspace(int32_t n_seg, int64_t n_obs)
+{
+    if (n_seg < 1 || n_obs < 1) return 0;
+    Carve c(nullptr);
+    c.take<double>(3 * n_obs);
+    c.take<double>(3 * n_obs);
+    c.take<int32_t>(3 * (int64_t)n_seg);
+    return c.used;
+}
+
+kr_status kr_hvi_scores(int32_t n_seg, int64_t n_cand, const int64_t *cand_off,
+                        const double *T_hat, const double *E_hat, int64_t n_obs,
+                        const int64_t *obs_off, const double *T_obs, const double *E_obs,
+                        double p_static, double *hvi_out, double *hv_out, double *ref_out,
+                        int32_t *status_out, void *ws, size_t ws_bytes, void *stream)
+{
+    const size_t need = kr_hvi_scores_workspace(n_seg, n_obs);
+    if (need == 0 || n_cand < 0 || !cand_off || !obs_off || !T_obs || !E_obs || !hv_out ||
+        !ref_out || !status_out || !ws || !(p_static == p_static) ||
+        (n_cand > 0 && (!T_hat || !E_hat || !hvi_out)))
+        return KR_EINVAL;
+    if (ws_bytes < need) return KR_ECAPACITY;
+    Carve c(ws);
+    HviArgs a;
+    a.n_seg = n_seg;
+    a.n_cand = n_cand;
+    a.n_obs = n_obs;
+    a.cand_off = cand_off;
+    a.obs_off = obs_off;
+    a.T_hat = T_hat;
+    a.E_hat = E_hat;
+    a.T_obs = T_obs;
+    a.E_obs = E_obs;
+    a.p_static = p_static;
+    a.fr_T = c.take<double>(3 * n_obs);
+    a.fr_E = c.take<double>(3 * n_obs);
+    a.fr_n = c.take<int32_t>(3 * (int64_t)n_seg);
+    a.hvi = hvi_out;
+    a.hv = hv_out;
+    a.ref = ref_out;
+    a.status = status_out;
+    return launch_hvi(a, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
+}
+
+kr_status kr_uncertainty(int32_t n_members, int64_t n, const double *T_m, const double *E_m,
+                         double *unc_out, void *stream)
+{
+    if (n_members < 1 || n_members > 64 || n < 0 || (n > 0 && (!T_m || !E_m || !unc_out)))
+        return KR_EINVAL;
+    return launch_uncertainty(n_members, n, T_m, E_m, unc_out, (hipStream_t)stream) ==
+                   hipSuccess
+               ? KR_OK
+               : KR_EHIP;
+}
+
+size_t kr_select_batch_workspace(int32_t n_seg, int64_t n_cand)
+{
+    if (n_seg < 1 || n_cand < 0) return 0;
+    const int64_t tiles = n_cand / KR_SEL_TILE + n_seg;
+    Carve c(nullptr);
+    c.take<int64_t>(n_seg + 1);
+    c.take<int32_t>(1);
+    c.take<uint64_t>(tiles * 4 * KR_SEL_LIST);
+    c.take<int32_t>(tiles * 4 * KR_SEL_LIST);
+    return c.used;
+}
+
+kr_status kr_select_batch(int32_t n_seg, int64_t n_cand, const int64_t *cand_off,
+                          const double *score, const double *unc, const int64_t *obs_off,
+                          const int64_t *obs_idx, int32_t k1, int32_t k2, int32_t k3, int32_t k,
+                          int64_t *sel_out, int32_t *count_out, int32_t *status_out, void *ws,
+                          size_t ws_bytes, void *stream)
+{
+    const size_t need = kr_select_batch_workspace(n_seg, n_cand);
+    if (need == 0 || !cand_off || !obs_off || !obs_idx || !count_out || !status_out || !ws ||
+        (n_cand > 0 && !score) || k1 < 0 || k2 < 0 || k3 < 0 ||
+        (int64_t)k1 + k2 + k3 > k || k > KR_SELECT_MAX_K || (k > 0 && !sel_out))
+        return KR_EINVAL;
+    if (ws_bytes < need) return KR_ECAPACITY;
+    Carve c(ws);
+    SelArgs a;
+    a.n_seg = n_seg;
+    a.n_cand = n_cand;
+    a.cand_off = cand_off;
+    a.obs_off = obs_off;
+    a.obs_idx = obs_idx;
+    a.score = score;
+    a.unc = unc;
+    a.k[0] = k1;
+    a.k[1] = k2;
+    a.k[2] = k3;
+    a.k[3] = k;
+    a.npass = unc ? 4 : 3;
+    a.max_tiles = n_cand / KR_SEL_TILE + n_seg;
+    a.tile_off = c.take<int64_t>(n_seg + 1);
+    a.flag = c.take<int32_t>(1);
+    a.part_key = c.take<uint64_t>(a.max_tiles * 4 * KR_SEL_LIST);
+    a.part_idx = c.take<int32_t>(a.max_tiles * 4 * KR_SEL_LIST);
+    a.sel = sel_out;
+    a.count = count_out;
+    a.status = status_out;
+    return launch_select(a, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
+}
+
+int32_t kr_hv_converged(int32_t n, const double *hv_history, int32_t R, double eps)
+{
+    if (R < 1 || !hv_history || n - 1 < R) return 0;
+    double s = 0.0;
+    for (int b = n - R; b < n; ++b) {
+        if (!(hv_history[b - 1] != 0.0)) return 0;
+        s = s + (hv_history[b] - hv_history[b - 1]) / hv_history[b - 1];
+    }
+    return s / R < eps ? 1 : 0;
+}
+
 kr_status kr_set_phase_events(int32_t phase, void *start_event, void *stop_event)
 {
     if (phase < 0 || phase > 2) return KR_EINVAL;

@@ -156,4 +156,42 @@ hipError_t launch_mb_enum_gather(const MbArgs &a, const int64_t *base, const int
                                  double *out_T, double *out_E, int32_t *out_f, int32_t *out_choice,
                                  int64_t *n_out, int64_t slots, hipStream_t st);
 
+// mbo.hip: scores and batch selection of the Bayesian optimisation (Section 4.3,
+// Algorithm 1).
+#define KR_HVI_TILE 1024  // candidates per block of the score kernel
+#define KR_SEL_TILE 4096  // candidates per block of the selection tile kernel
+#define KR_SEL_LIST 64    // entries of a wave's top list (one per lane)
+
+struct HviArgs {
+    int32_t n_seg;
+    int64_t n_cand, n_obs;
+    const int64_t *cand_off, *obs_off;
+    const double *T_hat, *E_hat, *T_obs, *E_obs;
+    double p_static;
+    double *fr_T, *fr_E;  // [3][n_obs]: variant v's frontier of partition g at obs_off[g]
+    int32_t *fr_n;        // [n_seg][3] frontier sizes, -1 for a partition with bad counts
+    double *hvi, *hv, *ref;
+    int32_t *status;
+};
+hipError_t launch_hvi(const HviArgs &a, hipStream_t st);
+hipError_t launch_uncertainty(int M, int64_t n, const double *Tm, const double *Em, double *unc,
+                              hipStream_t st);
+
+struct SelArgs {
+    int32_t n_seg;
+    int64_t n_cand;
+    const int64_t *cand_off, *obs_off, *obs_idx;
+    const double *score, *unc;  // unc == nullptr: no exploration pass
+    int32_t k[4];               // k1, k2, k3, k
+    int npass;                  // 3 or 4
+    int64_t max_tiles;          // launch bound on the selection tiles
+    int64_t *tile_off;          // [n_seg + 1]
+    int32_t *flag;              // [1] set when a score is NaN
+    uint64_t *part_key;         // [max_tiles][npass][KR_SEL_LIST]
+    int32_t *part_idx;
+    int64_t *sel;               // [n_seg][k]
+    int32_t *count, *status;
+};
+hipError_t launch_select(const SelArgs &a, hipStream_t st);
+
 }  // namespace kr

@@ -276,3 +276,42 @@ def microbatch_components(seed: int, n_comp: int, freqs: Sequence[float]) -> tup
     T = t0[:, None] * (alpha[:, None] * fmax / f[None, :] + 1.0 - alpha[:, None])
     E = P0[:, None] * (f[None, :] / fmax) ** gamma[:, None] * T
     return T, E
+
+
+# ---- inputs of the Bayesian optimisation's scores and selection (Section 4.3) --------
+# Appendix C's settings for a large partition: 96 initial samples, batches of 32, an
+# ensemble of 5; the batch shares 0.4 / 0.2 / 0.2 of total / dynamic / static energy
+# rounded to whole candidates, the rest by uncertainty.
+MBO_N_INIT = 96
+MBO_BATCH = 32
+MBO_PASSES = (13, 6, 6)
+MBO_MEMBERS = 5
+NOISE_TABLE = 1 << 20
+
+
+def mbo_observations(seed: int, n_cand: Sequence[int], n_obs: int) -> tuple:
+    """The measured sample of each partition: n_obs candidate indices drawn uniformly
+    (repeats allowed) and a measurement-noise draw in [-1, 1) for the time and the energy
+    of each.  Returns (obs_off int64[P+1], obs_idx int64 local indices, z [n][2])."""
+    P = len(n_cand)
+    u = splitmix64_uniform(seed, 0, 3 * P * n_obs).reshape(P * n_obs, 3)
+    n = np.repeat(np.asarray(n_cand, dtype=np.int64), n_obs)
+    idx = np.minimum((u[:, 0] * n).astype(np.int64), np.maximum(n - 1, 0))
+    obs_off = np.arange(P + 1, dtype=np.int64) * n_obs
+    return obs_off, idx, 2.0 * u[:, 1:] - 1.0
+
+
+def noise_table(seed: int) -> np.ndarray:
+    """NOISE_TABLE uniform draws in [-1, 1), indexed by noise_index."""
+    return 2.0 * splitmix64_uniform(seed, 0, NOISE_TABLE) - 1.0
+
+
+def noise_index(stream: int, x):
+    """Table slot of draw `stream` for global candidate index x (numpy or torch int64)."""
+    return (x * 0x9E3779B1 + (stream + 1) * 0x85EBCA77) & (NOISE_TABLE - 1)
+
+
+def perturb(v, z, rel: float):
+    """v * (1 + rel * z): a prediction or measurement off by up to rel (numpy or torch;
+    one rounding per operation, so both give the same bits)."""
+    return v * (1.0 + rel * z)

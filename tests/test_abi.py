@@ -70,6 +70,35 @@ def test_host_validation_without_gpu():
     assert L.kr_compose_frontiers(4, one, one, one, 1024, -1.0, one, one, one, one, one, one, one,
                                   one, one, one, one, 1 << 30, null) == b.KR_EINVAL
     assert b.candidates_per_partition(I.SPACES[2]["space"]) == 1148928
+    # scores and selection: shapes and counts are checked before any launch
+    assert L.kr_hvi_scores_workspace(0, 10) == 0 and L.kr_hvi_scores_workspace(4, 0) == 0
+    assert L.kr_select_batch_workspace(0, 10) == 0
+    assert L.kr_hvi_scores(2, 10, one, one, one, 8, one, one, one, 90.0, one, one, one, one, one,
+                           16, null) == b.KR_ECAPACITY
+    assert L.kr_hvi_scores(2, 10, null, one, one, 8, one, one, one, 90.0, one, one, one, one, one,
+                           1 << 20, null) == b.KR_EINVAL
+    big = 1 << 20
+    for ks in ((13, 6, 6, 32), (0, 0, 0, 0), (64, 0, 0, 64)):
+        assert L.kr_select_batch(1, 10, one, one, one, one, one, *ks, one, one, one, one, 16,
+                                 null) == b.KR_ECAPACITY
+    for ks in ((13, 6, 6, 24), (-1, 0, 0, 4), (0, 0, 0, 65)):
+        assert L.kr_select_batch(1, 10, one, one, one, one, one, *ks, one, one, one, one, big,
+                                 null) == b.KR_EINVAL
+    assert L.kr_uncertainty(0, 10, one, one, one, null) == b.KR_EINVAL
+    assert L.kr_uncertainty(65, 10, one, one, one, null) == b.KR_EINVAL
+
+
+def test_hv_stopping_rule_matches_oracle():
+    """The library's host stopping rule against the oracle's on hand-made histories."""
+    import oracle
+    from paper_2601_17654_amd import binding as b
+
+    cases = [[1.0, 1.0005, 1.0006], [1.0, 1.1, 1.1001], [1.0, 1.0], [1.0, 1.0, 1.0],
+             [0.0, 0.0, 1.0, 1.0], [0.0, 1.0, 1.0, 1.0], [2.0, 2.001, 2.0021, 2.0022, 2.00225]]
+    for h in cases:
+        for R in (1, 2, 3):
+            for eps in (1e-3, 1e-4):
+                assert b.hv_converged(h, R, eps) == oracle.hv_converged(h, R, eps), (h, R, eps)
 
 
 def test_oracle_and_library_share_nothing():
