@@ -95,6 +95,15 @@ def copy_calibration():
     print(json.dumps({"copy_bytes_read": n * 8, "copy_bytes_written": n * 8, "launches": 3}))
 
 
+def mk_events(n):
+    import torch
+
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+    for e in evs:
+        e.record()  # creates the HIP event behind the handle
+    return evs
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -103,7 +112,7 @@ def main():
     ap.add_argument("--skip-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true")
-    ap.add_argument("--part", choices=["all", "eval", "compose"], default="all",
+    ap.add_argument("--part", choices=["all", "eval", "compose", "mbo"], default="all",
                     help="profiling aid: run only one half of the step (prints no bench line)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -138,6 +147,10 @@ def main():
     comp = kr.compose_frontiers(off4_d, T4_d, E4_d, B)
     torch.cuda.synchronize()
 
+    if args.part == "mbo":
+        res, _ = bench_mbo(kr, I, torch, sp, d, args, mk_events)
+        log("mbo: " + json.dumps(res))
+        return
     if args.part != "all":
         for _ in range(args.warmup + args.steps):
             if args.part == "eval":
@@ -161,11 +174,7 @@ def main():
         ev[3].record()
         return f
 
-    def mk(n):
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
-        for e in evs:
-            e.record()  # creates the HIP event behind the handle
-        return evs
+    mk = mk_events
 
     for _ in range(args.warmup):
         step(mk(4), [mk(2), mk(2)])
@@ -273,6 +282,8 @@ def main():
         "configurations_per_s": n_configs / (mx_ms * 1e-3),
         "grid_ms": round(mb_ms, 4), "grid_bins": MB_BINS, "grid_points": int(mres.T.numel())}
 
+    out["mbo"], mbo_ctx = bench_mbo(kr, I, torch, sp, d, args, mk)
+
     if not args.skip_cpu:
         import oracle
 
@@ -299,22 +310,163 @@ def main():
         out["cpu_baseline_compose"] = {"value": cells / el, "unit": "cells/s", "cores": 1,
                                        "kind": "oracle", "sample": "full compose-stress batch, "
                                        "%.1f s" % el}
-        mT_h, mE_h = mfr.T.cpu().numpy(), mfr.E.cpu().numpy()
+        # the oracle's own per-(type, frequency) frontiers of the same tables
+        oseg, oT, oE = [0], [], []
+        for t in range(mK):
+            Tr, Er = oracle.evaluate_partition(msp, mb_w.t, mb_w.pw, mb_w.tc, mb_w.pc, t)
+            for f in range(mF):
+                ix = oracle.pareto(Tr[f * mCf:(f + 1) * mCf], Er[f * mCf:(f + 1) * mCf])
+                oT.append(Tr[f * mCf + ix])
+                oE.append(Er[f * mCf + ix])
+                oseg.append(oseg[-1] + len(ix))
+        oseg, oT, oE = np.array(oseg, dtype=np.int64), np.concatenate(oT), np.concatenate(oE)
         t0 = time.perf_counter()
-        rx = oracle.microbatch_exact(mseg, mT_h, mE_h, mK, mF, mseq, mcT, mcE)
+        rx = oracle.microbatch_exact(oseg, oT, oE, mK, mF, mseq, mcT, mcE)
         el = time.perf_counter() - t0
         t0 = time.perf_counter()
-        ro = oracle.microbatch(mseg, mT_h, mE_h, mK, mF, mseq, mcT, mcE, n_bins=MB_BINS)
+        ro = oracle.microbatch(oseg, oT, oE, mK, mF, mseq, mcT, mcE, n_bins=MB_BINS)
         elg = time.perf_counter() - t0
         out["microbatch"]["cpu_baseline"] = {
             "value": n_configs / el, "unit": "configurations/s", "cores": 1, "kind": "oracle",
             "sample": "the same microbatch by enumeration, %.4f s (grid composition %.2f s)"
                       % (el, elg),
-            "parity": bool(np.array_equal(rx[0], mexa.T.cpu().numpy()) and
+            "parity": bool(np.array_equal(oseg, mseg) and
+                           np.array_equal(rx[0], mexa.T.cpu().numpy()) and
                            np.array_equal(rx[3], mexa.choice.cpu().numpy()) and
                            np.array_equal(ro[0], mres.T.cpu().numpy()) and
                            np.array_equal(ro[3], mres.choice.cpu().numpy()))}
+        out["mbo"]["cpu_baseline"] = mbo_cpu_baseline(oracle, I, w, mbo_ctx, args.cpu_seconds)
     print(json.dumps(out))
+
+
+def mbo_inputs(kr, I, torch, sp, d, seed=11):
+    """Predictions of every eval-stress candidate (the cost model), a measured sample of
+    96 per partition and a 5-member ensemble around the predictions, all on the device."""
+    T, E = kr.evaluate_partition(sp, *d)
+    T, E = T.reshape(-1), E.reshape(-1)
+    C, P = sp.n_cand, sp.n_parts
+    obs_off, idx, z = I.mbo_observations(seed, [C] * P, I.MBO_N_INIT)
+    gidx = torch.from_numpy(np.repeat(np.arange(P, dtype=np.int64) * C, I.MBO_N_INIT) + idx).cuda()
+    zd = torch.from_numpy(z).cuda()
+    To = I.perturb(T[gidx], zd[:, 0].contiguous(), 0.02)
+    Eo = I.perturb(E[gidx], zd[:, 1].contiguous(), 0.02)
+    tab = torch.from_numpy(I.noise_table(seed + 1)).cuda()
+    x = torch.arange(C * P, device="cuda", dtype=torch.int64)
+    Tm = torch.empty((I.MBO_MEMBERS, C * P), dtype=torch.float64, device="cuda")
+    Em = torch.empty_like(Tm)
+    for m in range(I.MBO_MEMBERS):
+        Tm[m] = I.perturb(T, tab[I.noise_index(2 * m, x)], 0.05)
+        Em[m] = I.perturb(E, tab[I.noise_index(2 * m + 1, x)], 0.05)
+    del x
+    return dict(T=T, E=E, To=To, Eo=Eo, Tm=Tm, Em=Em, idx=idx, z=z, seed=seed,
+                cand_off=torch.arange(P + 1, dtype=torch.int64, device="cuda") * C,
+                obs_off=torch.from_numpy(obs_off).cuda(),
+                idx_d=torch.from_numpy(idx).cuda())
+
+
+def bench_mbo(kr, I, torch, sp, d, args, mk):
+    """Scores and batch selection of the Bayesian optimisation (Section 4.3, Algorithm 1)
+    over the whole eval-stress candidate space: the three HVI scores of every candidate,
+    the ensemble uncertainty, and one batch of 32 per partition."""
+    c = mbo_inputs(kr, I, torch, sp, d)
+    n = c["T"].numel()
+    P = sp.n_parts
+    k1, k2, k3 = I.MBO_PASSES
+    sc = kr.hvi_scores(c["cand_off"], c["T"], c["E"], c["obs_off"], c["To"], c["Eo"], sp.p_static)
+    unc = kr.uncertainty(c["Tm"], c["Em"])
+    bt = kr.select_batch(c["cand_off"], sc.hvi, unc, c["obs_off"], c["idx_d"], k1, k2, k3,
+                         I.MBO_BATCH)
+    torch.cuda.synchronize()
+
+    def run():
+        kr.hvi_scores(c["cand_off"], c["T"], c["E"], c["obs_off"], c["To"], c["Eo"],
+                      sp.p_static, check=False, out=sc)
+        kr.uncertainty(c["Tm"], c["Em"], out=unc)
+        kr.select_batch(c["cand_off"], sc.hvi, unc, c["obs_off"], c["idx_d"], k1, k2, k3,
+                        I.MBO_BATCH, check=False, out=bt)
+
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    steps = args.steps
+    ev = [mk(2) for _ in range(steps)]
+    ph = [[mk(2) for _ in range(3)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    for k in range(steps):
+        kr.set_phase_events(kr.PHASE_HVI, *ph[k][0])
+        kr.set_phase_events(kr.PHASE_UNC, *ph[k][1])
+        kr.set_phase_events(kr.PHASE_SELECT, *ph[k][2])
+        ev[k][0].record()
+        run()
+        ev[k][1].record()
+    torch.cuda.synchronize()
+    for p in (kr.PHASE_HVI, kr.PHASE_UNC, kr.PHASE_SELECT):
+        kr.set_phase_events(p)
+    assert int(sc.status.item()) == 0 and int(bt.status.item()) == 0
+    step_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    hvi_ms, unc_ms, sel_ms = (float(np.mean([q[i][0].elapsed_time(q[i][1]) for q in ph]))
+                              for i in range(3))
+
+    def roof(nbytes, ms, kernel):
+        a = nbytes / (ms * 1e-3) / 1e9
+        return {"bound": "hbm", "achieved": round(a, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(a / HBM_PEAK_GBS, 4), "traffic": None, "kernel": kernel,
+                "kernel_ms": round(ms, 4), "algorithmic_bytes": nbytes}
+
+    M = I.MBO_MEMBERS
+    res = {
+        "workload": "mbo-eval-stress: every candidate of the 1,024 eval-stress partitions "
+                    "(135,168 each) scored against 96 measured points per partition "
+                    "(3 HVI variants), a 5-member ensemble, one batch of 32 per partition "
+                    "(13 / 6 / 6 by HVI, the rest by uncertainty)",
+        "candidates": n, "partitions": P,
+        "step_ms": round(step_ms, 4), "candidates_per_s": n / (step_ms * 1e-3),
+        "hvi_ms": round(hvi_ms, 4), "uncertainty_ms": round(unc_ms, 4),
+        "select_tile_ms": round(sel_ms, 4),
+        "roofline": roof(40 * n, hvi_ms, "hvi_score_kernel (2 predictions in, 3 scores out)"),
+        "uncertainty_roofline": roof((16 * M + 8) * n, unc_ms,
+                                     "unc_kernel (%d members x 2 predictions in, 1 out)" % M),
+        "select_roofline": roof(32 * n, sel_ms, "sel_tile_kernel (4 scores in)"),
+    }
+    ctx = dict(c=c, sc=sc, unc=unc, bt=bt, sp=sp)
+    return res, ctx
+
+
+def mbo_cpu_baseline(oracle, I, w, ctx, seconds):
+    """The oracle's scores, uncertainty and selection on whole partitions from the start
+    of the batch (its own cost-model predictions), for about `seconds`; scores compared
+    with the GPU's within the rounding bound of the parity tests."""
+    c, sp = ctx["c"], ctx["sp"]
+    C = sp.n_cand
+    U = 2.0 ** -53
+    gh = ctx["sc"].hvi
+    tab = I.noise_table(c["seed"] + 1)
+    t0 = time.perf_counter()
+    n, worst = 0, 0.0
+    while n < sp.n_parts and (time.perf_counter() - t0) < seconds:
+        Tr, Er = oracle.evaluate_partition(sp, w.t, w.pw, w.tc, w.pc, n)
+        o = slice(n * I.MBO_N_INIT, (n + 1) * I.MBO_N_INIT)
+        To = I.perturb(Tr[c["idx"][o]], c["z"][o, 0], 0.02)
+        Eo = I.perturb(Er[c["idx"][o]], c["z"][o, 1], 0.02)
+        rh, rhv, _ = oracle.hvi([0, C], Tr, Er, [0, I.MBO_N_INIT], To, Eo, sp.p_static)
+        xs = np.arange(n * C, (n + 1) * C, dtype=np.int64)
+        Tm = np.stack([I.perturb(Tr, tab[I.noise_index(2 * m, xs)], 0.05)
+                       for m in range(I.MBO_MEMBERS)])
+        Em = np.stack([I.perturb(Er, tab[I.noise_index(2 * m + 1, xs)], 0.05)
+                       for m in range(I.MBO_MEMBERS)])
+        ru = oracle.uncertainty(Tm, Em)
+        k1, k2, k3 = I.MBO_PASSES
+        oracle.select([0, C], rh, ru, [0, I.MBO_N_INIT], c["idx"][o], k1, k2, k3, I.MBO_BATCH)
+        g = gh[:, n * C:(n + 1) * C].cpu().numpy()
+        tol = (3 * (I.MBO_N_INIT + 1) + 8) * U * (rhv[0][:, None] + np.maximum(abs(g), abs(rh)))
+        worst = max(worst, float(np.max(np.abs(g - rh) / tol)))
+        n += 1
+    el = time.perf_counter() - t0
+    return {"value": n * C / el, "unit": "candidates/s", "cores": 1, "kind": "oracle",
+            "sample": "first %d of the 1024 partitions (%d candidates): cost model, 3 HVI "
+                      "scores, uncertainty and selection, single-threaded C oracle, %.1f s"
+                      % (n, n * C, el),
+            "parity_worst_error_over_bound": worst}
 
 
 if __name__ == "__main__":

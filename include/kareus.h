@@ -380,10 +380,16 @@ kr_status kr_decode_candidates(const kr_space *space, const int32_t *idx, int64_
  *                       kr_evaluate_and_filter
  *   KR_PHASE_MERGE      its staircase merges and output compaction
  *   KR_PHASE_MINPLUS    the min-plus steps of kr_compose_frontiers
+ *   KR_PHASE_HVI        the per-candidate score kernel of kr_hvi_scores
+ *   KR_PHASE_SELECT     the per-tile top-k kernel of kr_select_batch
+ *   KR_PHASE_UNC        the kernel of kr_uncertainty
  */
 #define KR_PHASE_EVAL_TILE 0
 #define KR_PHASE_MERGE 1
 #define KR_PHASE_MINPLUS 2
+#define KR_PHASE_HVI 3
+#define KR_PHASE_SELECT 4
+#define KR_PHASE_UNC 5
 kr_status kr_set_phase_events(int32_t phase, void *start_event, void *stop_event);
 
 /* Human-readable name of a status code. */

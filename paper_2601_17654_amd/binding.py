@@ -123,7 +123,7 @@ def _workspace(nbytes: int) -> torch.Tensor:
     return buf
 
 
-PHASE_EVAL_TILE, PHASE_MERGE, PHASE_MINPLUS = 0, 1, 2
+PHASE_EVAL_TILE, PHASE_MERGE, PHASE_MINPLUS, PHASE_HVI, PHASE_SELECT, PHASE_UNC = range(6)
 
 
 def set_phase_events(phase: int, start=None, stop=None) -> None:

@@ -141,7 +141,7 @@ bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)
 }
 
 // Caller-owned events recorded around a phase (kr_set_phase_events).
-hipEvent_t g_phase_ev[3][2] = {};
+hipEvent_t g_phase_ev[6][2] = {};
 
 void phase_mark(int phase, int which, hipStream_t st)
 {
@@ -676,7 +676,8 @@ kr_status kr_hvi_scores(int32_t n_seg, int64_t n_cand, const int64_t *cand_off,
     a.hv = hv_out;
     a.ref = ref_out;
     a.status = status_out;
-    return launch_hvi(a, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
+    return launch_hvi(a, g_phase_ev[KR_PHASE_HVI], (hipStream_t)stream) == hipSuccess ? KR_OK
+                                                                                  : KR_EHIP;
 }
 
 kr_status kr_uncertainty(int32_t n_members, int64_t n, const double *T_m, const double *E_m,
@@ -684,7 +685,8 @@ kr_status kr_uncertainty(int32_t n_members, int64_t n, const double *T_m, const 
 {
     if (n_members < 1 || n_members > 64 || n < 0 || (n > 0 && (!T_m || !E_m || !unc_out)))
         return KR_EINVAL;
-    return launch_uncertainty(n_members, n, T_m, E_m, unc_out, (hipStream_t)stream) ==
+    return launch_uncertainty(n_members, n, T_m, E_m, unc_out, g_phase_ev[KR_PHASE_UNC],
+                              (hipStream_t)stream) ==
                    hipSuccess
                ? KR_OK
                : KR_EHIP;
@@ -736,7 +738,9 @@ kr_status kr_select_batch(int32_t n_seg, int64_t n_cand, const int64_t *cand_off
     a.sel = sel_out;
     a.count = count_out;
     a.status = status_out;
-    return launch_select(a, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
+    return launch_select(a, g_phase_ev[KR_PHASE_SELECT], (hipStream_t)stream) == hipSuccess
+               ? KR_OK
+               : KR_EHIP;
 }
 
 int32_t kr_hv_converged(int32_t n, const double *hv_history, int32_t R, double eps)
@@ -752,7 +756,7 @@ int32_t kr_hv_converged(int32_t n, const double *hv_history, int32_t R, double e
 
 kr_status kr_set_phase_events(int32_t phase, void *start_event, void *stop_event)
 {
-    if (phase < 0 || phase > 2) return KR_EINVAL;
+    if (phase < 0 || phase > 5) return KR_EINVAL;
     g_phase_ev[phase][0] = (hipEvent_t)start_event;
     g_phase_ev[phase][1] = (hipEvent_t)stop_event;
     return KR_OK;

@@ -159,7 +159,7 @@ hipError_t launch_mb_enum_gather(const MbArgs &a, const int64_t *base, const int
 // mbo.hip: scores and batch selection of the Bayesian optimisation (Section 4.3,
 // Algorithm 1).
 #define KR_HVI_TILE 1024  // candidates per block of the score kernel
-#define KR_SEL_TILE 4096  // candidates per block of the selection tile kernel
+#define KR_SEL_TILE 16384  // candidates per block of the selection tile kernel
 #define KR_SEL_LIST 64    // entries of a wave's top list (one per lane)
 
 struct HviArgs {
@@ -173,9 +173,9 @@ struct HviArgs {
     double *hvi, *hv, *ref;
     int32_t *status;
 };
-hipError_t launch_hvi(const HviArgs &a, hipStream_t st);
+hipError_t launch_hvi(const HviArgs &a, hipEvent_t *ev, hipStream_t st);
 hipError_t launch_uncertainty(int M, int64_t n, const double *Tm, const double *Em, double *unc,
-                              hipStream_t st);
+                              hipEvent_t *ev, hipStream_t st);
 
 struct SelArgs {
     int32_t n_seg;
@@ -192,6 +192,6 @@ struct SelArgs {
     int64_t *sel;               // [n_seg][k]
     int32_t *count, *status;
 };
-hipError_t launch_select(const SelArgs &a, hipStream_t st);
+hipError_t launch_select(const SelArgs &a, hipEvent_t *ev, hipStream_t st);
 
 }  // namespace kr

@@ -177,59 +177,131 @@ __global__ void __launch_bounds__(KR_BLOCK) hvi_score_kernel(HviArgs a)
         const double rT = a.ref[g * 4];
         const double rE[3] = {a.ref[g * 4 + 1], a.ref[g * 4 + 2], a.ref[g * 4 + 3]};
         const int64_t x0 = c0 > t0 ? c0 : t0, x1 = c1 < t1 ? c1 : t1;
-        for (int64_t x = x0 + tid; x < x1; x += KR_BLOCK) {
-            const double t = a.T_hat[x], e = a.E_hat[x];
+        // all of this thread's candidates of the partition are loaded before any is
+        // scored, so their loads are in flight together
+        constexpr int kPer = KR_HVI_TILE / KR_BLOCK;
+        double t[kPer], e[kPer];
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            const int64_t x = x0 + tid + (int64_t)j * KR_BLOCK;
+            t[j] = x < x1 ? a.T_hat[x] : 0.0;
+            e[j] = x < x1 ? a.E_hat[x] : 0.0;
+        }
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            const int64_t x = x0 + tid + (int64_t)j * KR_BLOCK;
+            if (x >= x1) break;
 #pragma unroll
             for (int v = 0; v < 3; ++v) {
                 const double h = bad ? NAN
-                                     : hvi_one(fT[v], fE[v], s[v], rT, rE[v], t,
-                                               energy_variant(v, t, e, a.p_static));
+                                     : hvi_one(fT[v], fE[v], s[v], rT, rE[v], t[j],
+                                               energy_variant(v, t[j], e[j], a.p_static));
                 a.hvi[(int64_t)v * a.n_cand + x] = h;
             }
         }
     }
 }
 
-hipError_t launch_hvi(const HviArgs &a, hipStream_t st)
+// ev: optional start/stop events around the score kernel (null entries: none).
+static void mark(hipEvent_t *ev, int which, hipStream_t st)
+{
+    if (ev && ev[0] && ev[1]) (void)hipEventRecord(ev[which], st);
+}
+
+hipError_t launch_hvi(const HviArgs &a, hipEvent_t *ev, hipStream_t st)
 {
     hipLaunchKernelGGL(hvi_init_kernel, dim3(1), dim3(1), 0, st, a.status);
     hipLaunchKernelGGL(hvi_prep_kernel, dim3(a.n_seg), dim3(KR_BLOCK), 0, st, a);
     if (a.n_cand > 0) {
         const int64_t blocks = (a.n_cand + KR_HVI_TILE - 1) / KR_HVI_TILE;
+        mark(ev, 0, st);
         hipLaunchKernelGGL(hvi_score_kernel, dim3((unsigned)blocks), dim3(KR_BLOCK), 0, st, a);
+        mark(ev, 1, st);
     }
     return hipGetLastError();
 }
 
-// Population standard deviation of the members' T plus that of their E.
-__global__ void __launch_bounds__(KR_BLOCK) unc_kernel(int M, int64_t n, const double *Tm,
+// Population standard deviation of the members' T plus that of their E.  With M a
+// compile-time count the members stay in registers between the mean and the deviations;
+// the generic form reads them twice.
+template <int MC>
+__global__ void __launch_bounds__(KR_BLOCK) unc_kernel(int M_rt, int64_t n, const double *Tm,
                                                      const double *Em, double *unc)
 {
+    const int M = MC > 0 ? MC : M_rt;
     const int64_t stride = (int64_t)gridDim.x * KR_BLOCK;
+    if constexpr (MC > 0) {
+        // two candidates per step, all their members loaded before either is reduced
+        for (int64_t x = (int64_t)blockIdx.x * KR_BLOCK + threadIdx.x; x < n; x += 2 * stride) {
+            const int64_t xs[2] = {x, x + stride < n ? x + stride : x};
+            double t[2][MC], e[2][MC];
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+                for (int m = 0; m < MC; ++m) {
+                    t[j][m] = Tm[(int64_t)m * n + xs[j]];
+                    e[j][m] = Em[(int64_t)m * n + xs[j]];
+                }
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                double st = 0.0, se = 0.0;
+#pragma unroll
+                for (int m = 0; m < MC; ++m) {
+                    st = st + t[j][m];
+                    se = se + e[j][m];
+                }
+                const double mt = st / M, me = se / M;
+                double vt = 0.0, ve = 0.0;
+#pragma unroll
+                for (int m = 0; m < MC; ++m) {
+                    const double dt = t[j][m] - mt, de = e[j][m] - me;
+                    vt = vt + dt * dt;
+                    ve = ve + de * de;
+                }
+                if (j == 0 || x + stride < n) unc[xs[j]] = sqrt(vt / M) + sqrt(ve / M);
+            }
+        }
+        return;
+    }
     for (int64_t x = (int64_t)blockIdx.x * KR_BLOCK + threadIdx.x; x < n; x += stride) {
         double st = 0.0, se = 0.0;
-        for (int m = 0; m < M; ++m) {
-            st = st + Tm[(int64_t)m * n + x];
-            se = se + Em[(int64_t)m * n + x];
+        {
+            for (int m = 0; m < M; ++m) {
+                st = st + Tm[(int64_t)m * n + x];
+                se = se + Em[(int64_t)m * n + x];
+            }
+            const double mt = st / M, me = se / M;
+            double vt = 0.0, ve = 0.0;
+            for (int m = 0; m < M; ++m) {
+                const double dt = Tm[(int64_t)m * n + x] - mt, de = Em[(int64_t)m * n + x] - me;
+                vt = vt + dt * dt;
+                ve = ve + de * de;
+            }
+            unc[x] = sqrt(vt / M) + sqrt(ve / M);
         }
-        const double mt = st / M, me = se / M;
-        double vt = 0.0, ve = 0.0;
-        for (int m = 0; m < M; ++m) {
-            const double dt = Tm[(int64_t)m * n + x] - mt, de = Em[(int64_t)m * n + x] - me;
-            vt = vt + dt * dt;
-            ve = ve + de * de;
-        }
-        unc[x] = sqrt(vt / M) + sqrt(ve / M);
     }
 }
 
 hipError_t launch_uncertainty(int M, int64_t n, const double *Tm, const double *Em, double *unc,
-                              hipStream_t st)
+                              hipEvent_t *ev, hipStream_t st)
 {
     if (n == 0) return hipSuccess;
     const int64_t blocks = (n + KR_BLOCK - 1) / KR_BLOCK;
     const unsigned grid = (unsigned)(blocks < 8192 ? blocks : 8192);
-    hipLaunchKernelGGL(unc_kernel, dim3(grid), dim3(KR_BLOCK), 0, st, M, n, Tm, Em, unc);
+    const dim3 g(grid), b(KR_BLOCK);
+    mark(ev, 0, st);
+    switch (M) {
+    case 1: hipLaunchKernelGGL(unc_kernel<1>, g, b, 0, st, M, n, Tm, Em, unc); break;
+    case 2: hipLaunchKernelGGL(unc_kernel<2>, g, b, 0, st, M, n, Tm, Em, unc); break;
+    case 3: hipLaunchKernelGGL(unc_kernel<3>, g, b, 0, st, M, n, Tm, Em, unc); break;
+    case 4: hipLaunchKernelGGL(unc_kernel<4>, g, b, 0, st, M, n, Tm, Em, unc); break;
+    case 5: hipLaunchKernelGGL(unc_kernel<5>, g, b, 0, st, M, n, Tm, Em, unc); break;
+    case 6: hipLaunchKernelGGL(unc_kernel<6>, g, b, 0, st, M, n, Tm, Em, unc); break;
+    case 7: hipLaunchKernelGGL(unc_kernel<7>, g, b, 0, st, M, n, Tm, Em, unc); break;
+    case 8: hipLaunchKernelGGL(unc_kernel<8>, g, b, 0, st, M, n, Tm, Em, unc); break;
+    default: hipLaunchKernelGGL(unc_kernel<0>, g, b, 0, st, M, n, Tm, Em, unc); break;
+    }
+    mark(ev, 1, st);
     return hipGetLastError();
 }
 
@@ -328,12 +400,17 @@ __global__ void __launch_bounds__(KR_BLOCK) sel_plan_kernel(SelArgs a)
     }
 }
 
-// One block per tile: each pass's best KR_SEL_LIST unmeasured candidates of the tile.
+// One block per tile: each pass's best KR_SEL_LIST unmeasured candidates of the tile, in
+// one sweep over the scores of all passes.  Per pass a wave keeps its sorted list and a
+// threshold (the list's last entry); candidates that beat the threshold are compacted
+// into an LDS buffer, and the buffer is sorted and merged into the list only when the
+// next batch would overflow it, so merges grow with the log of the candidates seen
+// rather than with their number.
 __global__ void __launch_bounds__(KR_BLOCK) sel_tile_kernel(SelArgs a)
 {
     __shared__ uint32_t excl[KR_SEL_TILE / 32];
-    __shared__ uint64_t lkey[KR_WAVES][KR_SEL_LIST];
-    __shared__ int32_t lidx[KR_WAVES][KR_SEL_LIST];
+    __shared__ uint64_t bkey[KR_WAVES][4][KR_SEL_LIST];
+    __shared__ int32_t bidx[KR_WAVES][4][KR_SEL_LIST];
     const int64_t b = blockIdx.x;
     if (b >= a.tile_off[a.n_seg]) return;
     int lo = 0, hi = a.n_seg;
@@ -354,46 +431,103 @@ __global__ void __launch_bounds__(KR_BLOCK) sel_tile_kernel(SelArgs a)
         if (x >= l0 && x < l1) atomicOr(&excl[(x - l0) >> 5], 1u << ((x - l0) & 31));
     }
     __syncthreads();
+    const int np = a.npass;
+    const double *src[4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+        src[p] = (p < 3 ? a.score + (int64_t)p * a.n_cand : (p < np ? a.unc : a.score)) + c0;
+    Entry L[4];
+    Entry thr[4];
+    int cnt[4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        L[p].key = 0;
+        L[p].idx = INT32_MAX;
+        thr[p] = L[p];
+        cnt[p] = 0;
+    }
     constexpr int kPerWave = KR_SEL_TILE / KR_WAVES;
+    const int64_t w0 = l0 + (int64_t)wave * kPerWave;  // this wave's first local index
     bool nan_seen = false;
-    for (int p = 0; p < a.npass; ++p) {
-        const double *s = (p < 3 ? a.score + (int64_t)p * a.n_cand : a.unc) + c0;
-        Entry list;
-        list.key = 0;
-        list.idx = INT32_MAX;
-        for (int i = 0; i < kPerWave; i += 64) {
-            const int64_t off = (int64_t)wave * kPerWave + i + lane;  // offset in the tile
-            const int64_t x = l0 + off;
+    double cur[4], nxt[4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) cur[p] = p < np && w0 + lane < l1 ? src[p][w0 + lane] : 0.0;
+    for (int i = 0; i < kPerWave; i += 64) {
+        const int64_t x = w0 + i + lane;
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+            nxt[p] = p < np && i + 64 < kPerWave && x + 64 < l1 ? src[p][x + 64] : 0.0;
+        const int64_t off = x - l0;
+        const bool in = x < l1 && !((excl[(off >> 5) & (KR_SEL_TILE / 32 - 1)] >> (off & 31)) & 1u);
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            if (p >= np) break;
+            const double v = cur[p];
+            nan_seen = nan_seen || (x < l1 && v != v);
             Entry c;
-            c.key = 0;
-            c.idx = INT32_MAX;
-            if (x < l1) {
-                const double v = s[x];
-                nan_seen = nan_seen || v != v;
-                if (v == v && !((excl[off >> 5] >> (off & 31)) & 1u)) {
-                    c.key = score_key(v);
-                    c.idx = (int32_t)x;
-                }
+            c.key = in && v == v ? score_key(v) : 0;
+            c.idx = (int32_t)x;
+            bool pass = c.key != 0 && better(c, thr[p]);
+            uint64_t m = __ballot(pass);
+            if (m == 0) continue;
+            int n = __popcll(m);
+            if (cnt[p] + n > KR_SEL_LIST) {
+                Entry e;
+                e.key = lane < cnt[p] ? bkey[wave][p][lane] : 0;
+                e.idx = lane < cnt[p] ? bidx[wave][p][lane] : INT32_MAX;
+                L[p] = wave_merge(L[p], wave_sort(e, lane), lane);
+                thr[p].key = lane_u64(L[p].key, 63);
+                thr[p].idx = lane_i32(L[p].idx, 63);
+                cnt[p] = 0;
+                pass = c.key != 0 && better(c, thr[p]);
+                m = __ballot(pass);
+                n = __popcll(m);
             }
-            list = wave_offer(list, c, lane);
+            if (pass) {
+                const int pos = cnt[p] + (int)__builtin_amdgcn_mbcnt_hi(
+                                             (uint32_t)(m >> 32),
+                                             __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+                bkey[wave][p][pos] = c.key;
+                bidx[wave][p][pos] = c.idx;
+            }
+            cnt[p] += n;
         }
-        if (wave > 0) {
-            lkey[wave][lane] = list.key;
-            lidx[wave][lane] = list.idx;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) cur[p] = nxt[p];
+    }
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        if (p >= np) break;
+        if (cnt[p] > 0) {
+            Entry e;
+            e.key = lane < cnt[p] ? bkey[wave][p][lane] : 0;
+            e.idx = lane < cnt[p] ? bidx[wave][p][lane] : INT32_MAX;
+            L[p] = wave_merge(L[p], wave_sort(e, lane), lane);
         }
-        __syncthreads();
-        if (wave == 0) {
+    }
+    __syncthreads();  // every wave is done with its buffers
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        if (p >= np) break;
+        bkey[wave][p][lane] = L[p].key;
+        bidx[wave][p][lane] = L[p].idx;
+    }
+    __syncthreads();
+    if (wave == 0) {
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            if (p >= np) break;
+            Entry list = L[p];
             for (int w = 1; w < KR_WAVES; ++w) {
                 Entry o;
-                o.key = lkey[w][lane];
-                o.idx = lidx[w][lane];
+                o.key = bkey[w][p][lane];
+                o.idx = bidx[w][p][lane];
                 list = wave_merge(list, o, lane);
             }
-            const int64_t slot = (b * a.npass + p) * KR_SEL_LIST + lane;
+            const int64_t slot = (b * np + p) * KR_SEL_LIST + lane;
             a.part_key[slot] = list.key;
             a.part_idx[slot] = list.idx;
         }
-        __syncthreads();
     }
     if (nan_seen) *a.flag = 1;
 }
@@ -460,12 +594,14 @@ __global__ void __launch_bounds__(KR_BLOCK) sel_final_kernel(SelArgs a)
     if (lane == 0) a.count[g] = cnt;
 }
 
-hipError_t launch_select(const SelArgs &a, hipStream_t st)
+hipError_t launch_select(const SelArgs &a, hipEvent_t *ev, hipStream_t st)
 {
     hipLaunchKernelGGL(sel_plan_kernel, dim3(1), dim3(KR_BLOCK), 0, st, a);
+    mark(ev, 0, st);
     if (a.max_tiles > 0)
         hipLaunchKernelGGL(sel_tile_kernel, dim3((unsigned)a.max_tiles), dim3(KR_BLOCK), 0, st,
                            a);
+    mark(ev, 1, st);
     hipLaunchKernelGGL(sel_final_kernel, dim3(a.n_seg), dim3(KR_BLOCK), 0, st, a);
     return hipGetLastError();
 }
