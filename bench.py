@@ -65,6 +65,42 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+MBO_COUNTERS = os.path.join(ROOT, "profiles", "mbo_counters_eval_stress.txt")
+MBO_KERNELS = ("hvi_score_kernel", "unc_kernel", "sel_tile_kernel")
+
+
+def mbo_source_hash() -> str:
+    """sha256 (first 16 hex) of what the score, uncertainty and selection kernels are
+    built and launched from."""
+    csrc = os.path.join(ROOT, "paper_2601_17654_amd", "csrc")
+    h = hashlib.sha256()
+    for f in ("mbo.hip", "kr_device.h"):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    with open(os.path.join(csrc, "kr_launch.h")) as fh:
+        h.update(_between(fh.read(), "// mbo.hip", "}  // namespace kr").encode())
+    with open(os.path.join(csrc, "api.hip")) as fh:
+        h.update(_between(fh.read(), "size_t kr_hvi_scores_workspace", "\n}\n\nint32_t "
+                          "kr_hv_converged").encode())
+    return h.hexdigest()[:16]
+
+
+def read_mbo_traffic():
+    """HBM bytes per launch of each score/selection kernel from the committed counter
+    summary, if it was taken on the current sources; else {}."""
+    if not os.path.exists(MBO_COUNTERS):
+        return {}, "no counter summary"
+    vals = {}
+    for line in open(MBO_COUNTERS):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.strip().split("=", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_hash") != mbo_source_hash():
+        return {}, "kernels changed since counters were taken"
+    return {k: float(vals[k + ".traffic_bytes_per_launch"]) for k in MBO_KERNELS
+            if k + ".traffic_bytes_per_launch" in vals}, "counters"
+
+
 def read_traffic(n_launch_bytes_alg: float):
     """HBM bytes per launch of the fused kernel from the committed counter summary, if
     it was taken on the current kernel source; else None."""
@@ -407,11 +443,15 @@ def bench_mbo(kr, I, torch, sp, d, args, mk):
     hvi_ms, unc_ms, sel_ms = (float(np.mean([q[i][0].elapsed_time(q[i][1]) for q in ph]))
                               for i in range(3))
 
+    traffic, tsrc = read_mbo_traffic()
+
     def roof(nbytes, ms, kernel):
         a = nbytes / (ms * 1e-3) / 1e9
+        name = kernel.split(" ")[0]
         return {"bound": "hbm", "achieved": round(a, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(a / HBM_PEAK_GBS, 4), "traffic": None, "kernel": kernel,
-                "kernel_ms": round(ms, 4), "algorithmic_bytes": nbytes}
+                "frac": round(a / HBM_PEAK_GBS, 4), "traffic": traffic.get(name),
+                "kernel": kernel, "kernel_ms": round(ms, 4), "algorithmic_bytes": nbytes,
+                "traffic_source": tsrc}
 
     M = I.MBO_MEMBERS
     res = {
