@@ -58,10 +58,11 @@ def _load():
         lib.oracle_uncertainty.argtypes = [i, ctypes.c_int64, dp, dp, dp]
         lib.oracle_select.argtypes = [i, lp, dp, dp, lp, lp, i, i, i, i, lp, ip]
         lib.oracle_hv_converged.argtypes = [i, dp, i, d]
+        lib.oracle_compare.argtypes = [ctypes.c_int64, dp, dp, ctypes.c_int64, dp, dp, dp]
         for fn in ("oracle_evaluate", "oracle_pareto", "oracle_compose", "oracle_staircase",
                    "oracle_extract", "oracle_microbatch", "oracle_microbatch_exact",
                    "oracle_hypervolume", "oracle_hvi", "oracle_uncertainty", "oracle_select",
-                   "oracle_hv_converged"):
+                   "oracle_hv_converged", "oracle_compare"):
             getattr(lib, fn).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -320,6 +321,21 @@ def hv_converged(hv_history, R: int = 2, eps: float = 1e-3) -> bool:
     lib = _load()
     h = _f64(hv_history)
     return bool(lib.oracle_hv_converged(h.shape[0], _p(h, ctypes.c_double), R, float(eps)))
+
+
+def compare(TA, EA, TB, EB) -> np.ndarray:
+    """Frontier metrics of B against baseline A (Section 6.1): float64[10] =
+    (leftmost time red. %, leftmost energy red. %, iso-time energy red. %,
+     iso-energy time red. %, d, E_A(d), E_B(d), b, T_A(b), T_B(b))."""
+    lib = _load()
+    TA, EA, TB, EB = _f64(TA), _f64(EA), _f64(TB), _f64(EB)
+    out = np.empty(10)
+    rc = lib.oracle_compare(TA.shape[0], _p(TA, ctypes.c_double), _p(EA, ctypes.c_double),
+                            TB.shape[0], _p(TB, ctypes.c_double), _p(EB, ctypes.c_double),
+                            _p(out, ctypes.c_double))
+    if rc != 0:
+        raise OracleError("oracle_compare failed: %d" % rc)
+    return out
 
 
 def decode(space, idx: int):

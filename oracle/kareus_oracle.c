@@ -32,6 +32,8 @@
  *   oracle_hv_converged  the scores, candidate selection and stopping rule of the
  *                     multi-pass Bayesian optimisation (Section 4.3, Algorithm 1,
  *                     Appendix C).
+ *   oracle_compare    the evaluation's frontier metrics: max-throughput, iso-time
+ *                     energy and iso-energy time reductions (Section 6.1).
  *
  * Every floating-point line is one IEEE fp64 rounding in the written order; the file
  * must be compiled without FMA contraction and without fast-math.
@@ -946,4 +948,56 @@ int oracle_hv_converged(int n, const double *hv, int R, double eps)
         s = s + (hv[b] - hv[b - 1]) / hv[b - 1];
     }
     return s / R < eps;
+}
+
+/* ------------------------------------------------------------------------------
+ * Frontier comparison metrics of the evaluation (Section 6.1, "Metrics"): baseline
+ * point set A against point set B, all in percent of the baseline's value.
+ *   out[0], out[1]  max-throughput comparison: time and energy reduction of B's
+ *                   leftmost point against A's (leftmost = least time, ties to the
+ *                   least energy)
+ *   out[2]          iso-time energy reduction: deadline d = A's least time;
+ *                   E_X(d) = least energy among X's points with time <= d
+ *   out[3]          iso-energy time reduction: budget b = A's least energy;
+ *                   T_X(b) = least time among X's points with energy <= b
+ *   out[4..6]       d, E_A(d), E_B(d);   out[7..9]  b, T_A(b), T_B(b)
+ * A reduction is (base - x) / base * 100; NaN when B has no point within the deadline
+ * or budget.  A and B need at least one point each.
+ * ---------------------------------------------------------------------------- */
+int oracle_compare(int64_t nA, const double *TA, const double *EA, int64_t nB,
+                   const double *TB, const double *EB, double *out)
+{
+    if (nA < 1 || nB < 1) return OR_EINVAL;
+    int64_t la = 0, lb = 0;
+    for (int64_t i = 1; i < nA; i++)
+        if (TA[i] < TA[la] || (TA[i] == TA[la] && EA[i] < EA[la])) la = i;
+    for (int64_t i = 1; i < nB; i++)
+        if (TB[i] < TB[lb] || (TB[i] == TB[lb] && EB[i] < EB[lb])) lb = i;
+    out[0] = (TA[la] - TB[lb]) / TA[la] * 100.0;
+    out[1] = (EA[la] - EB[lb]) / EA[la] * 100.0;
+    double d = TA[la];
+    double ea = INFINITY, eb = INFINITY;
+    for (int64_t i = 0; i < nA; i++)
+        if (TA[i] <= d && EA[i] < ea) ea = EA[i];
+    for (int64_t i = 0; i < nB; i++)
+        if (TB[i] <= d && EB[i] < eb) eb = EB[i];
+    if (eb == INFINITY) eb = NAN;
+    out[2] = (ea - eb) / ea * 100.0;
+    out[4] = d;
+    out[5] = ea;
+    out[6] = eb;
+    double b = EA[0];
+    for (int64_t i = 1; i < nA; i++)
+        if (EA[i] < b) b = EA[i];
+    double ta = INFINITY, tb = INFINITY;
+    for (int64_t i = 0; i < nA; i++)
+        if (EA[i] <= b && TA[i] < ta) ta = TA[i];
+    for (int64_t i = 0; i < nB; i++)
+        if (EB[i] <= b && TB[i] < tb) tb = TB[i];
+    if (tb == INFINITY) tb = NAN;
+    out[3] = (ta - tb) / ta * 100.0;
+    out[7] = b;
+    out[8] = ta;
+    out[9] = tb;
+    return OR_OK;
 }
