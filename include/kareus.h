@@ -362,6 +362,30 @@ kr_status kr_select_batch(int32_t n_seg, int64_t n_cand, const int64_t *cand_off
 int32_t kr_hv_converged(int32_t n, const double *hv_history, int32_t R, double eps);
 
 /*
+ * kr_compare_frontiers -- the evaluation's frontier metrics (Section 6.1, "Metrics") of
+ * point set B (a method's frontier) against point set A (the baseline's), in percent
+ * of the baseline's value, (base - x) / base * 100:
+ *   out[0], out[1]  max-throughput comparison: time and energy reduction of B's
+ *                   leftmost point against A's (leftmost = least time, ties to the
+ *                   least energy)
+ *   out[2]          iso-time energy reduction at the deadline d = A's least time, with
+ *                   E_X(d) = least energy among X's points of time <= d
+ *   out[3]          iso-energy time reduction at the budget b = A's least energy, with
+ *                   T_X(b) = least time among X's points of energy <= b
+ *   out[4..6]       d, E_A(d), E_B(d);   out[7..9]  b, T_A(b), T_B(b)
+ * A metric is NaN when B has no point within the deadline or budget.  The points may
+ * come in any order and include dominated ones.  Every value is exact (minima under
+ * predicates) and equals the oracle's bit for bit.
+ *   nA, nB            host >= 1
+ *   TA, EA / TB, EB   device [nA] / [nB]
+ *   out               device [10]
+ */
+size_t kr_compare_frontiers_workspace(void);
+kr_status kr_compare_frontiers(int64_t nA, const double *TA, const double *EA, int64_t nB,
+                               const double *TB, const double *EB, double *out, void *ws,
+                               size_t ws_bytes, void *stream);
+
+/*
  * kr_decode_candidates -- candidate index -> (frequency index, launch positions, SM
  * choices) under the index order above.
  *   idx [n] device; f_out [n]; pos_out [n][M]; sm_out [n][M] (device)

@@ -64,6 +64,8 @@ _SIGS = {
                                _vp, _vp, _vp, _sz, _vp]),
     "kr_select_batch_workspace": (_sz, [_i32, _i64]),
     "kr_hv_converged": (_i32, [_i32, _vp, _i32, _f64]),
+    "kr_compare_frontiers": (_i32, [_i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "kr_compare_frontiers_workspace": (_sz, []),
     "kr_status_string": (ctypes.c_char_p, [_i32]),
     "kr_set_phase_events": (_i32, [_i32, _vp, _vp]),
 }
@@ -519,3 +521,21 @@ def hv_converged(hv_history, R: int = 2, eps: float = 1e-3) -> bool:
     """Stopping rule of Algorithm 1 (kr_hv_converged, host)."""
     h = np.ascontiguousarray(np.asarray(hv_history, dtype=np.float64))
     return bool(_lib.kr_hv_converged(h.shape[0], h.ctypes.data_as(ctypes.c_void_p), R, float(eps)))
+
+
+def compare_frontiers(TA, EA, TB, EB, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Frontier metrics of B against baseline A (kr_compare_frontiers): float64[10] on the
+    device (leftmost time and energy reduction %, iso-time energy reduction %, iso-energy
+    time reduction %, d, E_A(d), E_B(d), b, T_A(b), T_B(b))."""
+    TA = _dev(TA, torch.float64, "TA").reshape(-1)
+    EA = _dev(EA, torch.float64, "EA").reshape(-1)
+    TB = _dev(TB, torch.float64, "TB").reshape(-1)
+    EB = _dev(EB, torch.float64, "EB").reshape(-1)
+    if out is None:
+        out = torch.empty(10, dtype=torch.float64, device="cuda")
+    wsb = _lib.kr_compare_frontiers_workspace()
+    ws = _workspace(wsb)
+    _check("kr_compare_frontiers",
+           _lib.kr_compare_frontiers(TA.numel(), _ptr(TA), _ptr(EA), TB.numel(), _ptr(TB),
+                                     _ptr(EB), _ptr(out), _ptr(ws), wsb, _stream()))
+    return out

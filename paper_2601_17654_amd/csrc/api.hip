@@ -743,6 +743,36 @@ kr_status kr_select_batch(int32_t n_seg, int64_t n_cand, const int64_t *cand_off
                : KR_EHIP;
 }
 
+size_t kr_compare_frontiers_workspace(void)
+{
+    Carve c(nullptr);
+    c.take<double>(3 * KR_CMP_BLOCKS);
+    c.take<double>(5 * KR_CMP_BLOCKS);
+    return c.used;
+}
+
+kr_status kr_compare_frontiers(int64_t nA, const double *TA, const double *EA, int64_t nB,
+                               const double *TB, const double *EB, double *out, void *ws,
+                               size_t ws_bytes, void *stream)
+{
+    if (nA < 1 || nB < 1 || !TA || !EA || !TB || !EB || !out || !ws) return KR_EINVAL;
+    if (ws_bytes < kr_compare_frontiers_workspace()) return KR_ECAPACITY;
+    Carve c(ws);
+    CmpArgs a;
+    a.nA = nA;
+    a.nB = nB;
+    a.TA = TA;
+    a.EA = EA;
+    a.TB = TB;
+    a.EB = EB;
+    const int64_t need = (std::max(nA, nB) + KR_BLOCK * 4 - 1) / (KR_BLOCK * 4);
+    a.blocks = (int)std::min<int64_t>(KR_CMP_BLOCKS, std::max<int64_t>(1, need));
+    a.part = c.take<double>(3 * KR_CMP_BLOCKS);
+    a.part2 = c.take<double>(5 * KR_CMP_BLOCKS);
+    a.out = out;
+    return launch_compare(a, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
+}
+
 int32_t kr_hv_converged(int32_t n, const double *hv_history, int32_t R, double eps)
 {
     if (R < 1 || !hv_history || n - 1 < R) return 0;

@@ -194,4 +194,15 @@ struct SelArgs {
 };
 hipError_t launch_select(const SelArgs &a, hipEvent_t *ev, hipStream_t st);
 
+// metrics.hip: frontier comparison metrics (Section 6.1).
+#define KR_CMP_BLOCKS 512  // blocks of the two reduction passes at most
+struct CmpArgs {
+    int64_t nA, nB;
+    const double *TA, *EA, *TB, *EB;
+    int blocks;
+    double *part, *part2;  // [blocks][3], [blocks][5]
+    double *out;           // [10]
+};
+hipError_t launch_compare(const CmpArgs &a, hipStream_t st);
+
 }  // namespace kr

@@ -32,7 +32,7 @@ __device__ __forceinline__ double energy_variant(int v, double t, double e, doub
     return ps * t;
 }
 
-struct MaxF64 {
+struct HvMaxF64 {
     __device__ __forceinline__ double operator()(double a, double b) const { return b > a ? b : a; }
 };
 struct SumI32x {
@@ -67,7 +67,7 @@ __global__ void __launch_bounds__(KR_BLOCK) hvi_prep_kernel(HviArgs a)
         sE[i] = a.E_obs[o0 + i];
         mt = sT[i] > mt ? sT[i] : mt;
     }
-    const double rT = 1.1 * block_reduce(mt, (double)-INFINITY, MaxF64(), red);
+    const double rT = 1.1 * block_reduce(mt, (double)-INFINITY, HvMaxF64(), red);
     if (tid == 0) a.ref[g * 4] = rT;
     for (int v = 0; v < 3; ++v) {
         double me = -INFINITY;
@@ -75,7 +75,7 @@ __global__ void __launch_bounds__(KR_BLOCK) hvi_prep_kernel(HviArgs a)
             sV[i] = energy_variant(v, sT[i], sE[i], a.p_static);
             me = sV[i] > me ? sV[i] : me;
         }
-        const double rE = 1.1 * block_reduce(me, (double)-INFINITY, MaxF64(), red);
+        const double rE = 1.1 * block_reduce(me, (double)-INFINITY, HvMaxF64(), red);
         // a point opens a staircase step iff it is inside the box and no point inside the
         // box is at least as good in both and earlier in (T, energy, index) order
         int32_t mine = 0;

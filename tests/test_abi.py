@@ -85,6 +85,8 @@ def test_host_validation_without_gpu():
         assert L.kr_select_batch(1, 10, one, one, one, one, one, *ks, one, one, one, one, big,
                                  null) == b.KR_EINVAL
     assert L.kr_uncertainty(0, 10, one, one, one, null) == b.KR_EINVAL
+    assert L.kr_compare_frontiers(0, one, one, 1, one, one, one, one, big, null) == b.KR_EINVAL
+    assert L.kr_compare_frontiers(1, one, one, 1, one, one, one, one, 8, null) == b.KR_ECAPACITY
     assert L.kr_uncertainty(65, 10, one, one, one, null) == b.KR_EINVAL
 
 
