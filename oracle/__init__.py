@@ -59,10 +59,11 @@ def _load():
         lib.oracle_select.argtypes = [i, lp, dp, dp, lp, lp, i, i, i, i, lp, ip]
         lib.oracle_hv_converged.argtypes = [i, dp, i, d]
         lib.oracle_compare.argtypes = [ctypes.c_int64, dp, dp, ctypes.c_int64, dp, dp, dp]
+        lib.oracle_launch_dp.argtypes = [i, i, ip, dp, d, i, ctypes.c_int64, dp, dp, ip, lp, lp]
         for fn in ("oracle_evaluate", "oracle_pareto", "oracle_compose", "oracle_staircase",
                    "oracle_extract", "oracle_microbatch", "oracle_microbatch_exact",
                    "oracle_hypervolume", "oracle_hvi", "oracle_uncertainty", "oracle_select",
-                   "oracle_hv_converged", "oracle_compare"):
+                   "oracle_hv_converged", "oracle_compare", "oracle_launch_dp"):
             getattr(lib, fn).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -336,6 +337,29 @@ def compare(TA, EA, TB, EB) -> np.ndarray:
     if rc != 0:
         raise OracleError("oracle_compare failed: %d" % rc)
     return out
+
+
+def launch_dp(kind1, kind2, ops, p_static: float, kmax: int):
+    """Launch-timing frontier of two operation sequences (Appendix B).  kind1 [I],
+    kind2 [J]: 0 computation, 1 communication; ops [I + J][4] (S1's ops, then S2's).
+    Returns (T, E, schedules int32[n][I + J], max_cell)."""
+    lib = _load()
+    kind = np.ascontiguousarray(np.concatenate([np.asarray(kind1), np.asarray(kind2)]),
+                                dtype=np.int32)
+    I, J = len(kind1), len(kind2)
+    ops = _f64(ops).reshape(I + J, 4)
+    cap = 4096
+    oT, oE = np.empty(cap), np.empty(cap)
+    sched = np.empty((cap, I + J), dtype=np.int32)
+    n, mc = ctypes.c_int64(0), ctypes.c_int64(0)
+    rc = lib.oracle_launch_dp(I, J, _p(kind, ctypes.c_int32), _p(ops, ctypes.c_double),
+                              float(p_static), kmax, cap, _p(oT, ctypes.c_double),
+                              _p(oE, ctypes.c_double), _p(sched, ctypes.c_int32),
+                              ctypes.byref(n), ctypes.byref(mc))
+    if rc != 0:
+        raise OracleError("oracle_launch_dp failed: %d" % rc)
+    k = min(n.value, cap)
+    return oT[:k].copy(), oE[:k].copy(), sched[:k].copy(), mc.value
 
 
 def decode(space, idx: int):

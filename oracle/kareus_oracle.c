@@ -34,6 +34,8 @@
  *                     Appendix C).
  *   oracle_compare    the evaluation's frontier metrics: max-throughput, iso-time
  *                     energy and iso-energy time reductions (Section 6.1).
+ *   oracle_launch_dp  the launch-timing frontier of two operation sequences by the
+ *                     dynamic program of Appendix B.
  *
  * Every floating-point line is one IEEE fp64 rounding in the written order; the file
  * must be compiled without FMA contraction and without fast-math.
@@ -1000,4 +1002,202 @@ int oracle_compare(int64_t nA, const double *TA, const double *EA, int64_t nB,
     out[8] = ta;
     out[9] = tb;
     return OR_OK;
+}
+
+/* ------------------------------------------------------------------------------
+ * Launch-timing frontier of two operation sequences (Appendix B's dynamic program).
+ *
+ * S1 = ops[0 .. I-1] and S2 = ops[I .. I+J-1] run in their own order; ops of different
+ * sequences are independent.  kind[o] = 0 for a computation, 1 for a communication (a
+ * run of consecutive collectives counts as one).  Per op, ops[o*4 + 0..3]:
+ *   computation: time and dynamic power alone (all SMs), time and dynamic power while
+ *                a communication holds its SMs;
+ *   communication: time and dynamic power (with its SM allocation), unused, unused.
+ * A schedule is a sequence of groups, each one of
+ *   case 0: the next op of S1 alone;  case 1: the next op of S2 alone;
+ *   case 2: the next op of S1, a communication, overlapped with the next k (1 .. Kmax)
+ *           ops of S2, all computations;
+ *   case 3: the same with the roles of S1 and S2 swapped.
+ * Groups run one after another; a schedule's time and energy are the sums over its
+ * groups.  P(i, j), the frontier of the suffixes from S1[i] and S2[j], is GetFrontier of
+ * (group cost + point of the successor cell) over every case, with P(I, J) = {(0, 0)}.
+ *
+ * Readings (the appendix leaves these open): overlap only pairs a communication with
+ * computations; within an overlapped group both start together, the computations run
+ * in order in the shared state until the communication ends and alone after it (the
+ * fluid progress of the partition cost model), and the group ends when both are done;
+ * every group's energy is its dynamic energy plus static power times its time.
+ *
+ * Floating-point order: group time/energy as written in group_cost; a candidate is
+ * (g.T + p.T, g.E + p.E).  Candidates are generated by case (0, 1, 2 by k, 3 by k) and,
+ * within one, by the successor's points in ascending time; GetFrontier keeps the first
+ * of exact duplicates.  Output: P(0, 0) in ascending time with each point's schedule
+ * as codes case * 32 + k (k = 0 for a lone op), padded with -1 to I + J entries;
+ * *max_cell = the largest frontier of any cell.
+ * ---------------------------------------------------------------------------- */
+typedef struct { double T, E; int32_t src, q; } dp_pt;
+
+typedef struct {
+    int ncase, k, ni, nj;  /* decision and successor cell */
+    double T, E;
+} dp_src;
+
+static void group_cost(const double *ops, int comm, const int *run, int k, double ps, double *T,
+                       double *E)
+{
+    const double *c = ops + 4 * comm;
+    double tc = c[0], pc = c[1];
+    double tau = 0.0, e = 0.0;
+    for (int r = 0; r < k; r++) {
+        const double *o = ops + 4 * run[r];
+        double t0 = o[0], p0 = o[1], t1 = o[2], p1 = o[3];
+        if (tau < tc) {
+            double nt = tau + t1;
+            if (nt <= tc) {
+                e = e + t1 * p1;
+                tau = nt;
+            } else {
+                double dt = tc - tau;
+                double rem = 1.0 - dt / t1;
+                double ta = rem * t0;
+                e = e + dt * p1;
+                e = e + ta * p0;
+                tau = tc + ta;
+            }
+        } else {
+            e = e + t0 * p0;
+            tau = tau + t0;
+        }
+    }
+    double t = tau > tc ? tau : tc;
+    *T = t;
+    *E = (e + tc * pc) + ps * t;
+}
+
+static void alone_cost(const double *ops, int o, double ps, double *T, double *E)
+{
+    double t = ops[4 * o], p = ops[4 * o + 1];
+    *T = t;
+    *E = t * p + ps * t;
+}
+
+static int cmp_dp(const void *a, const void *b)
+{
+    const dp_pt *x = (const dp_pt *)a, *y = (const dp_pt *)b;
+    if (x->T < y->T) return -1;
+    if (x->T > y->T) return 1;
+    if (x->E < y->E) return -1;
+    if (x->E > y->E) return 1;
+    /* candidate order: src then q (the order they were generated in) */
+    if (x->src != y->src) return x->src < y->src ? -1 : 1;
+    return (x->q > y->q) - (x->q < y->q);
+}
+
+int oracle_launch_dp(int I, int J, const int32_t *kind, const double *ops, double ps, int Kmax,
+                     int64_t cap, double *oT, double *oE, int32_t *osched, int64_t *n_out,
+                     int64_t *max_cell)
+{
+    if (I < 0 || J < 0 || I + J < 1 || Kmax < 0 || cap < 0) return OR_EINVAL;
+    int W = J + 1;
+    int ncell = (I + 1) * (J + 1);
+    dp_pt **cell = (dp_pt **)calloc((size_t)ncell, sizeof(dp_pt *));
+    int *cnt = (int *)calloc((size_t)ncell, sizeof(int));
+    dp_src **srcs = (dp_src **)calloc((size_t)ncell, sizeof(dp_src *));
+    int *run = (int *)malloc(sizeof(int) * (size_t)(I + J + 1));
+    int rc = OR_OK;
+    if (!cell || !cnt || !srcs || !run) { rc = OR_EINVAL; goto done; }
+    *max_cell = 1;
+    cell[I * W + J] = (dp_pt *)malloc(sizeof(dp_pt));
+    cell[I * W + J][0].T = 0.0;
+    cell[I * W + J][0].E = 0.0;
+    cell[I * W + J][0].src = -1;
+    cell[I * W + J][0].q = -1;
+    cnt[I * W + J] = 1;
+    for (int i = I; i >= 0; i--) {
+        for (int j = J; j >= 0; j--) {
+            if (i == I && j == J) continue;
+            dp_src *s = (dp_src *)malloc(sizeof(dp_src) * (size_t)(2 + 2 * (Kmax + 1)));
+            int ns = 0;
+            if (i < I) {
+                s[ns].ncase = 0; s[ns].k = 0; s[ns].ni = i + 1; s[ns].nj = j;
+                alone_cost(ops, i, ps, &s[ns].T, &s[ns].E);
+                ns++;
+            }
+            if (j < J) {
+                s[ns].ncase = 1; s[ns].k = 0; s[ns].ni = i; s[ns].nj = j + 1;
+                alone_cost(ops, I + j, ps, &s[ns].T, &s[ns].E);
+                ns++;
+            }
+            if (i < I && kind[i] == 1) {
+                for (int k = 1; k <= Kmax && j + k <= J; k++) {
+                    if (kind[I + j + k - 1] != 0) break;
+                    for (int r = 0; r < k; r++) run[r] = I + j + r;
+                    s[ns].ncase = 2; s[ns].k = k; s[ns].ni = i + 1; s[ns].nj = j + k;
+                    group_cost(ops, i, run, k, ps, &s[ns].T, &s[ns].E);
+                    ns++;
+                }
+            }
+            if (j < J && kind[I + j] == 1) {
+                for (int k = 1; k <= Kmax && i + k <= I; k++) {
+                    if (kind[i + k - 1] != 0) break;
+                    for (int r = 0; r < k; r++) run[r] = i + r;
+                    s[ns].ncase = 3; s[ns].k = k; s[ns].ni = i + k; s[ns].nj = j + 1;
+                    group_cost(ops, I + j, run, k, ps, &s[ns].T, &s[ns].E);
+                    ns++;
+                }
+            }
+            int nc = 0;
+            for (int a = 0; a < ns; a++) nc += cnt[s[a].ni * W + s[a].nj];
+            dp_pt *cand = (dp_pt *)malloc(sizeof(dp_pt) * (size_t)(nc > 0 ? nc : 1));
+            int w = 0;
+            for (int a = 0; a < ns; a++) {
+                const dp_pt *succ = cell[s[a].ni * W + s[a].nj];
+                for (int q = 0; q < cnt[s[a].ni * W + s[a].nj]; q++) {
+                    cand[w].T = s[a].T + succ[q].T;
+                    cand[w].E = s[a].E + succ[q].E;
+                    cand[w].src = a;
+                    cand[w].q = q;
+                    w++;
+                }
+            }
+            qsort(cand, (size_t)nc, sizeof(dp_pt), cmp_dp);
+            double best = INFINITY;
+            int kept = 0;
+            for (int c = 0; c < nc; c++)
+                if (cand[c].E < best) {
+                    best = cand[c].E;
+                    cand[kept++] = cand[c];
+                }
+            cell[i * W + j] = cand;
+            cnt[i * W + j] = kept;
+            srcs[i * W + j] = s;
+            if (kept > *max_cell) *max_cell = kept;
+        }
+    }
+    *n_out = cnt[0];
+    for (int q = 0; q < cnt[0] && q < cap; q++) {
+        oT[q] = cell[0][q].T;
+        oE[q] = cell[0][q].E;
+        int32_t *sc = osched + (int64_t)q * (I + J);
+        for (int d = 0; d < I + J; d++) sc[d] = -1;
+        int ci = 0, cj = 0, cq = q, d = 0;
+        while (!(ci == I && cj == J)) {
+            const dp_pt *p = &cell[ci * W + cj][cq];
+            const dp_src *a = &srcs[ci * W + cj][p->src];
+            sc[d++] = a->ncase * 32 + a->k;
+            ci = a->ni;
+            cj = a->nj;
+            cq = p->q;
+        }
+    }
+done:
+    if (cell)
+        for (int c = 0; c < ncell; c++) free(cell[c]);
+    if (srcs)
+        for (int c = 0; c < ncell; c++) free(srcs[c]);
+    free(cell);
+    free(cnt);
+    free(srcs);
+    free(run);
+    return rc;
 }
