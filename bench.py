@@ -149,7 +149,7 @@ def main():
     ap.add_argument("--skip-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true")
-    ap.add_argument("--part", choices=["all", "eval", "compose", "mbo"], default="all",
+    ap.add_argument("--part", choices=["all", "eval", "compose", "mbo", "dp"], default="all",
                     help="profiling aid: run only one half of the step (prints no bench line)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -184,6 +184,10 @@ def main():
     comp = kr.compose_frontiers(off4_d, T4_d, E4_d, B)
     torch.cuda.synchronize()
 
+    if args.part == "dp":
+        res, _ = bench_dp(kr, I, torch, args, mk_events)
+        log("dp: " + json.dumps(res))
+        return
     if args.part == "mbo":
         res, _ = bench_mbo(kr, I, torch, sp, d, args, mk_events)
         log("mbo: " + json.dumps(res))
@@ -345,6 +349,8 @@ def main():
         "iso_time_energy_reduction_pct": float(cm[2]),
         "iso_energy_time_reduction_pct": float(cm[3])}
 
+    out["launch_timing"], dp_ctx = bench_dp(kr, I, torch, args, mk)
+
     if not args.skip_cpu:
         import oracle
 
@@ -412,7 +418,64 @@ def main():
             "value": 2 * len(oT) / el, "unit": "points/s", "cores": 1, "kind": "oracle",
             "sample": "the same comparison, %.4f s" % el,
             "parity": bool(np.array_equal(rc, cm, equal_nan=True))}
+        out["launch_timing"]["cpu_baseline"] = dp_cpu_baseline(oracle, dp_ctx, args.cpu_seconds)
     print(json.dumps(out))
+
+
+def bench_dp(kr, I, torch, args, mk):
+    """Launch-timing frontiers (Appendix B's dynamic program) of two nanobatches of a
+    transformer block for every (partition, frequency, SM choice) of the two-comm tables."""
+    w2 = I.config_workload(2)
+    sp2 = w2.space
+    k1, k2, ops, idx = I.dp_instances(w2, range(sp2.n_parts))
+    ops_d = torch.from_numpy(ops).cuda()
+    res = kr.launch_timing_frontier(k1, k2, ops_d, sp2.p_static, I.DP_KMAX)
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        kr.launch_timing_frontier(k1, k2, ops_d, sp2.p_static, I.DP_KMAX, check=False, out=res)
+    torch.cuda.synchronize()
+    ev = mk(2 * args.steps)
+    for k in range(args.steps):
+        ev[2 * k].record()
+        kr.launch_timing_frontier(k1, k2, ops_d, sp2.p_static, I.DP_KMAX, check=False, out=res)
+        ev[2 * k + 1].record()
+    torch.cuda.synchronize()
+    assert int(res.status.item()) == 0
+    ms = float(np.mean([ev[2 * k].elapsed_time(ev[2 * k + 1]) for k in range(args.steps)]))
+    n = ops.shape[0]
+    cells = n * ((len(k1) + 1) * (len(k2) + 1) - 1)
+    sizes = res.n.cpu().numpy()
+    out = {
+        "workload": "launch-timing-two-comm: two nanobatches of a transformer block (4 "
+                    "computations, a collective, 5 computations, a collective) per "
+                    "(partition, frequency, SM choice) of the two-comm tables, overlap runs "
+                    "up to %d" % I.DP_KMAX,
+        "instances": n, "cells": cells, "call_ms": round(ms, 4),
+        "instances_per_s": n / (ms * 1e-3), "cells_per_s": cells / (ms * 1e-3),
+        "frontier_points_mean": float(sizes.mean()), "frontier_points_max": int(sizes.max())}
+    return out, dict(k1=k1, k2=k2, ops=ops, res=res, ps=sp2.p_static)
+
+
+def dp_cpu_baseline(oracle, ctx, seconds):
+    """The oracle's dynamic program on the first instances of the same batch for about
+    `seconds`, checked bit for bit against the GPU's frontiers."""
+    import torch  # noqa: F401
+
+    res = ctx["res"]
+    gT, gE, gn = res.T.cpu().numpy(), res.E.cpu().numpy(), res.n.cpu().numpy()
+    gS = res.sched.cpu().numpy()
+    t0 = time.perf_counter()
+    n, mism = 0, 0
+    while n < len(ctx["ops"]) and time.perf_counter() - t0 < seconds:
+        T, E, S, _ = oracle.launch_dp(ctx["k1"], ctx["k2"], ctx["ops"][n], ctx["ps"], 9)
+        m = len(T)
+        mism += int(not (gn[n] == m and np.array_equal(gT[n, :m], T) and
+                         np.array_equal(gE[n, :m], E) and np.array_equal(gS[n, :m], S)))
+        n += 1
+    el = time.perf_counter() - t0
+    return {"value": n / el, "unit": "instances/s", "cores": 1, "kind": "oracle",
+            "sample": "first %d of the instances, single-threaded C oracle, %.1f s" % (n, el),
+            "mismatches": mism}
 
 
 def mbo_inputs(kr, I, torch, sp, d, seed=11):

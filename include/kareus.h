@@ -386,6 +386,52 @@ kr_status kr_compare_frontiers(int64_t nA, const double *TA, const double *EA, i
                                size_t ws_bytes, void *stream);
 
 /*
+ * kr_launch_timing_frontier -- the launch-timing frontier of two operation sequences by
+ * the dynamic program of Appendix B, for a batch of instances that share the sequences'
+ * structure (one instance per frequency and SM allocation, say).
+ *
+ * S1 = ops 0 .. I-1 and S2 = ops I .. I+J-1 each run in order; ops of different
+ * sequences are independent.  kind[o] = 0 for a computation, 1 for a communication (a
+ * run of consecutive collectives counts as one).  A schedule is a sequence of groups:
+ * the next op of S1 alone (code 0), the next op of S2 alone (code 32), S1's next op, a
+ * communication, overlapped with S2's next k computations (code 64 + k), or S2's next
+ * communication overlapped with S1's next k computations (code 96 + k), k = 1 .. kmax.
+ * Groups run one after another.  In an overlapped group both sides start together, the
+ * computations run in order with the shared-state time and power until the
+ * communication ends and with the alone time and power after it (the partition cost
+ * model's fluid progress), and the group ends when both are done.  A group's energy is
+ * its dynamic energy plus p_static times its time; a schedule sums its groups.
+ * P(i, j) = GetFrontier over the four cases of (group + P(successor)), P(I, J) =
+ * {(0, 0)}; exact duplicates keep the first candidate in the order (case, k, the
+ * successor's point in ascending time).  Bit-exact with the oracle.
+ *   n_inst          host >= 0 instances
+ *   I, J            host 0 .. KR_DP_MAX_OPS, I + J >= 1
+ *   kind            host [I + J]
+ *   ops             device [n_inst][I + J][4]: computation (time alone, power alone,
+ *                   time shared, power shared); communication (time, power, -, -)
+ *   kmax            host 0 .. KR_DP_MAX_K
+ *   out_cap         host 1 .. 64: points kept per instance
+ *   out_T, out_E    device [n_inst][out_cap]: P(0, 0) in ascending time
+ *   out_sched       device [n_inst][out_cap][I + J] decision codes padded with -1, or
+ *                   NULL
+ *   out_n           device [n_inst]: frontier size (may exceed out_cap), or -1 when the
+ *                   instance exceeded an on-chip limit (a cell frontier above
+ *                   KR_DP_CELL_CAP points, more than KR_DP_CAND candidates in a cell, or
+ *                   more than KR_DP_ARENA points over all cells)
+ *   status_out      device [1]: KR_OK, or KR_ECAPACITY if any instance hit a limit
+ */
+#define KR_DP_MAX_OPS 24
+#define KR_DP_MAX_K 16
+#define KR_DP_CELL_CAP 64
+#define KR_DP_CAND 512
+#define KR_DP_ARENA 1024
+kr_status kr_launch_timing_frontier(int64_t n_inst, int32_t I, int32_t J, const int32_t *kind,
+                                    const double *ops, double p_static, int32_t kmax,
+                                    int32_t out_cap, double *out_T, double *out_E,
+                                    int32_t *out_sched, int32_t *out_n, int32_t *status_out,
+                                    void *stream);
+
+/*
  * kr_decode_candidates -- candidate index -> (frequency index, launch positions, SM
  * choices) under the index order above.
  *   idx [n] device; f_out [n]; pos_out [n][M]; sm_out [n][M] (device)

@@ -342,7 +342,8 @@ def compare(TA, EA, TB, EB) -> np.ndarray:
 def launch_dp(kind1, kind2, ops, p_static: float, kmax: int):
     """Launch-timing frontier of two operation sequences (Appendix B).  kind1 [I],
     kind2 [J]: 0 computation, 1 communication; ops [I + J][4] (S1's ops, then S2's).
-    Returns (T, E, schedules int32[n][I + J], max_cell)."""
+    Returns (T, E, schedules int32[n][I + J], stats) with stats = (largest cell
+    frontier, frontier points of all cells, most candidates of a cell)."""
     lib = _load()
     kind = np.ascontiguousarray(np.concatenate([np.asarray(kind1), np.asarray(kind2)]),
                                 dtype=np.int32)
@@ -351,15 +352,16 @@ def launch_dp(kind1, kind2, ops, p_static: float, kmax: int):
     cap = 4096
     oT, oE = np.empty(cap), np.empty(cap)
     sched = np.empty((cap, I + J), dtype=np.int32)
-    n, mc = ctypes.c_int64(0), ctypes.c_int64(0)
+    n = ctypes.c_int64(0)
+    st = np.zeros(3, dtype=np.int64)
     rc = lib.oracle_launch_dp(I, J, _p(kind, ctypes.c_int32), _p(ops, ctypes.c_double),
                               float(p_static), kmax, cap, _p(oT, ctypes.c_double),
                               _p(oE, ctypes.c_double), _p(sched, ctypes.c_int32),
-                              ctypes.byref(n), ctypes.byref(mc))
+                              ctypes.byref(n), _p(st, ctypes.c_int64))
     if rc != 0:
         raise OracleError("oracle_launch_dp failed: %d" % rc)
     k = min(n.value, cap)
-    return oT[:k].copy(), oE[:k].copy(), sched[:k].copy(), mc.value
+    return oT[:k].copy(), oE[:k].copy(), sched[:k].copy(), tuple(int(x) for x in st)
 
 
 def decode(space, idx: int):

@@ -1033,7 +1033,8 @@ int oracle_compare(int64_t nA, const double *TA, const double *EA, int64_t nB,
  * within one, by the successor's points in ascending time; GetFrontier keeps the first
  * of exact duplicates.  Output: P(0, 0) in ascending time with each point's schedule
  * as codes case * 32 + k (k = 0 for a lone op), padded with -1 to I + J entries;
- * *max_cell = the largest frontier of any cell.
+ * stats[0] = the largest frontier of any cell, stats[1] = the frontier points of all
+ * cells together, stats[2] = the most candidates of any cell.
  * ---------------------------------------------------------------------------- */
 typedef struct { double T, E; int32_t src, q; } dp_pt;
 
@@ -1095,7 +1096,7 @@ static int cmp_dp(const void *a, const void *b)
 
 int oracle_launch_dp(int I, int J, const int32_t *kind, const double *ops, double ps, int Kmax,
                      int64_t cap, double *oT, double *oE, int32_t *osched, int64_t *n_out,
-                     int64_t *max_cell)
+                     int64_t *stats)
 {
     if (I < 0 || J < 0 || I + J < 1 || Kmax < 0 || cap < 0) return OR_EINVAL;
     int W = J + 1;
@@ -1106,7 +1107,9 @@ int oracle_launch_dp(int I, int J, const int32_t *kind, const double *ops, doubl
     int *run = (int *)malloc(sizeof(int) * (size_t)(I + J + 1));
     int rc = OR_OK;
     if (!cell || !cnt || !srcs || !run) { rc = OR_EINVAL; goto done; }
-    *max_cell = 1;
+    stats[0] = 1;
+    stats[1] = 1;
+    stats[2] = 0;
     cell[I * W + J] = (dp_pt *)malloc(sizeof(dp_pt));
     cell[I * W + J][0].T = 0.0;
     cell[I * W + J][0].E = 0.0;
@@ -1171,7 +1174,9 @@ int oracle_launch_dp(int I, int J, const int32_t *kind, const double *ops, doubl
             cell[i * W + j] = cand;
             cnt[i * W + j] = kept;
             srcs[i * W + j] = s;
-            if (kept > *max_cell) *max_cell = kept;
+            if (kept > stats[0]) stats[0] = kept;
+            stats[1] += kept;
+            if (nc > stats[2]) stats[2] = nc;
         }
     }
     *n_out = cnt[0];

@@ -66,6 +66,8 @@ _SIGS = {
     "kr_hv_converged": (_i32, [_i32, _vp, _i32, _f64]),
     "kr_compare_frontiers": (_i32, [_i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _sz, _vp]),
     "kr_compare_frontiers_workspace": (_sz, []),
+    "kr_launch_timing_frontier": (_i32, [_i64, _i32, _i32, _vp, _vp, _f64, _i32, _i32, _vp, _vp,
+                                         _vp, _vp, _vp, _vp]),
     "kr_status_string": (ctypes.c_char_p, [_i32]),
     "kr_set_phase_events": (_i32, [_i32, _vp, _vp]),
 }
@@ -538,4 +540,40 @@ def compare_frontiers(TA, EA, TB, EB, out: Optional[torch.Tensor] = None) -> tor
     _check("kr_compare_frontiers",
            _lib.kr_compare_frontiers(TA.numel(), _ptr(TA), _ptr(EA), TB.numel(), _ptr(TB),
                                      _ptr(EB), _ptr(out), _ptr(ws), wsb, _stream()))
+    return out
+
+
+@dataclasses.dataclass
+class LaunchFrontier:
+    T: torch.Tensor       # [n_inst][out_cap]
+    E: torch.Tensor
+    sched: Optional[torch.Tensor]  # [n_inst][out_cap][I + J] decision codes, -1 padded
+    n: torch.Tensor       # [n_inst] frontier sizes (-1: an on-chip limit was hit)
+    status: torch.Tensor  # [1]
+
+
+def launch_timing_frontier(kind1, kind2, ops, p_static: float, kmax: int, out_cap: int = 64,
+                           sched: bool = True, check: bool = True,
+                           out: Optional[LaunchFrontier] = None) -> LaunchFrontier:
+    """Launch-timing frontier of two operation sequences (kr_launch_timing_frontier).
+    kind1 [I], kind2 [J]: 0 computation, 1 communication; ops [n_inst][I + J][4]."""
+    kind = np.ascontiguousarray(np.concatenate([np.asarray(kind1), np.asarray(kind2)]),
+                                dtype=np.int32)
+    I, J = len(kind1), len(kind2)
+    ops = _dev(ops, torch.float64, "ops").reshape(-1, I + J, 4)
+    n = ops.shape[0]
+    if out is None:
+        out = LaunchFrontier(
+            torch.empty((n, out_cap), dtype=torch.float64, device="cuda"),
+            torch.empty((n, out_cap), dtype=torch.float64, device="cuda"),
+            torch.empty((n, out_cap, I + J), dtype=torch.int32, device="cuda") if sched else None,
+            torch.empty(max(n, 1), dtype=torch.int32, device="cuda"),
+            torch.empty(1, dtype=torch.int32, device="cuda"))
+    _check("kr_launch_timing_frontier",
+           _lib.kr_launch_timing_frontier(n, I, J, kind.ctypes.data_as(ctypes.c_void_p),
+                                          _ptr(ops), float(p_static), kmax, out_cap,
+                                          _ptr(out.T), _ptr(out.E), _ptr(out.sched),
+                                          _ptr(out.n), _ptr(out.status), _stream()))
+    if check and int(out.status.item()) != KR_OK:
+        raise KrError("kr_launch_timing_frontier", int(out.status.item()))
     return out

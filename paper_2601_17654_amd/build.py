@@ -16,7 +16,8 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libkareus_mi355x.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["api.hip", "eval.hip", "eval_wave.hip", "pareto.hip", "compose.hip", "microbatch.hip",
-           "mbo.hip", "metrics.hip"]
+           "mbo.hip", "metrics.hip",
+           "launch_dp.hip"]
 FLAGS = [
     "--offload-arch=gfx950",
     "-O3",

@@ -773,6 +773,41 @@ kr_status kr_compare_frontiers(int64_t nA, const double *TA, const double *EA, i
     return launch_compare(a, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
 }
 
+kr_status kr_launch_timing_frontier(int64_t n_inst, int32_t I, int32_t J, const int32_t *kind,
+                                    const double *ops, double p_static, int32_t kmax,
+                                    int32_t out_cap, double *out_T, double *out_E,
+                                    int32_t *out_sched, int32_t *out_n, int32_t *status_out,
+                                    void *stream)
+{
+    if (n_inst < 0 || n_inst > INT32_MAX || I < 0 || J < 0 || I > KR_DP_MAX_OPS ||
+        J > KR_DP_MAX_OPS || I + J < 1 || !kind || kmax < 0 || kmax > KR_DP_MAX_K ||
+        out_cap < 1 || out_cap > 64 || !status_out || !(p_static == p_static) ||
+        (n_inst > 0 && (!ops || !out_T || !out_E || !out_n)))
+        return KR_EINVAL;
+    DpArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.n_inst = n_inst;
+    a.I = I;
+    a.J = J;
+    a.kmax = kmax;
+    a.out_cap = out_cap;
+    for (int o = 0; o < I + J; ++o) {
+        if (kind[o] != 0 && kind[o] != 1) return KR_EINVAL;
+        a.kind[o] = (int8_t)kind[o];
+    }
+    for (int i = I - 1; i >= 0; --i) a.run1[i] = kind[i] == 0 ? (int8_t)(a.run1[i + 1] + 1) : 0;
+    for (int j = J - 1; j >= 0; --j)
+        a.run2[j] = kind[I + j] == 0 ? (int8_t)(a.run2[j + 1] + 1) : 0;
+    a.ops = ops;
+    a.p_static = p_static;
+    a.out_T = out_T;
+    a.out_E = out_E;
+    a.out_sched = out_sched;
+    a.out_n = out_n;
+    a.status = status_out;
+    return launch_dp(a, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
+}
+
 int32_t kr_hv_converged(int32_t n, const double *hv_history, int32_t R, double eps)
 {
     if (R < 1 || !hv_history || n - 1 < R) return 0;

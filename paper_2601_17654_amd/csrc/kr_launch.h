@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/kareus.h"
+
 #define KR_FIN_CAP 2560    // points the finalize kernel sorts in LDS
 #define KR_FIN_UNITS 2048  // units per segment the finalize kernel's LDS path takes
 #define KR_TILE 2048       // points per tile of the stand-alone filter
@@ -204,5 +206,20 @@ struct CmpArgs {
     double *out;           // [10]
 };
 hipError_t launch_compare(const CmpArgs &a, hipStream_t st);
+
+// launch_dp.hip: launch-timing frontier of two operation sequences (Appendix B).
+struct DpArgs {
+    int64_t n_inst;
+    int I, J, kmax, out_cap;
+    int8_t kind[2 * KR_DP_MAX_OPS];      // S1's kinds, then S2's (1 = communication)
+    int8_t run1[KR_DP_MAX_OPS + 1];      // computations in a row from S1[i] (0 at i = I)
+    int8_t run2[KR_DP_MAX_OPS + 1];      // the same for S2
+    const double *ops;                   // [n_inst][I + J][4]
+    double p_static;
+    double *out_T, *out_E;               // [n_inst][out_cap]
+    int32_t *out_sched;                  // [n_inst][out_cap][I + J] or null
+    int32_t *out_n, *status;
+};
+hipError_t launch_dp(const DpArgs &a, hipStream_t st);
 
 }  // namespace kr

@@ -1,0 +1,288 @@
+// Launch-timing frontier of two operation sequences (Appendix B's dynamic program), one
+// instance per 64-lane workgroup.
+//
+// The cells P(i, j) (suffixes from S1[i] and S2[j]) are filled from (I, J) back to
+// (0, 0), row by row, so every successor is ready.  Per cell:
+//   * one lane per decision slot (S1 op alone, S2 op alone, S1's communication
+//     overlapped with k of S2's computations, the same swapped) prices its group with
+//     the fluid overlap walk and checks that it is allowed; the allowed slots, in that
+//     order, become the cell's sources;
+//   * the candidates are (group + successor point) over the sources, in source order
+//     and then the successor's order; their index is their generation order;
+//   * a candidate is kept iff no candidate before it in (T, E, index) order has energy at
+//     or below its own (GetFrontier with exact duplicates to the first), decided by
+//     comparing against every candidate through LDS broadcast reads (cells hold tens of
+//     candidates, so this beats sorting); a kept point's rank is the number of kept
+//     points with a smaller time;
+//   * the kept points go to an LDS arena with their back-pointer (source, point).
+// The schedules of P(0, 0) are then walked back one lane per point.
+#include <math.h>
+
+#include "kr_device.h"
+#include "kr_launch.h"
+
+namespace kr {
+
+namespace {
+
+constexpr int kSlots = 2 + 2 * KR_DP_MAX_K;
+
+__device__ __forceinline__ void dp_alone(const double *op, double ps, double *T, double *E)
+{
+    const double t = op[0], p = op[1];
+    *T = t;
+    *E = t * p + ps * t;
+}
+
+// A communication `c` with the computations ops[r0], ops[r0 + 1], ... ops[r0 + k - 1].
+__device__ __forceinline__ void dp_group(const double *ops, int c, int r0, int k, double ps,
+                                         double *T, double *E)
+{
+    const double tc = ops[4 * c], pc = ops[4 * c + 1];
+    double tau = 0.0, e = 0.0;
+    for (int r = 0; r < k; ++r) {
+        const double *o = ops + 4 * (r0 + r);
+        const double t0 = o[0], p0 = o[1], t1 = o[2], p1 = o[3];
+        if (tau < tc) {
+            const double nt = tau + t1;
+            if (nt <= tc) {
+                e = e + t1 * p1;
+                tau = nt;
+            } else {
+                const double dt = tc - tau;
+                const double rem = 1.0 - dt / t1;
+                const double ta = rem * t0;
+                e = e + dt * p1;
+                e = e + ta * p0;
+                tau = tc + ta;
+            }
+        } else {
+            e = e + t0 * p0;
+            tau = tau + t0;
+        }
+    }
+    const double t = tau > tc ? tau : tc;
+    *T = t;
+    *E = (e + tc * pc) + ps * t;
+}
+
+struct Slots {
+    int va, vb, nc, nd;  // allowed: S1 alone, S2 alone, overlaps of each kind
+};
+
+__device__ __forceinline__ Slots dp_slots(const DpArgs &a, int i, int j)
+{
+    Slots s;
+    s.va = i < a.I;
+    s.vb = j < a.J;
+    s.nc = i < a.I && a.kind[i] == 1 ? min(a.kmax, (int)a.run2[j]) : 0;
+    s.nd = j < a.J && a.kind[a.I + j] == 1 ? min(a.kmax, (int)a.run1[i]) : 0;
+    return s;
+}
+
+// Source r of cell (i, j) -> decision code (case * 32 + k) and successor cell.
+__device__ __forceinline__ int dp_decode(const DpArgs &a, int i, int j, int r, int *ni, int *nj)
+{
+    const Slots s = dp_slots(a, i, j);
+    if (r < s.va) {
+        *ni = i + 1;
+        *nj = j;
+        return 0;
+    }
+    r -= s.va;
+    if (r < s.vb) {
+        *ni = i;
+        *nj = j + 1;
+        return 32;
+    }
+    r -= s.vb;
+    if (r < s.nc) {
+        *ni = i + 1;
+        *nj = j + r + 1;
+        return 64 + r + 1;
+    }
+    r -= s.nc;
+    *ni = i + r + 1;
+    *nj = j + 1;
+    return 96 + r + 1;
+}
+
+__global__ void __launch_bounds__(64) dp_kernel(DpArgs a)
+{
+    __shared__ double ops[4 * 2 * KR_DP_MAX_OPS];
+    __shared__ double arT[KR_DP_ARENA], arE[KR_DP_ARENA];
+    __shared__ int16_t arB[KR_DP_ARENA];
+    __shared__ int16_t cstart[(KR_DP_MAX_OPS + 1) * (KR_DP_MAX_OPS + 1)];
+    __shared__ int16_t ccnt[(KR_DP_MAX_OPS + 1) * (KR_DP_MAX_OPS + 1)];
+    __shared__ double cT[KR_DP_CAND], cE[KR_DP_CAND];
+    __shared__ uint8_t keep[KR_DP_CAND];
+    __shared__ double sT[kSlots], sE[kSlots];
+    __shared__ int32_t soff[kSlots + 1], sstart[kSlots];
+    const int lane = threadIdx.x;
+    const int64_t inst = blockIdx.x;
+    const int nops = a.I + a.J, W = a.J + 1;
+    for (int x = lane; x < 4 * nops; x += 64) ops[x] = a.ops[inst * 4 * nops + x];
+    if (lane == 0) {
+        const int last = a.I * W + a.J;
+        arT[0] = 0.0;
+        arE[0] = 0.0;
+        arB[0] = -1;
+        cstart[last] = 0;
+        ccnt[last] = 1;
+    }
+    __syncthreads();
+    int used = 1;  // arena points in use (uniform)
+    bool ok = true;
+    for (int i = a.I; i >= 0 && ok; --i) {
+        for (int j = a.J; j >= 0 && ok; --j) {
+            if (i == a.I && j == a.J) continue;
+            const Slots s = dp_slots(a, i, j);
+            // lane = decision slot in canonical order; allowed slots become sources
+            bool allowed = false;
+            double gT = 0.0, gE = 0.0;
+            int ni = 0, nj = 0;
+            if (lane == 0 && s.va) {
+                allowed = true;
+                dp_alone(ops + 4 * i, a.p_static, &gT, &gE);
+                ni = i + 1;
+                nj = j;
+            } else if (lane == 1 && s.vb) {
+                allowed = true;
+                dp_alone(ops + 4 * (a.I + j), a.p_static, &gT, &gE);
+                ni = i;
+                nj = j + 1;
+            } else if (lane >= 2 && lane < 2 + KR_DP_MAX_K && lane - 1 <= s.nc) {
+                const int k = lane - 1;
+                allowed = true;
+                dp_group(ops, i, a.I + j, k, a.p_static, &gT, &gE);
+                ni = i + 1;
+                nj = j + k;
+            } else if (lane >= 2 + KR_DP_MAX_K && lane < kSlots &&
+                       lane - 1 - KR_DP_MAX_K <= s.nd) {
+                const int k = lane - 1 - KR_DP_MAX_K;
+                allowed = true;
+                dp_group(ops, a.I + j, i, k, a.p_static, &gT, &gE);
+                ni = i + k;
+                nj = j + 1;
+            }
+            const uint64_t m = __ballot(allowed);
+            const int ns = __popcll(m);
+            const int r = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+            const int n_succ = allowed ? ccnt[ni * W + nj] : 0;
+            // exclusive prefix of the successor counts in source order
+            int inc = n_succ;
+            for (int d = 1; d < 64; d <<= 1) {
+                const int y = __shfl_up(inc, d, 64);
+                if (lane >= d) inc += y;
+            }
+            const int C = __shfl(inc, 63, 64);
+            if (allowed) {
+                sT[r] = gT;
+                sE[r] = gE;
+                soff[r] = inc - n_succ;
+                sstart[r] = cstart[ni * W + nj];
+            }
+            if (lane == 0) soff[ns] = C;
+            __syncthreads();
+            if (C > KR_DP_CAND) {
+                ok = false;
+                break;
+            }
+            for (int c = lane; c < C; c += 64) {
+                int lo = 0, hi = ns - 1;  // last source with soff <= c
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (soff[mid] <= c) lo = mid;
+                    else hi = mid - 1;
+                }
+                const int q = c - soff[lo];
+                cT[c] = sT[lo] + arT[sstart[lo] + q];
+                cE[c] = sE[lo] + arE[sstart[lo] + q];
+            }
+            __syncthreads();
+            int kept_here = 0;
+            for (int c = lane; c < C; c += 64) {
+                const double t = cT[c], e = cE[c];
+                bool k = true;
+                for (int y = 0; y < C; ++y) {
+                    const double ty = cT[y], ey = cE[y];
+                    const bool before = ty < t || (ty == t && (ey < e || (ey == e && y < c)));
+                    if (before && ey <= e) k = false;
+                }
+                keep[c] = k;
+                kept_here += k;
+            }
+            __syncthreads();
+            int kept = kept_here;
+            for (int d = 32; d > 0; d >>= 1) kept += __shfl_xor(kept, d, 64);
+            if (kept > KR_DP_CELL_CAP || used + kept > KR_DP_ARENA) {
+                ok = false;
+                break;
+            }
+            for (int c = lane; c < C; c += 64) {
+                if (!keep[c]) continue;
+                const double t = cT[c];
+                int rank = 0;
+                for (int y = 0; y < C; ++y) rank += keep[y] && cT[y] < t;
+                int lo = 0, hi = ns - 1;
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (soff[mid] <= c) lo = mid;
+                    else hi = mid - 1;
+                }
+                arT[used + rank] = t;
+                arE[used + rank] = cE[c];
+                arB[used + rank] = (int16_t)(lo * 64 + (c - soff[lo]));
+            }
+            if (lane == 0) {
+                cstart[i * W + j] = (int16_t)used;
+                ccnt[i * W + j] = (int16_t)kept;
+            }
+            used += kept;
+            __syncthreads();
+        }
+    }
+    if (!ok) {
+        if (lane == 0) {
+            a.out_n[inst] = -1;
+            *a.status = KR_ECAPACITY;
+        }
+        return;
+    }
+    const int n0 = ccnt[0];
+    if (lane == 0) a.out_n[inst] = n0;
+    const int q = lane;
+    if (q < n0 && q < a.out_cap) {
+        const int64_t o = inst * a.out_cap + q;
+        a.out_T[o] = arT[cstart[0] + q];
+        a.out_E[o] = arE[cstart[0] + q];
+        if (a.out_sched) {
+            int32_t *sc = a.out_sched + o * nops;
+            int ci = 0, cj = 0, cq = q, d = 0;
+            while (!(ci == a.I && cj == a.J) && d < nops) {
+                const int b = arB[cstart[ci * W + cj] + cq];
+                int ni, nj;
+                sc[d++] = dp_decode(a, ci, cj, b / 64, &ni, &nj);
+                ci = ni;
+                cj = nj;
+                cq = b % 64;
+            }
+            for (; d < nops; ++d) sc[d] = -1;
+        }
+    }
+}
+
+__global__ void dp_init_kernel(int32_t *status) { *status = KR_OK; }
+
+}  // namespace
+
+hipError_t launch_dp(const DpArgs &a, hipStream_t st)
+{
+    hipLaunchKernelGGL(dp_init_kernel, dim3(1), dim3(1), 0, st, a.status);
+    if (a.n_inst > 0)
+        hipLaunchKernelGGL(dp_kernel, dim3((unsigned)a.n_inst), dim3(64), 0, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace kr

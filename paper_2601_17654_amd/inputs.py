@@ -315,3 +315,45 @@ def perturb(v, z, rel: float):
     """v * (1 + rel * z): a prediction or measurement off by up to rel (numpy or torch;
     one rounding per operation, so both give the same bits)."""
     return v * (1.0 + rel * z)
+
+
+# ---- two-sequence launch-timing instances (Appendix B) ------------------------------
+# A transformer block of one nanobatch: four computations, a collective, five
+# computations, a collective; two nanobatches give the two sequences (Appendix B's
+# 9 computations and the block's collectives per sequence).
+DP_BLOCK = (0, 0, 0, 0, 1, 0, 0, 0, 0, 0, 1)
+DP_KMAX = 9
+
+
+def dp_instances(w: "Workload", parts: Sequence[int], block: Sequence[int] = DP_BLOCK) -> tuple:
+    """Per (partition, frequency, SM choice) the ops of two nanobatches of `block`, read
+    from a workload with two comm kernels: S1 takes computations 0, 1, ... and the comm
+    kernels in order, S2 the next computations and the same comm kernels.  Computation
+    o: (t alone, power alone, t shared, power shared) at SM state 0 and s + 1;
+    communication m: (tc, pc) at SM choice s.  Returns (kind1, kind2, ops [n][I + J][4],
+    index [n][3] of (partition, f, s)), instances in (partition, f, s) order."""
+    sp = w.space
+    parts = np.asarray(list(parts), dtype=np.int64)
+    P, F, S = len(parts), sp.n_freq, sp.n_sm
+    ncomp = sum(1 for k in block if k == 0)
+    t, pw, tc, pc = w.t[parts], w.pw[parts], w.tc[parts], w.pc[parts]
+    cols = []
+    for seq in range(2):
+        ci, cm = seq * ncomp, 0
+        for k in block:
+            op = np.zeros((P, F, S, 4))
+            if k == 0:
+                op[..., 0] = t[:, :, ci, 0][:, :, None]
+                op[..., 1] = pw[:, :, ci, 0][:, :, None]
+                op[..., 2] = t[:, :, ci, 1:S + 1]
+                op[..., 3] = pw[:, :, ci, 1:S + 1]
+                ci += 1
+            else:
+                op[..., 0] = tc[:, :, cm % sp.n_comm, :S]
+                op[..., 1] = pc[:, :, cm % sp.n_comm, :S]
+                cm += 1
+            cols.append(op)
+    ops = np.stack(cols, axis=3).reshape(P * F * S, len(cols), 4)
+    pi, fi, si = np.meshgrid(parts, np.arange(F), np.arange(S), indexing="ij")
+    index = np.stack([pi.ravel(), fi.ravel(), si.ravel()], axis=1).astype(np.int32)
+    return list(block), list(block), np.ascontiguousarray(ops), index

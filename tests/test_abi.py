@@ -87,6 +87,11 @@ def test_host_validation_without_gpu():
     assert L.kr_uncertainty(0, 10, one, one, one, null) == b.KR_EINVAL
     assert L.kr_compare_frontiers(0, one, one, 1, one, one, one, one, big, null) == b.KR_EINVAL
     assert L.kr_compare_frontiers(1, one, one, 1, one, one, one, one, 8, null) == b.KR_ECAPACITY
+    kind = (ctypes.c_int32 * 30)(*([0] * 29 + [2]))
+    for n, I_, J_, kmax, cap in ((1, 25, 1, 1, 8), (1, 0, 0, 1, 8), (1, 3, 3, 17, 8),
+                                 (1, 3, 3, 1, 65), (1, 3, 3, 1, 0), (1, 29, 1, 1, 8)):
+        assert L.kr_launch_timing_frontier(n, I_, J_, kind, one, 90.0, kmax, cap, one, one, one,
+                                           one, one, null) == b.KR_EINVAL
     assert L.kr_uncertainty(65, 10, one, one, one, null) == b.KR_EINVAL
 
 
