@@ -419,17 +419,20 @@ kr_status kr_compare_frontiers(int64_t nA, const double *TA, const double *EA, i
  *                   KR_DP_CELL_CAP points, more than KR_DP_CAND candidates in a cell, or
  *                   more than KR_DP_ARENA points over all cells)
  *   status_out      device [1]: KR_OK, or KR_ECAPACITY if any instance hit a limit
+ * Instances are first solved with a small on-chip budget (many per compute unit); the
+ * few that need more are queued and solved again with the full budget.
  */
 #define KR_DP_MAX_OPS 24
 #define KR_DP_MAX_K 16
 #define KR_DP_CELL_CAP 64
-#define KR_DP_CAND 512
-#define KR_DP_ARENA 1024
+#define KR_DP_CAND 1024
+#define KR_DP_ARENA 2048
+size_t kr_launch_timing_frontier_workspace(int64_t n_inst);
 kr_status kr_launch_timing_frontier(int64_t n_inst, int32_t I, int32_t J, const int32_t *kind,
                                     const double *ops, double p_static, int32_t kmax,
                                     int32_t out_cap, double *out_T, double *out_E,
                                     int32_t *out_sched, int32_t *out_n, int32_t *status_out,
-                                    void *stream);
+                                    void *ws, size_t ws_bytes, void *stream);
 
 /*
  * kr_decode_candidates -- candidate index -> (frequency index, launch positions, SM

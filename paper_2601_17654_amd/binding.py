@@ -67,7 +67,8 @@ _SIGS = {
     "kr_compare_frontiers": (_i32, [_i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _sz, _vp]),
     "kr_compare_frontiers_workspace": (_sz, []),
     "kr_launch_timing_frontier": (_i32, [_i64, _i32, _i32, _vp, _vp, _f64, _i32, _i32, _vp, _vp,
-                                         _vp, _vp, _vp, _vp]),
+                                         _vp, _vp, _vp, _vp, _sz, _vp]),
+    "kr_launch_timing_frontier_workspace": (_sz, [_i64]),
     "kr_status_string": (ctypes.c_char_p, [_i32]),
     "kr_set_phase_events": (_i32, [_i32, _vp, _vp]),
 }
@@ -569,11 +570,14 @@ def launch_timing_frontier(kind1, kind2, ops, p_static: float, kmax: int, out_ca
             torch.empty((n, out_cap, I + J), dtype=torch.int32, device="cuda") if sched else None,
             torch.empty(max(n, 1), dtype=torch.int32, device="cuda"),
             torch.empty(1, dtype=torch.int32, device="cuda"))
+    wsb = _lib.kr_launch_timing_frontier_workspace(n)
+    ws = _workspace(wsb)
     _check("kr_launch_timing_frontier",
            _lib.kr_launch_timing_frontier(n, I, J, kind.ctypes.data_as(ctypes.c_void_p),
                                           _ptr(ops), float(p_static), kmax, out_cap,
                                           _ptr(out.T), _ptr(out.E), _ptr(out.sched),
-                                          _ptr(out.n), _ptr(out.status), _stream()))
+                                          _ptr(out.n), _ptr(out.status), _ptr(ws), wsb,
+                                          _stream()))
     if check and int(out.status.item()) != KR_OK:
         raise KrError("kr_launch_timing_frontier", int(out.status.item()))
     return out

@@ -773,17 +773,27 @@ kr_status kr_compare_frontiers(int64_t nA, const double *TA, const double *EA, i
     return launch_compare(a, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
 }
 
+size_t kr_launch_timing_frontier_workspace(int64_t n_inst)
+{
+    if (n_inst < 0 || n_inst > INT32_MAX) return 0;
+    Carve c(nullptr);
+    c.take<int32_t>(1);
+    c.take<int32_t>(std::max<int64_t>(n_inst, 1));
+    return c.used;
+}
+
 kr_status kr_launch_timing_frontier(int64_t n_inst, int32_t I, int32_t J, const int32_t *kind,
                                     const double *ops, double p_static, int32_t kmax,
                                     int32_t out_cap, double *out_T, double *out_E,
                                     int32_t *out_sched, int32_t *out_n, int32_t *status_out,
-                                    void *stream)
+                                    void *ws, size_t ws_bytes, void *stream)
 {
     if (n_inst < 0 || n_inst > INT32_MAX || I < 0 || J < 0 || I > KR_DP_MAX_OPS ||
         J > KR_DP_MAX_OPS || I + J < 1 || !kind || kmax < 0 || kmax > KR_DP_MAX_K ||
         out_cap < 1 || out_cap > 64 || !status_out || !(p_static == p_static) ||
-        (n_inst > 0 && (!ops || !out_T || !out_E || !out_n)))
+        (n_inst > 0 && (!ops || !out_T || !out_E || !out_n)) || !ws)
         return KR_EINVAL;
+    if (ws_bytes < kr_launch_timing_frontier_workspace(n_inst)) return KR_ECAPACITY;
     DpArgs a;
     std::memset(&a, 0, sizeof(a));
     a.n_inst = n_inst;
@@ -805,6 +815,12 @@ kr_status kr_launch_timing_frontier(int64_t n_inst, int32_t I, int32_t J, const 
     a.out_sched = out_sched;
     a.out_n = out_n;
     a.status = status_out;
+    // first pass: a budget that lets many instances share a compute unit's LDS
+    a.arena_s = 384;
+    a.cand_s = 128;
+    Carve c(ws);
+    a.retry_n = c.take<int32_t>(1);
+    a.retry = c.take<int32_t>(std::max<int64_t>(n_inst, 1));
     return launch_dp(a, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
 }
 

@@ -219,6 +219,8 @@ struct DpArgs {
     double *out_T, *out_E;               // [n_inst][out_cap]
     int32_t *out_sched;                  // [n_inst][out_cap][I + J] or null
     int32_t *out_n, *status;
+    int arena_s, cand_s;                 // first pass's on-chip budget (points, candidates)
+    int32_t *retry, *retry_n;            // [n_inst], [1]: instances left to the full budget
 };
 hipError_t launch_dp(const DpArgs &a, hipStream_t st);
 

@@ -107,20 +107,52 @@ __device__ __forceinline__ int dp_decode(const DpArgs &a, int i, int j, int r, i
     return 96 + r + 1;
 }
 
-__global__ void __launch_bounds__(64) dp_kernel(DpArgs a)
+// Byte offsets of the LDS sections of one instance (all 8-byte aligned).
+struct DpLds {
+    int ops, arT, arE, cT, cE, sT, sE, soff, sstart, arB, cstart, ccnt, keep, bytes;
+};
+
+__host__ __device__ inline DpLds dp_lds(int nops, int ncell, int arena, int cand)
 {
-    __shared__ double ops[4 * 2 * KR_DP_MAX_OPS];
-    __shared__ double arT[KR_DP_ARENA], arE[KR_DP_ARENA];
-    __shared__ int16_t arB[KR_DP_ARENA];
-    __shared__ int16_t cstart[(KR_DP_MAX_OPS + 1) * (KR_DP_MAX_OPS + 1)];
-    __shared__ int16_t ccnt[(KR_DP_MAX_OPS + 1) * (KR_DP_MAX_OPS + 1)];
-    __shared__ double cT[KR_DP_CAND], cE[KR_DP_CAND];
-    __shared__ uint8_t keep[KR_DP_CAND];
-    __shared__ double sT[kSlots], sE[kSlots];
-    __shared__ int32_t soff[kSlots + 1], sstart[kSlots];
+    DpLds l;
+    int o = 0;
+    auto take = [&](int bytes) {
+        const int at = o;
+        o += (bytes + 7) / 8 * 8;
+        return at;
+    };
+    l.ops = take(32 * nops);
+    l.arT = take(8 * arena);
+    l.arE = take(8 * arena);
+    l.cT = take(8 * cand);
+    l.cE = take(8 * cand);
+    l.sT = take(8 * kSlots);
+    l.sE = take(8 * kSlots);
+    l.soff = take(4 * (kSlots + 1));
+    l.sstart = take(4 * kSlots);
+    l.arB = take(2 * arena);
+    l.cstart = take(2 * ncell);
+    l.ccnt = take(2 * ncell);
+    l.keep = take(cand);
+    l.bytes = o;
+    return l;
+}
+
+// One instance by one wave, with an arena of `arena` points and `cand` candidates per
+// cell; false (nothing written) if the instance needs more.
+__device__ bool dp_solve(const DpArgs &a, int64_t inst, char *lds, int arena, int cand)
+{
     const int lane = threadIdx.x;
-    const int64_t inst = blockIdx.x;
     const int nops = a.I + a.J, W = a.J + 1;
+    const DpLds L = dp_lds(nops, (a.I + 1) * W, arena, cand);
+    double *ops = (double *)(lds + L.ops);
+    double *arT = (double *)(lds + L.arT), *arE = (double *)(lds + L.arE);
+    double *cT = (double *)(lds + L.cT), *cE = (double *)(lds + L.cE);
+    double *sT = (double *)(lds + L.sT), *sE = (double *)(lds + L.sE);
+    int32_t *soff = (int32_t *)(lds + L.soff), *sstart = (int32_t *)(lds + L.sstart);
+    int16_t *arB = (int16_t *)(lds + L.arB);
+    int16_t *cstart = (int16_t *)(lds + L.cstart), *ccnt = (int16_t *)(lds + L.ccnt);
+    uint8_t *keep = (uint8_t *)(lds + L.keep);
     for (int x = lane; x < 4 * nops; x += 64) ops[x] = a.ops[inst * 4 * nops + x];
     if (lane == 0) {
         const int last = a.I * W + a.J;
@@ -185,7 +217,7 @@ __global__ void __launch_bounds__(64) dp_kernel(DpArgs a)
             }
             if (lane == 0) soff[ns] = C;
             __syncthreads();
-            if (C > KR_DP_CAND) {
+            if (C > cand) {
                 ok = false;
                 break;
             }
@@ -216,7 +248,7 @@ __global__ void __launch_bounds__(64) dp_kernel(DpArgs a)
             __syncthreads();
             int kept = kept_here;
             for (int d = 32; d > 0; d >>= 1) kept += __shfl_xor(kept, d, 64);
-            if (kept > KR_DP_CELL_CAP || used + kept > KR_DP_ARENA) {
+            if (kept > KR_DP_CELL_CAP || used + kept > arena) {
                 ok = false;
                 break;
             }
@@ -243,13 +275,7 @@ __global__ void __launch_bounds__(64) dp_kernel(DpArgs a)
             __syncthreads();
         }
     }
-    if (!ok) {
-        if (lane == 0) {
-            a.out_n[inst] = -1;
-            *a.status = KR_ECAPACITY;
-        }
-        return;
-    }
+    if (!ok) return false;
     const int n0 = ccnt[0];
     if (lane == 0) a.out_n[inst] = n0;
     const int q = lane;
@@ -271,17 +297,54 @@ __global__ void __launch_bounds__(64) dp_kernel(DpArgs a)
             for (; d < nops; ++d) sc[d] = -1;
         }
     }
+    return true;
 }
 
-__global__ void dp_init_kernel(int32_t *status) { *status = KR_OK; }
+__global__ void dp_init_kernel(int32_t *status, int32_t *retry_n)
+{
+    *status = KR_OK;
+    *retry_n = 0;
+}
+
+// Every instance with the small on-chip budget; the ones that need more are queued.
+__global__ void __launch_bounds__(64) dp_first_kernel(DpArgs a)
+{
+    extern __shared__ double dp_smem[];
+    const int64_t inst = blockIdx.x;
+    if (!dp_solve(a, inst, (char *)dp_smem, a.arena_s, a.cand_s) && threadIdx.x == 0) {
+        a.out_n[inst] = -1;
+        a.retry[atomicAdd(a.retry_n, 1)] = (int32_t)inst;
+    }
+}
+
+// The queued instances with the full budget (persistent grid over the queue).
+__global__ void __launch_bounds__(64) dp_retry_kernel(DpArgs a)
+{
+    extern __shared__ double dp_smem[];
+    const int n = *a.retry_n;
+    for (int r = blockIdx.x; r < n; r += gridDim.x) {
+        const int64_t inst = a.retry[r];
+        if (!dp_solve(a, inst, (char *)dp_smem, KR_DP_ARENA, KR_DP_CAND) && threadIdx.x == 0) {
+            a.out_n[inst] = -1;
+            *a.status = KR_ECAPACITY;
+        }
+        __syncthreads();
+    }
+}
 
 }  // namespace
 
 hipError_t launch_dp(const DpArgs &a, hipStream_t st)
 {
-    hipLaunchKernelGGL(dp_init_kernel, dim3(1), dim3(1), 0, st, a.status);
-    if (a.n_inst > 0)
-        hipLaunchKernelGGL(dp_kernel, dim3((unsigned)a.n_inst), dim3(64), 0, st, a);
+    hipLaunchKernelGGL(dp_init_kernel, dim3(1), dim3(1), 0, st, a.status, a.retry_n);
+    if (a.n_inst > 0) {
+        const int nops = a.I + a.J, ncell = (a.I + 1) * (a.J + 1);
+        const int small = dp_lds(nops, ncell, a.arena_s, a.cand_s).bytes;
+        const int big = dp_lds(nops, ncell, KR_DP_ARENA, KR_DP_CAND).bytes;
+        hipLaunchKernelGGL(dp_first_kernel, dim3((unsigned)a.n_inst), dim3(64), small, st, a);
+        const int64_t g = a.n_inst < 1024 ? a.n_inst : 1024;
+        hipLaunchKernelGGL(dp_retry_kernel, dim3((unsigned)g), dim3(64), big, st, a);
+    }
     return hipGetLastError();
 }
 

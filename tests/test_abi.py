@@ -91,7 +91,9 @@ def test_host_validation_without_gpu():
     for n, I_, J_, kmax, cap in ((1, 25, 1, 1, 8), (1, 0, 0, 1, 8), (1, 3, 3, 17, 8),
                                  (1, 3, 3, 1, 65), (1, 3, 3, 1, 0), (1, 29, 1, 1, 8)):
         assert L.kr_launch_timing_frontier(n, I_, J_, kind, one, 90.0, kmax, cap, one, one, one,
-                                           one, one, null) == b.KR_EINVAL
+                                           one, one, one, big, null) == b.KR_EINVAL
+    assert L.kr_launch_timing_frontier(4, 3, 3, kind, one, 90.0, 2, 8, one, one, one, one, one,
+                                       one, 4, null) == b.KR_ECAPACITY
     assert L.kr_uncertainty(65, 10, one, one, one, null) == b.KR_EINVAL
 
 

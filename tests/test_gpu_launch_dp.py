@@ -14,7 +14,7 @@ from paper_2601_17654_amd import inputs as I
 pytestmark = pytest.mark.gpu
 
 # the kernel's on-chip limits: points of one cell, points of all cells, candidates of a cell
-LIMITS = (64, 1024, 512)
+LIMITS = (64, 2048, 1024)
 
 
 @pytest.fixture(scope="module")
@@ -72,7 +72,8 @@ def _compare(kr, kind1, kind2, ops, ps, kmax, what, out_cap=64):
     ([0, 0, 0, 0, 0, 0], [], 3),              # one sequence only
     ([], [1, 0, 0], 2),
     ([0] * 24, [1] * 2, 16),                  # the longest sequence, the largest kmax
-    ([0, 1] * 6, [1, 0] * 6, 16),
+    ([0, 1] * 6, [1, 0] * 6, 16),             # many instances past the first pass's budget
+    ([0, 1] * 12, [1, 0] * 12, 16),           # some past the full budget
 ])
 def test_random_instances(kr, kind1, kind2, kmax):
     rng = np.random.default_rng(len(kind1) * 31 + len(kind2) + kmax)
