@@ -420,7 +420,8 @@ kr_status kr_compare_frontiers(int64_t nA, const double *TA, const double *EA, i
  *                   more than KR_DP_ARENA points over all cells)
  *   status_out      device [1]: KR_OK, or KR_ECAPACITY if any instance hit a limit
  * Instances are first solved with a small on-chip budget (many per compute unit); the
- * few that need more are queued and solved again with the full budget.
+ * few that need more are queued and solved again with half the full arena, and the
+ * rest with the full budget.
  */
 #define KR_DP_MAX_OPS 24
 #define KR_DP_MAX_K 16

@@ -777,8 +777,8 @@ size_t kr_launch_timing_frontier_workspace(int64_t n_inst)
 {
     if (n_inst < 0 || n_inst > INT32_MAX) return 0;
     Carve c(nullptr);
-    c.take<int32_t>(1);
-    c.take<int32_t>(std::max<int64_t>(n_inst, 1));
+    c.take<int32_t>(2);
+    c.take<int32_t>(2 * std::max<int64_t>(n_inst, 1));
     return c.used;
 }
 
@@ -819,8 +819,8 @@ kr_status kr_launch_timing_frontier(int64_t n_inst, int32_t I, int32_t J, const 
     a.arena_s = 384;
     a.cand_s = 128;
     Carve c(ws);
-    a.retry_n = c.take<int32_t>(1);
-    a.retry = c.take<int32_t>(std::max<int64_t>(n_inst, 1));
+    a.retry_n = c.take<int32_t>(2);
+    a.retry = c.take<int32_t>(2 * std::max<int64_t>(n_inst, 1));
     return launch_dp(a, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
 }
 

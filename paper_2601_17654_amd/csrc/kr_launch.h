@@ -220,7 +220,7 @@ struct DpArgs {
     int32_t *out_sched;                  // [n_inst][out_cap][I + J] or null
     int32_t *out_n, *status;
     int arena_s, cand_s;                 // first pass's on-chip budget (points, candidates)
-    int32_t *retry, *retry_n;            // [n_inst], [1]: instances left to the full budget
+    int32_t *retry, *retry_n;            // [2][n_inst], [2]: instances left to larger budgets
 };
 hipError_t launch_dp(const DpArgs &a, hipStream_t st);
 

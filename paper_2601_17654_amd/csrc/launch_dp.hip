@@ -303,7 +303,8 @@ __device__ bool dp_solve(const DpArgs &a, int64_t inst, char *lds, int arena, in
 __global__ void dp_init_kernel(int32_t *status, int32_t *retry_n)
 {
     *status = KR_OK;
-    *retry_n = 0;
+    retry_n[0] = 0;
+    retry_n[1] = 0;
 }
 
 // Every instance with the small on-chip budget; the ones that need more are queued.
@@ -317,16 +318,22 @@ __global__ void __launch_bounds__(64) dp_first_kernel(DpArgs a)
     }
 }
 
-// The queued instances with the full budget (persistent grid over the queue).
-__global__ void __launch_bounds__(64) dp_retry_kernel(DpArgs a)
+// The instances of queue `tier` (0 or 1) with a larger budget (persistent grid over the
+// queue); the ones that still do not fit go to the next queue, or are reported after
+// the last tier.
+__global__ void __launch_bounds__(64) dp_retry_kernel(DpArgs a, int tier, int arena, int cand)
 {
     extern __shared__ double dp_smem[];
-    const int n = *a.retry_n;
+    const int n = a.retry_n[tier];
+    const int32_t *q = a.retry + (int64_t)tier * a.n_inst;
     for (int r = blockIdx.x; r < n; r += gridDim.x) {
-        const int64_t inst = a.retry[r];
-        if (!dp_solve(a, inst, (char *)dp_smem, KR_DP_ARENA, KR_DP_CAND) && threadIdx.x == 0) {
+        const int64_t inst = q[r];
+        if (!dp_solve(a, inst, (char *)dp_smem, arena, cand) && threadIdx.x == 0) {
             a.out_n[inst] = -1;
-            *a.status = KR_ECAPACITY;
+            if (tier == 0)
+                a.retry[a.n_inst + atomicAdd(a.retry_n + 1, 1)] = (int32_t)inst;
+            else
+                *a.status = KR_ECAPACITY;
         }
         __syncthreads();
     }
@@ -340,10 +347,16 @@ hipError_t launch_dp(const DpArgs &a, hipStream_t st)
     if (a.n_inst > 0) {
         const int nops = a.I + a.J, ncell = (a.I + 1) * (a.J + 1);
         const int small = dp_lds(nops, ncell, a.arena_s, a.cand_s).bytes;
-        const int big = dp_lds(nops, ncell, KR_DP_ARENA, KR_DP_CAND).bytes;
         hipLaunchKernelGGL(dp_first_kernel, dim3((unsigned)a.n_inst), dim3(64), small, st, a);
-        const int64_t g = a.n_inst < 1024 ? a.n_inst : 1024;
-        hipLaunchKernelGGL(dp_retry_kernel, dim3((unsigned)g), dim3(64), big, st, a);
+        // middle budget: still several instances per compute unit; then the full one
+        const int am = KR_DP_ARENA / 2, cm = KR_DP_CAND / 4;
+        const int mid = dp_lds(nops, ncell, am, cm).bytes;
+        const int big = dp_lds(nops, ncell, KR_DP_ARENA, KR_DP_CAND).bytes;
+        const int64_t g1 = a.n_inst < 2048 ? a.n_inst : 2048;
+        const int64_t g2 = a.n_inst < 512 ? a.n_inst : 512;
+        hipLaunchKernelGGL(dp_retry_kernel, dim3((unsigned)g1), dim3(64), mid, st, a, 0, am, cm);
+        hipLaunchKernelGGL(dp_retry_kernel, dim3((unsigned)g2), dim3(64), big, st, a, 1,
+                           KR_DP_ARENA, KR_DP_CAND);
     }
     return hipGetLastError();
 }
