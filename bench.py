@@ -102,6 +102,25 @@ def read_mbo_traffic():
             if k + ".traffic_bytes_per_launch" in vals}, "counters"
 
 
+VALU_COUNTERS = os.path.join(ROOT, "profiles", "eval_valu_counters_eval_stress.txt")
+VALU_ISSUE_PEAK = 1024 * 2.4e9 / 4  # wave instructions/s: 4 cycles per wave64 instruction
+
+
+def read_valu():
+    """VALU wave instructions and fp64 flops per launch of the fused eval kernel from the
+    committed counter summary, if taken on the current sources; else None."""
+    if not os.path.exists(VALU_COUNTERS):
+        return None
+    vals = {}
+    for line in open(VALU_COUNTERS):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.strip().split("=", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_hash") != kernel_source_hash():
+        return None
+    return float(vals["valu_wave_instructions_per_launch"]), float(vals["fp64_flops_per_launch"])
+
+
 def read_traffic(n_launch_bytes_alg: float):
     """HBM bytes per launch of the fused kernel from the committed counter summary, if
     it was taken on the current kernel source; else None."""
@@ -251,6 +270,15 @@ def main():
             "kernel": "eval_filter_wave_kernel (fused evaluation + frontier, one wave per slab)",
             "kernel_ms": round(kern_ms, 4), "algorithmic_bytes": table_bytes,
             "traffic_source": tsrc}
+
+    valu = read_valu()
+    if valu is not None:
+        vi = valu[0] / (kern_ms * 1e-3)
+        roof["alu"] = {"bound": "alu", "achieved": round(vi / 1e9, 2), "peak": VALU_ISSUE_PEAK / 1e9,
+                       "unit": "G VALU wave-instructions/s", "frac": round(vi / VALU_ISSUE_PEAK, 4),
+                       "fp64_TFLOPs": round(valu[1] / (kern_ms * 1e-3) / 1e12, 2),
+                       "fp64_peak_TFLOPs": FP64_VECTOR_TFLOPS,
+                       "source": "profiles/eval_valu_counters_eval_stress.txt"}
 
     out = {
         "metric": METRIC,
