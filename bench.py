@@ -81,8 +81,9 @@ def mbo_source_hash() -> str:
         h.update(_between(fh.read(), "// mbo.hip", "launch_select(const SelArgs &a, "
                           "hipEvent_t *ev, hipStream_t st);").encode())
     with open(os.path.join(csrc, "api.hip")) as fh:
-        h.update(_between(fh.read(), "size_t kr_hvi_scores_workspace", "\n}\n\nint32_t "
-                          "kr_hv_converged").encode())
+        api = fh.read()
+        h.update(_between(api, "size_t kr_hvi_scores_workspace",
+                          "return launch_select(a, g_phase_ev[KR_PHASE_SELECT]").encode())
     return h.hexdigest()[:16]
 
 
