@@ -109,7 +109,7 @@ def test_hvi_bad_partition_status(kr):
 
 def test_uncertainty_parity(kr):
     rng = np.random.default_rng(5)
-    for M, n in ((5, 10007), (1, 300), (16, 64)):
+    for M, n in ((5, 10007), (5, 10008), (1, 300), (16, 64)):
         Tm = rng.uniform(1e-3, 2e-3, (M, n))
         Em = rng.uniform(0.2, 0.8, (M, n))
         got = kr.uncertainty(_cuda(Tm), _cuda(Em)).cpu().numpy()
