@@ -161,7 +161,7 @@ hipError_t launch_mb_enum_gather(const MbArgs &a, const int64_t *base, const int
 // mbo.hip: scores and batch selection of the Bayesian optimisation (Section 4.3,
 // Algorithm 1).
 #define KR_HVI_TILE 1024  // candidates per block of the score kernel
-#define KR_SEL_TILE 16384  // candidates per block of the selection tile kernel
+#define KR_SEL_TILE 32768  // candidates per block of the selection tile kernel
 #define KR_SEL_LIST 64    // entries of a wave's top list (one per lane)
 
 struct HviArgs {
