@@ -379,6 +379,7 @@ def main():
         "iso_energy_time_reduction_pct": float(cm[3])}
 
     out["launch_timing"], dp_ctx = bench_dp(kr, I, torch, args, mk)
+    out["eval_two_comm"], e2_ctx = bench_eval2(kr, I, torch, args, mk)
 
     if not args.skip_cpu:
         import oracle
@@ -448,7 +449,72 @@ def main():
             "sample": "the same comparison, %.4f s" % el,
             "parity": bool(np.array_equal(rc, cm, equal_nan=True))}
         out["launch_timing"]["cpu_baseline"] = dp_cpu_baseline(oracle, dp_ctx, args.cpu_seconds)
+        out["eval_two_comm"]["cpu_baseline"] = eval2_cpu_baseline(oracle, e2_ctx, args.cpu_seconds)
+        host = host_info()
+        for k in ("cpu_baseline", "cpu_baseline_compose"):
+            out[k]["host"] = host
     print(json.dumps(out))
+
+
+def host_info():
+    """CPU model, logical CPUs and the oracle's compiler flags."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    import oracle
+
+    return {"cpu": model, "logical_cpus": os.cpu_count(),
+            "oracle_build": "gcc " + " ".join(oracle.CFLAGS), "threads_used": 1}
+
+
+def bench_eval2(kr, I, torch, args, mk):
+    """Fused evaluation + frontier filter of the two-comm workload (256 partitions x
+    1,148,928 candidates, two comm kernels): VALU-bound, reported as candidates/s."""
+    w2 = I.config_workload(2)
+    sp2 = w2.space
+    d2 = [torch.from_numpy(getattr(w2, k)).cuda() for k in ("t", "pw", "tc", "pc")]
+    fr = kr.evaluate_and_filter(sp2, *d2)
+    cap = int(fr.off[-1].item())
+    for _ in range(args.warmup):
+        kr.evaluate_and_filter(sp2, *d2, cap=cap, sync=False)
+    torch.cuda.synchronize()
+    steps = max(3, args.steps // 4)
+    ev = mk(2 * steps)
+    for k in range(steps):
+        ev[2 * k].record()
+        fr = kr.evaluate_and_filter(sp2, *d2, cap=cap, sync=False)
+        ev[2 * k + 1].record()
+    torch.cuda.synchronize()
+    ms = sorted(ev[2 * k].elapsed_time(ev[2 * k + 1]) for k in range(steps))
+    n = sp2.n_parts * sp2.n_cand
+    res = {"workload": "two-comm (256 partitions x 1,148,928 candidates: 48 kernels, 561 "
+                       "launch-position pairs, 8 x 8 SM choices, 32 frequencies)",
+           "candidates": n, "frontier_points": cap, "call_ms_median": round(ms[len(ms) // 2], 4),
+           "candidates_per_s": n / (ms[len(ms) // 2] * 1e-3)}
+    return res, dict(w=w2, fr=fr)
+
+
+def eval2_cpu_baseline(oracle, ctx, seconds):
+    """The oracle's evaluation + GetFrontier on the first partitions of the two-comm batch
+    (at least one), checked against the GPU's frontiers."""
+    w, fr = ctx["w"], ctx["fr"]
+    off, idx = fr.off.cpu().numpy(), fr.idx.cpu().numpy()
+    t0 = time.perf_counter()
+    n, mism = 0, 0
+    while n < w.space.n_parts and (n == 0 or time.perf_counter() - t0 < seconds):
+        T, E = oracle.evaluate_partition(w.space, w.t, w.pw, w.tc, w.pc, n)
+        mism += int(not np.array_equal(idx[off[n]:off[n + 1]], oracle.pareto(T, E)))
+        n += 1
+    el = time.perf_counter() - t0
+    return {"value": n * w.space.n_cand / el, "unit": "candidates/s", "cores": 1,
+            "kind": "oracle",
+            "sample": "first %d of the 256 partitions, evaluate + GetFrontier, %.1f s" % (n, el),
+            "frontier_mismatches": mism}
 
 
 def bench_dp(kr, I, torch, args, mk):
