@@ -109,7 +109,7 @@ __device__ __forceinline__ int dp_decode(const DpArgs &a, int i, int j, int r, i
 
 // Byte offsets of the LDS sections of one instance (all 8-byte aligned).
 struct DpLds {
-    int ops, arT, arE, cT, cE, sT, sE, soff, sstart, arB, cstart, ccnt, keep, bytes;
+    int ops, arT, arE, cT, cE, sT, sE, soff, sstart, arB, cstart, ccnt, csrc, keep, bytes;
 };
 
 __host__ __device__ inline DpLds dp_lds(int nops, int ncell, int arena, int cand)
@@ -133,6 +133,7 @@ __host__ __device__ inline DpLds dp_lds(int nops, int ncell, int arena, int cand
     l.arB = take(2 * arena);
     l.cstart = take(2 * ncell);
     l.ccnt = take(2 * ncell);
+    l.csrc = take(cand);
     l.keep = take(cand);
     l.bytes = o;
     return l;
@@ -153,6 +154,7 @@ __device__ bool dp_solve(const DpArgs &a, int64_t inst, char *lds, int arena, in
     int16_t *arB = (int16_t *)(lds + L.arB);
     int16_t *cstart = (int16_t *)(lds + L.cstart), *ccnt = (int16_t *)(lds + L.ccnt);
     uint8_t *keep = (uint8_t *)(lds + L.keep);
+    uint8_t *csrc = (uint8_t *)(lds + L.csrc);  // source of each candidate of the cell
     for (int x = lane; x < 4 * nops; x += 64) ops[x] = a.ops[inst * 4 * nops + x];
     if (lane == 0) {
         const int last = a.I * W + a.J;
@@ -221,13 +223,11 @@ __device__ bool dp_solve(const DpArgs &a, int64_t inst, char *lds, int arena, in
                 ok = false;
                 break;
             }
+            if (allowed)  // each source marks its candidates
+                for (int q = 0; q < n_succ; ++q) csrc[inc - n_succ + q] = (uint8_t)r;
+            __syncthreads();
             for (int c = lane; c < C; c += 64) {
-                int lo = 0, hi = ns - 1;  // last source with soff <= c
-                while (lo < hi) {
-                    const int mid = (lo + hi + 1) >> 1;
-                    if (soff[mid] <= c) lo = mid;
-                    else hi = mid - 1;
-                }
+                const int lo = csrc[c];
                 const int q = c - soff[lo];
                 cT[c] = sT[lo] + arT[sstart[lo] + q];
                 cE[c] = sE[lo] + arE[sstart[lo] + q];
@@ -237,6 +237,7 @@ __device__ bool dp_solve(const DpArgs &a, int64_t inst, char *lds, int arena, in
             for (int c = lane; c < C; c += 64) {
                 const double t = cT[c], e = cE[c];
                 bool k = true;
+#pragma unroll 4
                 for (int y = 0; y < C; ++y) {
                     const double ty = cT[y], ey = cE[y];
                     const bool before = ty < t || (ty == t && (ey < e || (ey == e && y < c)));
@@ -256,13 +257,9 @@ __device__ bool dp_solve(const DpArgs &a, int64_t inst, char *lds, int arena, in
                 if (!keep[c]) continue;
                 const double t = cT[c];
                 int rank = 0;
+#pragma unroll 4
                 for (int y = 0; y < C; ++y) rank += keep[y] && cT[y] < t;
-                int lo = 0, hi = ns - 1;
-                while (lo < hi) {
-                    const int mid = (lo + hi + 1) >> 1;
-                    if (soff[mid] <= c) lo = mid;
-                    else hi = mid - 1;
-                }
+                const int lo = csrc[c];
                 arT[used + rank] = t;
                 arE[used + rank] = cE[c];
                 arB[used + rank] = (int16_t)(lo * 64 + (c - soff[lo]));
