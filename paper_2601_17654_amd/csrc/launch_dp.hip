@@ -27,6 +27,23 @@ namespace {
 
 constexpr int kSlots = 2 + 2 * KR_DP_MAX_K;
 
+// Value of lane `src` (per-lane index) for a 64-bit quantity.
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t x, int src)
+{
+    const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)x, src, 64);
+    const uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(x >> 32), src, 64);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// An instance is one wave, whose LDS accesses execute in order: ordering them for the
+// compiler is all the synchronisation a cell needs.
+__device__ __forceinline__ void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+}
+
 __device__ __forceinline__ void dp_alone(const double *op, double ps, double *T, double *E)
 {
     const double t = op[0], p = op[1];
@@ -164,7 +181,7 @@ __device__ bool dp_solve(const DpArgs &a, int64_t inst, char *lds, int arena, in
         cstart[last] = 0;
         ccnt[last] = 1;
     }
-    __syncthreads();
+    wave_sync();
     int used = 1;  // arena points in use (uniform)
     bool ok = true;
     for (int i = a.I; i >= 0 && ok; --i) {
@@ -211,65 +228,114 @@ __device__ bool dp_solve(const DpArgs &a, int64_t inst, char *lds, int arena, in
                 if (lane >= d) inc += y;
             }
             const int C = __shfl(inc, 63, 64);
-            if (allowed) {
-                sT[r] = gT;
-                sE[r] = gE;
-                soff[r] = inc - n_succ;
-                sstart[r] = cstart[ni * W + nj];
-            }
-            if (lane == 0) soff[ns] = C;
-            __syncthreads();
             if (C > cand) {
                 ok = false;
                 break;
             }
-            if (allowed)  // each source marks its candidates
-                for (int q = 0; q < n_succ; ++q) csrc[inc - n_succ + q] = (uint8_t)r;
-            __syncthreads();
-            for (int c = lane; c < C; c += 64) {
-                const int lo = csrc[c];
-                const int q = c - soff[lo];
-                cT[c] = sT[lo] + arT[sstart[lo] + q];
-                cE[c] = sE[lo] + arE[sstart[lo] + q];
-            }
-            __syncthreads();
-            int kept_here = 0;
-            for (int c = lane; c < C; c += 64) {
-                const double t = cT[c], e = cE[c];
-                bool k = true;
-#pragma unroll 4
+            const int ex = inc - n_succ;  // first candidate of this lane's source
+            const int st = allowed ? (int)cstart[ni * W + nj] : 0;
+            int kept;
+            if (C <= 64) {
+                // one candidate per lane; its source found and read through lane reads
+                const bool live = lane < C;
+                int sl = 0, sr = 0, rk = 0;
+                for (uint64_t mm = m; mm; mm &= mm - 1) {
+                    const int l = __ffsll((long long)mm) - 1;
+                    if (__builtin_amdgcn_readlane(ex, l) <= lane) {
+                        sl = l;
+                        sr = rk;
+                    }
+                    ++rk;
+                }
+                const double sgT = bitsd(shfl_u64(dbits(gT), sl));
+                const double sgE = bitsd(shfl_u64(dbits(gE), sl));
+                const int q = lane - __shfl(ex, sl, 64);
+                const int sst = __shfl(st, sl, 64);
+                double t = INFINITY, e = INFINITY;
+                const int lo = sr;
+                if (live) {
+                    t = sgT + arT[sst + q];
+                    e = sgE + arE[sst + q];
+                }
+                bool k = live;
                 for (int y = 0; y < C; ++y) {
-                    const double ty = cT[y], ey = cE[y];
-                    const bool before = ty < t || (ty == t && (ey < e || (ey == e && y < c)));
+                    const double ty = bitsd(lane_u64(dbits(t), y));
+                    const double ey = bitsd(lane_u64(dbits(e), y));
+                    const bool before = ty < t || (ty == t && (ey < e || (ey == e && y < lane)));
                     if (before && ey <= e) k = false;
                 }
-                keep[c] = k;
-                kept_here += k;
-            }
-            __syncthreads();
-            int kept = kept_here;
-            for (int d = 32; d > 0; d >>= 1) kept += __shfl_xor(kept, d, 64);
-            if (kept > KR_DP_CELL_CAP || used + kept > arena) {
-                ok = false;
-                break;
-            }
-            for (int c = lane; c < C; c += 64) {
-                if (!keep[c]) continue;
-                const double t = cT[c];
-                int rank = 0;
+                uint64_t km = __ballot(k);
+                kept = __popcll(km);
+                if (kept > KR_DP_CELL_CAP || used + kept > arena) {
+                    ok = false;
+                    break;
+                }
+                int rank = 0;  // kept points are strictly ordered in time
+                while (km) {
+                    const int y = __ffsll((long long)km) - 1;
+                    km &= km - 1;
+                    rank += bitsd(lane_u64(dbits(t), y)) < t ? 1 : 0;
+                }
+                if (k) {
+                    arT[used + rank] = t;
+                    arE[used + rank] = e;
+                    arB[used + rank] = (int16_t)(lo * 64 + q);
+                }
+            } else {
+                if (allowed) {
+                    sT[r] = gT;
+                    sE[r] = gE;
+                    soff[r] = ex;
+                    sstart[r] = st;
+                    for (int q = 0; q < n_succ; ++q) csrc[ex + q] = (uint8_t)r;
+                }
+                if (lane == 0) soff[ns] = C;
+                wave_sync();
+                for (int c = lane; c < C; c += 64) {
+                    const int lo = csrc[c];
+                    const int q = c - soff[lo];
+                    cT[c] = sT[lo] + arT[sstart[lo] + q];
+                    cE[c] = sE[lo] + arE[sstart[lo] + q];
+                }
+                wave_sync();
+                int kept_here = 0;
+                for (int c = lane; c < C; c += 64) {
+                    const double t = cT[c], e = cE[c];
+                    bool k = true;
 #pragma unroll 4
-                for (int y = 0; y < C; ++y) rank += keep[y] && cT[y] < t;
-                const int lo = csrc[c];
-                arT[used + rank] = t;
-                arE[used + rank] = cE[c];
-                arB[used + rank] = (int16_t)(lo * 64 + (c - soff[lo]));
+                    for (int y = 0; y < C; ++y) {
+                        const double ty = cT[y], ey = cE[y];
+                        const bool before = ty < t || (ty == t && (ey < e || (ey == e && y < c)));
+                        if (before && ey <= e) k = false;
+                    }
+                    keep[c] = k;
+                    kept_here += k;
+                }
+                wave_sync();
+                kept = kept_here;
+                for (int d = 32; d > 0; d >>= 1) kept += __shfl_xor(kept, d, 64);
+                if (kept > KR_DP_CELL_CAP || used + kept > arena) {
+                    ok = false;
+                    break;
+                }
+                for (int c = lane; c < C; c += 64) {
+                    if (!keep[c]) continue;
+                    const double t = cT[c];
+                    int rank = 0;
+#pragma unroll 4
+                    for (int y = 0; y < C; ++y) rank += keep[y] && cT[y] < t;
+                    const int lo = csrc[c];
+                    arT[used + rank] = t;
+                    arE[used + rank] = cE[c];
+                    arB[used + rank] = (int16_t)(lo * 64 + (c - soff[lo]));
+                }
             }
             if (lane == 0) {
                 cstart[i * W + j] = (int16_t)used;
                 ccnt[i * W + j] = (int16_t)kept;
             }
             used += kept;
-            __syncthreads();
+            wave_sync();
         }
     }
     if (!ok) return false;
@@ -332,7 +398,7 @@ __global__ void __launch_bounds__(64) dp_retry_kernel(DpArgs a, int tier, int ar
             else
                 *a.status = KR_ECAPACITY;
         }
-        __syncthreads();
+        wave_sync();
     }
 }
 
