@@ -11,9 +11,10 @@
 //     and then the successor's order; their index is their generation order;
 //   * a candidate is kept iff no candidate before it in (T, E, index) order has energy at
 //     or below its own (GetFrontier with exact duplicates to the first), decided by
-//     comparing against every candidate through LDS broadcast reads (cells hold tens of
-//     candidates, so this beats sorting); a kept point's rank is the number of kept
-//     points with a smaller time;
+//     comparing against every candidate (cells hold tens of candidates, so this beats
+//     sorting): with at most 64 candidates one per lane, through lane reads; otherwise
+//     through LDS broadcast reads; a kept point's rank is the number of kept points
+//     with a smaller time;
 //   * the kept points go to an LDS arena with their back-pointer (source, point).
 // The schedules of P(0, 0) are then walked back one lane per point.
 #include <math.h>
