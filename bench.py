@@ -401,6 +401,32 @@ def main():
             "sample": "first %d of the 1024 eval-stress partitions (%d candidates), evaluate + "
                       "GetFrontier, single-threaded C oracle, %.1f s" % (n, n * sp.n_cand, el)}
         out["parity_check"] = {"partitions": n, "frontier_mismatches": mism}
+        # the same oracle, partition-parallel over the host's cores (ctypes calls release
+        # the interpreter lock), on the next partitions of the batch
+        import concurrent.futures as cfu
+
+        nthreads = os.cpu_count() or 1
+        first = min(n, sp.n_parts - 1)
+        t0 = time.perf_counter()
+        done = 0
+        with cfu.ThreadPoolExecutor(max_workers=nthreads) as ex:
+            futs = []
+            for q in range(first, sp.n_parts):
+                futs.append(ex.submit(oracle.evaluate_partition, sp, w.t, w.pw, w.tc, w.pc, q))
+                if len(futs) >= 4 * nthreads:
+                    futs.pop(0).result()
+                    done += 1
+                    if time.perf_counter() - t0 > args.cpu_seconds:
+                        break
+            for f in futs:
+                f.result()
+                done += 1
+        el = time.perf_counter() - t0
+        out["cpu_baseline_parallel"] = {
+            "value": done * sp.n_cand / el, "unit": "candidates/s", "cores": nthreads,
+            "kind": "oracle",
+            "sample": "%d eval-stress partitions (evaluation only), %d threads, %.1f s"
+                      % (done, nthreads, el)}
         t0 = time.perf_counter()
         oracle.compose(off4, T4, E4, B)
         el = time.perf_counter() - t0
