@@ -402,16 +402,15 @@ def main():
                       "GetFrontier, single-threaded C oracle, %.1f s" % (n, n * sp.n_cand, el)}
         out["parity_check"] = {"partitions": n, "frontier_mismatches": mism}
         # the same oracle, partition-parallel over the host's cores (ctypes calls release
-        # the interpreter lock), on the next partitions of the batch
+        # the interpreter lock), over the batch from its first partition
         import concurrent.futures as cfu
 
         nthreads = os.cpu_count() or 1
-        first = min(n, sp.n_parts - 1)
         t0 = time.perf_counter()
         done = 0
         with cfu.ThreadPoolExecutor(max_workers=nthreads) as ex:
             futs = []
-            for q in range(first, sp.n_parts):
+            for q in range(sp.n_parts):
                 futs.append(ex.submit(oracle.evaluate_partition, sp, w.t, w.pw, w.tc, w.pc, q))
                 if len(futs) >= 4 * nthreads:
                     futs.pop(0).result()
