@@ -94,3 +94,9 @@ def test_output_capacity(kr):
     kind1, kind2 = [0, 0, 1, 0, 0, 1], [0, 0, 1, 0, 0, 1]
     ops = _random_batch(rng, kind1, kind2, 16)
     _compare(kr, kind1, kind2, ops, 0.0, 4, "capacity 1", out_cap=1)
+
+
+def test_no_instances(kr):
+    ops = torch.zeros((0, 4, 4), dtype=torch.float64, device="cuda")
+    got = kr.launch_timing_frontier([0, 1], [0, 0], ops, I.P_STATIC_W, 2)
+    assert got.T.shape[0] == 0 and int(got.status.item()) == kr.KR_OK

@@ -252,3 +252,20 @@ def test_mbo_chain_eval_stress_sampled(kr):
     oracle on sampled partitions."""
     w = I.config_workload(3)
     _mbo_chain(kr, w, [0, 517, 1023])
+
+
+def test_empty_candidate_sets(kr):
+    """No candidates at all: HV and r still come from the measured points; the batch is
+    empty."""
+    cand_off = np.zeros(3, dtype=np.int64)
+    obs_off = np.array([0, 2, 5], dtype=np.int64)
+    To = np.array([1e-3, 2e-3, 1e-3, 3e-3, 2e-3])
+    Eo = np.array([0.5, 0.4, 0.9, 0.3, 0.6])
+    empty = torch.zeros(0, dtype=torch.float64, device="cuda")
+    got = kr.hvi_scores(cand_off, empty, empty, obs_off, _cuda(To), _cuda(Eo), I.P_STATIC_W)
+    _, rhv, rref = oracle.hvi(cand_off, np.zeros(0), np.zeros(0), obs_off, To, Eo, I.P_STATIC_W)
+    np.testing.assert_array_equal(got.hv.cpu().numpy(), rhv)
+    np.testing.assert_array_equal(got.ref.cpu().numpy(), rref)
+    b = kr.select_batch(cand_off, torch.zeros((3, 0), dtype=torch.float64, device="cuda"),
+                        empty, obs_off, np.array([0, 1, 0, 1, 2]), 13, 6, 6, 32)
+    assert all(len(x) == 0 for x in b.lists())
