@@ -11,7 +11,12 @@
  * microbatch/iteration frontier (Section 4.4, Algorithm 2) and selecting the
  * schedule behind a frontier point (Section 5.1).  This library runs that search
  * over the whole candidate space with a closed cost model fed by per-kernel time and
- * power tables, on one GPU.
+ * power tables, on one GPU.  Beside that path it provides:
+ *  - the microbatch frontier under Algorithm 2's rules (Section 4.4);
+ *  - the scores, batch selection and stopping rule of the multi-pass Bayesian
+ *    optimisation (Section 4.3, Algorithm 1);
+ *  - the launch-timing frontier of two operation sequences (Appendix B);
+ *  - the evaluation's frontier comparison metrics (Section 6.1).
  *
  * Conventions for every entry point
  *  - Array arguments are DEVICE pointers unless marked "host".  The caller owns and
