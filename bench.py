@@ -406,12 +406,17 @@ def main():
         import concurrent.futures as cfu
 
         nthreads = os.cpu_count() or 1
+
+        def one(q):
+            T, E = oracle.evaluate_partition(sp, w.t, w.pw, w.tc, w.pc, q)
+            return oracle.pareto(T, E)
+
         t0 = time.perf_counter()
         done = 0
         with cfu.ThreadPoolExecutor(max_workers=nthreads) as ex:
             futs = []
             for q in range(sp.n_parts):
-                futs.append(ex.submit(oracle.evaluate_partition, sp, w.t, w.pw, w.tc, w.pc, q))
+                futs.append(ex.submit(one, q))
                 if len(futs) >= 4 * nthreads:
                     futs.pop(0).result()
                     done += 1
@@ -424,7 +429,7 @@ def main():
         out["cpu_baseline_parallel"] = {
             "value": done * sp.n_cand / el, "unit": "candidates/s", "cores": nthreads,
             "kind": "oracle",
-            "sample": "%d eval-stress partitions (evaluation only), %d threads, %.1f s"
+            "sample": "%d eval-stress partitions, evaluate + GetFrontier, %d threads, %.1f s"
                       % (done, nthreads, el)}
         t0 = time.perf_counter()
         oracle.compose(off4, T4, E4, B)

@@ -40,6 +40,7 @@
  * Every floating-point line is one IEEE fp64 rounding in the written order; the file
  * must be compiled without FMA contraction and without fast-math.
  */
+#define _GNU_SOURCE /* qsort_r: reentrant sorts, so partitions may run on threads */
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
@@ -246,15 +247,16 @@ int oracle_evaluate(int N, int M, int F, int S, int n_pos, double p_static,
  * is kept.  Done as: sort by (T, E, index), keep a point iff its energy is strictly
  * below every energy before it.  Output is in ascending time.
  * ---------------------------------------------------------------------------- */
-static const double *g_T, *g_E;
+typedef struct { const double *T, *E; } te_ctx;
 
-static int cmp_tei(const void *a, const void *b)
+static int cmp_tei(const void *a, const void *b, void *ctx)
 {
+    const te_ctx *c = (const te_ctx *)ctx;
     int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
-    if (g_T[x] < g_T[y]) return -1;
-    if (g_T[x] > g_T[y]) return 1;
-    if (g_E[x] < g_E[y]) return -1;
-    if (g_E[x] > g_E[y]) return 1;
+    if (c->T[x] < c->T[y]) return -1;
+    if (c->T[x] > c->T[y]) return 1;
+    if (c->E[x] < c->E[y]) return -1;
+    if (c->E[x] > c->E[y]) return 1;
     return (x > y) - (x < y);
 }
 
@@ -264,9 +266,8 @@ int oracle_pareto(int64_t n, const double *T, const double *E, int32_t *out_idx,
     int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
     if (!order) return OR_EINVAL;
     for (int64_t k = 0; k < n; k++) order[k] = (int32_t)k;
-    g_T = T;
-    g_E = E;
-    qsort(order, (size_t)n, sizeof(int32_t), cmp_tei);
+    te_ctx ctx = {T, E};
+    qsort_r(order, (size_t)n, sizeof(int32_t), cmp_tei, &ctx);
     double best = INFINITY;
     int64_t kept = 0;
     for (int64_t k = 0; k < n; k++) {
@@ -873,13 +874,12 @@ int oracle_uncertainty(int M, int64_t n, const double *Tm, const double *Em, dou
  * skipped) to sel[g * k ...], its size to count[g].  score [3][n_cand], unc [n_cand].
  * Needs 0 <= k1, k2, k3, k1 + k2 + k3 <= k; any NaN score is an error.
  * ---------------------------------------------------------------------------- */
-static const double *g_s;
-
-static int cmp_score(const void *a, const void *b)
+static int cmp_score(const void *a, const void *b, void *ctx)
 {
+    const double *sc = (const double *)ctx;
     int64_t x = *(const int64_t *)a, y = *(const int64_t *)b;
-    if (g_s[x] > g_s[y]) return -1;
-    if (g_s[x] < g_s[y]) return 1;
+    if (sc[x] > sc[y]) return -1;
+    if (sc[x] < sc[y]) return 1;
     return (x > y) - (x < y);
 }
 
@@ -916,8 +916,7 @@ int oracle_select(int n_seg, const int64_t *cand_off, const double *score, const
             int64_t na = 0;
             for (int64_t x = 0; x < ng; x++)
                 if (!in_d[x] && !(pass == 3 && in_c[x])) a[na++] = x;
-            g_s = s;
-            qsort(a, (size_t)na, sizeof(int64_t), cmp_score);
+            qsort_r(a, (size_t)na, sizeof(int64_t), cmp_score, (void *)s);
             int64_t m = pass < 3 ? want[pass] : k - cnt;
             if (m > na) m = na;
             for (int64_t r = 0; r < m; r++) {
