@@ -314,6 +314,8 @@ size_t kr_compose_frontiers_workspace(int32_t n_parts, int32_t n_bins)
     c.take<double>(B);
     c.take<double>(B);
     c.take<double>(P * B);
+    c.take<double>((B + KR_ST_CHUNK - 1) / KR_ST_CHUNK);
+    c.take<int32_t>((B + KR_ST_CHUNK - 1) / KR_ST_CHUNK);
     return c.used;
 }
 
@@ -347,6 +349,8 @@ kr_status kr_compose_frontiers(int32_t n_parts, const int64_t *off, const double
     w.F0 = c.take<double>(B);
     w.F1 = c.take<double>(B);
     w.Fh = c.take<double>(P * B);
+    w.chmin = c.take<double>((B + KR_ST_CHUNK - 1) / KR_ST_CHUNK);
+    w.chcnt = c.take<int32_t>((B + KR_ST_CHUNK - 1) / KR_ST_CHUNK);
     ComposeArgs a;
     a.P = n_parts;
     a.B = n_bins;

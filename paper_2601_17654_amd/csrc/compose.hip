@@ -737,48 +737,104 @@ __device__ __forceinline__ T block_scan_excl(T v, T identity, Op op, T *lds, T *
     return op(before, ex);
 }
 
-// Bins whose value is strictly below every earlier bin.  One block: thread t takes a
-// contiguous chunk of bins; a scan of the chunk minima gives each chunk the least value
-// before it, a scan of the keep counts gives the output positions.
-#define KR_ST_NT 1024
-__global__ void __launch_bounds__(KR_ST_NT) staircase_kernel(ComposeArgs a)
+// Bins whose value is strictly below every earlier bin, in three passes over chunks of
+// KR_ST_CHUNK bins, one block each: the least value of every chunk; then per chunk the
+// least value before it (from the chunk minima), a prefix-minimum scan inside it and
+// its count of kept bins; then the output position from the counts before it, and the
+// writes.  Thread t holds bins 4t .. 4t + 3 of its chunk.
+#define KR_ST_NT 256
+
+__device__ __forceinline__ double st_bin(const ComposeArgs &a, int b)
+{
+    return b < a.B ? a.F_out[b] : INFINITY;
+}
+
+__global__ void __launch_bounds__(KR_ST_NT) staircase_min_kernel(ComposeArgs a, ComposeWs w)
+{
+    __shared__ double sm[KR_ST_NT / 64];
+    const int base = blockIdx.x * KR_ST_CHUNK;
+    double m = INFINITY;
+#pragma unroll
+    for (int q = 0; q < KR_ST_CHUNK / KR_ST_NT; ++q)
+        m = MinF64()(m, st_bin(a, base + q * KR_ST_NT + threadIdx.x));
+    double tot;
+    block_scan_excl<KR_ST_NT>(m, (double)INFINITY, MinF64(), sm, &tot);
+    if (threadIdx.x == 0) w.chmin[blockIdx.x] = tot;
+}
+
+// Least value before this chunk, and this thread's kept bins (bit q: bin 4t + q).
+__device__ __forceinline__ uint32_t st_keep(const ComposeArgs &a, const ComposeWs &w,
+                                            double *sm, double (&v)[4])
+{
+    double before = INFINITY;
+    for (int c = threadIdx.x; c < (int)blockIdx.x; c += KR_ST_NT)
+        before = MinF64()(before, w.chmin[c]);
+    double tot;
+    block_scan_excl<KR_ST_NT>(before, (double)INFINITY, MinF64(), sm, &tot);
+    const int b0 = blockIdx.x * KR_ST_CHUNK + 4 * threadIdx.x;
+    double tm = INFINITY;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        v[q] = st_bin(a, b0 + q);
+        tm = MinF64()(tm, v[q]);
+    }
+    double run = block_scan_excl<KR_ST_NT>(tm, (double)INFINITY, MinF64(), sm, &before);
+    run = MinF64()(run, tot);
+    uint32_t k = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+        if (v[q] < run) {
+            k |= 1u << q;
+            run = v[q];
+        }
+    return k;
+}
+
+__global__ void __launch_bounds__(KR_ST_NT) staircase_count_kernel(ComposeArgs a, ComposeWs w)
 {
     __shared__ double sm[KR_ST_NT / 64];
     __shared__ int32_t si[KR_ST_NT / 64];
-    if (*a.status != KR_OK) {
-        if (threadIdx.x == 0) *a.n_stair = 0;
-        return;
-    }
-    const double delta = a.info[0], tmin_sum = a.info[1];
-    const int C = (a.B + KR_ST_NT - 1) / KR_ST_NT;
-    const int b0 = min(a.B, (int)threadIdx.x * C), b1 = min(a.B, b0 + C);
-    double cmin = INFINITY;
-    for (int b = b0; b < b1; ++b) cmin = MinF64()(cmin, a.F_out[b]);
-    double tot;
-    double run = block_scan_excl<KR_ST_NT>(cmin, (double)INFINITY, MinF64(), sm, &tot);
-    const double run0 = run;
-    int32_t nk = 0;
-    for (int b = b0; b < b1; ++b) {
-        const double v = a.F_out[b];
-        if (v < run) {
-            ++nk;
-            run = v;
-        }
-    }
+    double v[4];
+    const uint32_t k = st_keep(a, w, sm, v);
     int32_t n;
-    int32_t pos = block_scan_excl<KR_ST_NT>(nk, 0, SumI32(), si, &n);
-    run = run0;
-    for (int b = b0; b < b1; ++b) {
-        const double v = a.F_out[b];
-        if (v < run) {
-            a.stair_bin[pos] = b;
-            a.stair_Tlo[pos] = tmin_sum + (double)b * delta;
-            a.stair_E[pos] = v;
-            ++pos;
-            run = v;
-        }
+    block_scan_excl<KR_ST_NT>((int32_t)__popc(k), 0, SumI32(), si, &n);
+    if (threadIdx.x == 0) w.chcnt[blockIdx.x] = n;
+}
+
+__global__ void __launch_bounds__(KR_ST_NT) staircase_write_kernel(ComposeArgs a, ComposeWs w)
+{
+    __shared__ double sm[KR_ST_NT / 64];
+    __shared__ int32_t si[KR_ST_NT / 64];
+    const int nb = gridDim.x;
+    int32_t before = 0, all = 0;
+    for (int c = threadIdx.x; c < nb; c += KR_ST_NT) {
+        const int32_t x = w.chcnt[c];
+        if (c < (int)blockIdx.x) before += x;
+        all += x;
     }
-    if (threadIdx.x == 0) *a.n_stair = n;
+    int32_t tb, ta;
+    block_scan_excl<KR_ST_NT>(before, 0, SumI32(), si, &tb);
+    block_scan_excl<KR_ST_NT>(all, 0, SumI32(), si, &ta);
+    double v[4];
+    const uint32_t k = st_keep(a, w, sm, v);
+    int32_t n;
+    int32_t pos = tb + block_scan_excl<KR_ST_NT>((int32_t)__popc(k), 0, SumI32(), si, &n);
+    const double delta = a.info[0], tmin_sum = a.info[1];
+    const int b0 = blockIdx.x * KR_ST_CHUNK + 4 * threadIdx.x;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+        if (k >> q & 1u) {
+            a.stair_bin[pos] = b0 + q;
+            a.stair_Tlo[pos] = tmin_sum + (double)(b0 + q) * delta;
+            a.stair_E[pos] = v[q];
+            ++pos;
+        }
+    if (blockIdx.x == 0 && threadIdx.x == 0) *a.n_stair = ta;
+}
+
+__global__ void staircase_skip_kernel(ComposeArgs a)
+{
+    if (*a.status != KR_OK) *a.n_stair = 0;
 }
 
 // Whether G wavefront blocks can all be resident at once on the current device (a
@@ -835,7 +891,13 @@ hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipEvent_t *
         }
         if (minplus_ev) (void)hipEventRecord(minplus_ev[1], st);
     }
-    hipLaunchKernelGGL(staircase_kernel, dim3(1), dim3(KR_ST_NT), 0, st, a);
+    {
+        const int nb = (a.B + KR_ST_CHUNK - 1) / KR_ST_CHUNK;
+        hipLaunchKernelGGL(staircase_min_kernel, dim3(nb), dim3(KR_ST_NT), 0, st, a, w);
+        hipLaunchKernelGGL(staircase_count_kernel, dim3(nb), dim3(KR_ST_NT), 0, st, a, w);
+        hipLaunchKernelGGL(staircase_write_kernel, dim3(nb), dim3(KR_ST_NT), 0, st, a, w);
+        hipLaunchKernelGGL(staircase_skip_kernel, dim3(1), dim3(1), 0, st, a);
+    }
     return hipGetLastError();
 }
 

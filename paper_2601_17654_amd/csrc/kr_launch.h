@@ -99,7 +99,10 @@ struct ComposeWs {
     int32_t *occ;          // [P]
     double *F0, *F1;       // [B]
     double *Fh;            // [P][B] step history of the wavefront min-plus (or null)
+    double *chmin;         // [ceil(B / KR_ST_CHUNK)] least value of each staircase chunk
+    int32_t *chcnt;        // [ceil(B / KR_ST_CHUNK)] staircase bins of each chunk
 };
+#define KR_ST_CHUNK 1024   // bins per block of the staircase passes
 struct ComposeArgs {
     int P, B;
     double delta_in;
