@@ -80,14 +80,44 @@ __global__ void __launch_bounds__(KR_BLOCK) compose_range_kernel(ComposeArgs a, 
 // reductions and scans (exact).
 __global__ void __launch_bounds__(KR_BLOCK) compose_setup_kernel(ComposeArgs a, ComposeWs w)
 {
+    constexpr int kChunk = 1024;
     __shared__ double s_delta, s_tsum;
+    __shared__ double s_range[kChunk], s_tmin[kChunk];
     __shared__ int64_t sc[KR_WAVES];
     if (*a.status != KR_OK) return;
     const int P = a.P, B = a.B;
+    // the sums in partition order, by thread 0 from LDS copies the block loads together
+    double R = 0.0, tmin_sum = 0.0;
+    for (int k0 = 0; k0 < P; k0 += kChunk) {
+        const int n = min(kChunk, P - k0);
+        for (int k = threadIdx.x; k < n; k += KR_BLOCK) {
+            s_range[k] = w.range[k0 + k];
+            s_tmin[k] = w.tmin[k0 + k];
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            int k = 0;
+            for (; k + 8 <= n; k += 8) {
+                double r8[8], t8[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    r8[q] = s_range[k + q];
+                    t8[q] = s_tmin[k + q];
+                }
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    R = R + r8[q];
+                    tmin_sum = tmin_sum + t8[q];
+                }
+            }
+            for (; k < n; ++k) {
+                R = R + s_range[k];
+                tmin_sum = tmin_sum + s_tmin[k];
+            }
+        }
+        __syncthreads();
+    }
     if (threadIdx.x == 0) {
-        double R = 0.0, tmin_sum = 0.0;
-        for (int k = 0; k < P; ++k) R = R + w.range[k];
-        for (int k = 0; k < P; ++k) tmin_sum = tmin_sum + w.tmin[k];
         s_delta = a.delta_in > 0.0 ? a.delta_in : (R > 0.0 ? R / (double)(B - 1) : 1.0);
         s_tsum = tmin_sum;
     }
