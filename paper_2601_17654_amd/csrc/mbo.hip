@@ -447,16 +447,25 @@ __global__ void __launch_bounds__(KR_BLOCK) sel_tile_kernel(SelArgs a)
         cnt[p] = 0;
     }
     constexpr int kPerWave = KR_SEL_TILE / KR_WAVES;
+    constexpr int kRows = kPerWave / 64, kRowBits = __builtin_ctz(kRows);
+    static_assert((kRows & (kRows - 1)) == 0, "rows per wave must be a power of two");
     const int64_t w0 = l0 + (int64_t)wave * kPerWave;  // this wave's first local index
+    // Rows of 64 candidates are visited in bit-reversed order.  Scores trend along the
+    // index (it runs over frequencies slowest), and in index order late rows would keep
+    // beating the list's last entry and force merges; the result does not depend on the
+    // order, since (score, index) is a total order.
+    auto row = [&](int r) { return w0 + (int64_t)(__brev((uint32_t)r) >> (32 - kRowBits)) * 64 + lane; };
     bool nan_seen = false;
     double cur[4], nxt[4];
+    int64_t xn = row(0);
 #pragma unroll
-    for (int p = 0; p < 4; ++p) cur[p] = p < np && w0 + lane < l1 ? src[p][w0 + lane] : 0.0;
-    for (int i = 0; i < kPerWave; i += 64) {
-        const int64_t x = w0 + i + lane;
+    for (int p = 0; p < 4; ++p) cur[p] = p < np && xn < l1 ? src[p][xn] : 0.0;
+    for (int r = 0; r < kRows; ++r) {
+        const int64_t x = xn;
+        xn = row(r + 1 < kRows ? r + 1 : r);
 #pragma unroll
         for (int p = 0; p < 4; ++p)
-            nxt[p] = p < np && i + 64 < kPerWave && x + 64 < l1 ? src[p][x + 64] : 0.0;
+            nxt[p] = p < np && r + 1 < kRows && xn < l1 ? src[p][xn] : 0.0;
         const int64_t off = x - l0;
         const bool in = x < l1 && !((excl[(off >> 5) & (KR_SEL_TILE / 32 - 1)] >> (off & 31)) & 1u);
 #pragma unroll
