@@ -184,8 +184,8 @@ __global__ void __launch_bounds__(KR_BLOCK) hvi_score_kernel(HviArgs a)
 #pragma unroll
         for (int j = 0; j < kPer; ++j) {
             const int64_t x = x0 + tid + (int64_t)j * KR_BLOCK;
-            t[j] = x < x1 ? a.T_hat[x] : 0.0;
-            e[j] = x < x1 ? a.E_hat[x] : 0.0;
+            t[j] = x < x1 ? __builtin_nontemporal_load(a.T_hat + x) : 0.0;
+            e[j] = x < x1 ? __builtin_nontemporal_load(a.E_hat + x) : 0.0;
         }
 #pragma unroll
         for (int j = 0; j < kPer; ++j) {
@@ -196,7 +196,7 @@ __global__ void __launch_bounds__(KR_BLOCK) hvi_score_kernel(HviArgs a)
                 const double h = bad ? NAN
                                      : hvi_one(fT[v], fE[v], s[v], rT, rE[v], t[j],
                                                energy_variant(v, t[j], e[j], a.p_static));
-                a.hvi[(int64_t)v * a.n_cand + x] = h;
+                __builtin_nontemporal_store(h, a.hvi + (int64_t)v * a.n_cand + x);
             }
         }
     }
@@ -239,8 +239,8 @@ __global__ void __launch_bounds__(KR_BLOCK) unc_kernel(int M_rt, int64_t n, cons
             for (int j = 0; j < 2; ++j)
 #pragma unroll
                 for (int m = 0; m < MC; ++m) {
-                    t[j][m] = Tm[(int64_t)m * n + xs[j]];
-                    e[j][m] = Em[(int64_t)m * n + xs[j]];
+                    t[j][m] = __builtin_nontemporal_load(Tm + (int64_t)m * n + xs[j]);
+                    e[j][m] = __builtin_nontemporal_load(Em + (int64_t)m * n + xs[j]);
                 }
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
@@ -258,7 +258,8 @@ __global__ void __launch_bounds__(KR_BLOCK) unc_kernel(int M_rt, int64_t n, cons
                     vt = vt + dt * dt;
                     ve = ve + de * de;
                 }
-                if (j == 0 || x + stride < n) unc[xs[j]] = sqrt(vt / M) + sqrt(ve / M);
+                if (j == 0 || x + stride < n)
+                    __builtin_nontemporal_store(sqrt(vt / M) + sqrt(ve / M), unc + xs[j]);
             }
         }
         return;
@@ -459,13 +460,13 @@ __global__ void __launch_bounds__(KR_BLOCK) sel_tile_kernel(SelArgs a)
     double cur[4], nxt[4];
     int64_t xn = row(0);
 #pragma unroll
-    for (int p = 0; p < 4; ++p) cur[p] = p < np && xn < l1 ? src[p][xn] : 0.0;
+    for (int p = 0; p < 4; ++p) cur[p] = p < np && xn < l1 ? __builtin_nontemporal_load(src[p] + xn) : 0.0;
     for (int r = 0; r < kRows; ++r) {
         const int64_t x = xn;
         xn = row(r + 1 < kRows ? r + 1 : r);
 #pragma unroll
         for (int p = 0; p < 4; ++p)
-            nxt[p] = p < np && r + 1 < kRows && xn < l1 ? src[p][xn] : 0.0;
+            nxt[p] = p < np && r + 1 < kRows && xn < l1 ? __builtin_nontemporal_load(src[p] + xn) : 0.0;
         const int64_t off = x - l0;
         const bool in = x < l1 && !((excl[(off >> 5) & (KR_SEL_TILE / 32 - 1)] >> (off & 31)) & 1u);
 #pragma unroll
