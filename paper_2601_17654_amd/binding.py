@@ -319,17 +319,59 @@ class Microbatch:
         self.T, self.E, self.f, self.choice = T, E, f, choice
 
 
+@dataclasses.dataclass
+class MicrobatchBuffers:
+    """Caller-kept buffers of a microbatch call: outputs of capacity `cap`, the device
+    point count n [1] and status [1], and the device copy of seg_off.  A call given them
+    allocates nothing and copies nothing from the host; with check=False it also reads
+    nothing back, so it only enqueues work on the stream.  Results of a checked call are
+    views into the buffers, valid until the buffers are used again."""
+    T: torch.Tensor
+    E: torch.Tensor
+    f: torch.Tensor
+    choice: torch.Tensor
+    n: torch.Tensor
+    status: torch.Tensor
+    seg: torch.Tensor
+    seg_host: np.ndarray
+
+
+def microbatch_buffers(seg_off, n_types: int, cap: int) -> MicrobatchBuffers:
+    """Buffers for microbatch_frontier / microbatch_enumerate calls on segments seg_off
+    (host) with output capacity cap."""
+    seg_host = np.ascontiguousarray(np.asarray(seg_off, dtype=np.int64))
+    c = max(int(cap), 1)
+    return MicrobatchBuffers(
+        torch.empty(c, dtype=torch.float64, device="cuda"),
+        torch.empty(c, dtype=torch.float64, device="cuda"),
+        torch.empty(c, dtype=torch.int32, device="cuda"),
+        torch.empty((c, n_types), dtype=torch.int32, device="cuda"),
+        torch.empty(1, dtype=torch.int64, device="cuda"),
+        torch.empty(1, dtype=torch.int32, device="cuda"),
+        torch.from_numpy(seg_host.copy()).cuda(), seg_host)
+
+
+def _mb_buffers(out, seg_host, n_types, c):
+    if out is None:
+        return microbatch_buffers(seg_host, n_types, c)
+    if (out.T.numel() < max(c, 1) or out.choice.shape[1] != n_types
+            or not np.array_equal(out.seg_host, seg_host)):
+        raise ValueError("buffers were made for another shape, capacity or seg_off")
+    return out
+
+
 def microbatch_frontier(seg_off, T, E, n_types: int, n_freq: int, seq, comp_T=None, comp_E=None,
-                        n_bins: int = 4096, cap: Optional[int] = None) -> Microbatch:
+                        n_bins: int = 4096, cap: Optional[int] = None, check: bool = True,
+                        out: Optional[MicrobatchBuffers] = None):
     """Microbatch frontier of Algorithm 2 (one frequency per microbatch, one configuration
     per partition type).  seg_off [K*F+1] (segment t*F+f = type t's points at frequency f),
-    seq: host list of partition types in execution order, comp_T/comp_E [n_comp][F]."""
+    seq: host list of partition types in execution order, comp_T/comp_E [n_comp][F].
+    With check=False the buffers are returned untrimmed (out.n holds the count)."""
     seg_host = np.asarray(seg_off.cpu() if isinstance(seg_off, torch.Tensor) else seg_off,
                           dtype=np.int64)
     if len(seg_host) != n_types * n_freq + 1:
         raise ValueError("seg_off must have n_types * n_freq + 1 entries")
     n_points = int(seg_host[-1])
-    seg_dev = torch.from_numpy(seg_host).cuda()
     T = _dev(T, torch.float64, "T").reshape(-1)
     E = _dev(E, torch.float64, "E").reshape(-1)
     seq_h = np.ascontiguousarray(np.asarray(seq, dtype=np.int32))
@@ -340,27 +382,29 @@ def microbatch_frontier(seg_off, T, E, n_types: int, n_freq: int, seq, comp_T=No
         cE = _dev(comp_E, torch.float64, "comp_E").reshape(-1, n_freq)
         n_comp = cT.shape[0]
     c = int(cap) if cap is not None else n_freq * n_bins
-    oT = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
-    oE = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
-    of = torch.empty(max(c, 1), dtype=torch.int32, device="cuda")
-    och = torch.empty((max(c, 1), n_types), dtype=torch.int32, device="cuda")
-    n = torch.empty(1, dtype=torch.int64, device="cuda")
+    out = _mb_buffers(out, seg_host, n_types, c)
     wsb = _lib.kr_microbatch_frontier_workspace(n_types, n_freq, n_points, len(seq_h), n_bins)
     if wsb == 0:
         raise ValueError("unsupported microbatch shape")
     ws = _workspace(wsb)
     _check("kr_microbatch_frontier",
-           _lib.kr_microbatch_frontier(n_types, n_freq, _ptr(seg_dev), _ptr(T), _ptr(E), n_points,
+           _lib.kr_microbatch_frontier(n_types, n_freq, _ptr(out.seg), _ptr(T), _ptr(E), n_points,
                                        len(seq_h), seq_h.ctypes.data_as(ctypes.c_void_p), n_comp,
-                                       _ptr(cT), _ptr(cE), n_bins, c, _ptr(oT), _ptr(oE), _ptr(of),
-                                       _ptr(och), _ptr(n), _ptr(ws), wsb, _stream()))
-    k = min(int(n.item()), c)
-    return Microbatch(oT[:k], oE[:k], of[:k], och[:k])
+                                       _ptr(cT), _ptr(cE), n_bins, c, _ptr(out.T), _ptr(out.E),
+                                       _ptr(out.f), _ptr(out.choice), _ptr(out.n), _ptr(ws), wsb,
+                                       _stream()))
+    if not check:
+        return out
+    k = min(int(out.n.item()), c)
+    return Microbatch(out.T[:k], out.E[:k], out.f[:k], out.choice[:k])
 
 
 def microbatch_enumerate(seg_off, T, E, n_types: int, n_freq: int, seq, comp_T=None,
-                         comp_E=None, cap: Optional[int] = None) -> Microbatch:
-    """Microbatch frontier by enumerating every configuration (Algorithm 2 as written)."""
+                         comp_E=None, cap: Optional[int] = None, check: bool = True,
+                         out: Optional[MicrobatchBuffers] = None):
+    """Microbatch frontier by enumerating every configuration (Algorithm 2 as written).
+    With check=False the buffers are returned untrimmed and the status is not read
+    (out.n holds the count, out.status the status)."""
     seg_host = np.asarray(seg_off.cpu() if isinstance(seg_off, torch.Tensor) else seg_off,
                           dtype=np.int64)
     if len(seg_host) != n_types * n_freq + 1:
@@ -369,7 +413,6 @@ def microbatch_enumerate(seg_off, T, E, n_types: int, n_freq: int, seq, comp_T=N
     sizes = np.diff(seg_host).reshape(n_types, n_freq)
     used = sorted(set(seq_h.tolist()))
     n_configs = max(int(np.sum(np.prod(sizes[used], axis=0))), 1)
-    seg_dev = torch.from_numpy(seg_host).cuda()
     T = _dev(T, torch.float64, "T").reshape(-1)
     E = _dev(E, torch.float64, "E").reshape(-1)
     if comp_T is None:
@@ -379,27 +422,24 @@ def microbatch_enumerate(seg_off, T, E, n_types: int, n_freq: int, seq, comp_T=N
         cE = _dev(comp_E, torch.float64, "comp_E").reshape(-1, n_freq)
         n_comp = cT.shape[0]
     c = int(cap) if cap is not None else n_configs
-    oT = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
-    oE = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
-    of = torch.empty(max(c, 1), dtype=torch.int32, device="cuda")
-    och = torch.empty((max(c, 1), n_types), dtype=torch.int32, device="cuda")
-    n = torch.empty(1, dtype=torch.int64, device="cuda")
-    status = torch.empty(1, dtype=torch.int32, device="cuda")
+    out = _mb_buffers(out, seg_host, n_types, c)
     wsb = _lib.kr_microbatch_enumerate_workspace(n_types, n_freq, n_configs)
     if wsb == 0:
         raise ValueError("unsupported microbatch shape")
     ws = _workspace(wsb)
     _check("kr_microbatch_enumerate",
-           _lib.kr_microbatch_enumerate(n_types, n_freq, _ptr(seg_dev), _ptr(T), _ptr(E),
+           _lib.kr_microbatch_enumerate(n_types, n_freq, _ptr(out.seg), _ptr(T), _ptr(E),
                                         len(seq_h), seq_h.ctypes.data_as(ctypes.c_void_p),
-                                        n_comp, _ptr(cT), _ptr(cE), n_configs, c, _ptr(oT),
-                                        _ptr(oE), _ptr(of), _ptr(och), _ptr(n), _ptr(status),
-                                        _ptr(ws), wsb, _stream()))
-    st = int(status.item())
+                                        n_comp, _ptr(cT), _ptr(cE), n_configs, c, _ptr(out.T),
+                                        _ptr(out.E), _ptr(out.f), _ptr(out.choice), _ptr(out.n),
+                                        _ptr(out.status), _ptr(ws), wsb, _stream()))
+    if not check:
+        return out
+    st = int(out.status.item())
     if st != KR_OK:
         raise KrError("kr_microbatch_enumerate", st)
-    k = min(int(n.item()), c)
-    return Microbatch(oT[:k], oE[:k], of[:k], och[:k])
+    k = min(int(out.n.item()), c)
+    return Microbatch(out.T[:k], out.E[:k], out.f[:k], out.choice[:k])
 
 
 def decode_candidates(space, idx):

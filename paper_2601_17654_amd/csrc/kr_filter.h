@@ -69,6 +69,13 @@ struct FilterLds {
     FilterShared *sh;
     uint64_t *sT, *sE;  // [KR_SURV_CAP] survivors
     int32_t *sI;
+    // Optional room for big_cap survivors, sorted there when more than KR_SURV_CAP beat
+    // the first point; with none, `defer` returns -1 for such a tile instead of taking
+    // one block-wide minimum per kept point.
+    uint64_t *bT = nullptr, *bE = nullptr;
+    int32_t *bI = nullptr;
+    int big_cap = 0;
+    bool defer = false;
 };
 
 // Block-wide lexicographic minimum (one barrier; the two slot sets alternate so
@@ -90,8 +97,13 @@ __device__ inline Key block_min_key(const Key &k, FilterShared *sh, int &parity)
     return b;
 }
 
+__device__ inline void lds_sort_keys(uint64_t *sT, uint64_t *sE, int32_t *sI, int n);
+__device__ inline int lds_frontier_scan(const uint64_t *sT, const uint64_t *sE, const int32_t *sI,
+                                        int n, double *oT, double *oE, int32_t *oI);
+
 // Frontier of the block's points (slots k < CAP with ok[k]) written in ascending T to
-// oT/oE/oI[0 .. n); returns n in every thread.  Every thread of the block must call.
+// oT/oE/oI[0 .. n); returns n in every thread (-1 for a tile deferred as described in
+// FilterLds).  Every thread of the block must call.
 template <int CAP>
 __device__ inline int tile_frontier(const double (&vT)[CAP], const double (&vE)[CAP],
                                     const int32_t (&vI)[CAP], const bool (&ok)[CAP],
@@ -168,6 +180,27 @@ __device__ inline int tile_frontier(const double (&vT)[CAP], const double (&vE)[
         lds_barrier();
         return L.sh->nemit;
     }
+    if (total <= L.big_cap) {
+        // Many survivors: sort them in (T, E, index) order and keep each one whose E is
+        // below every earlier survivor's.  Points that are not survivors have E at or
+        // above A's and A precedes them all, so they can neither be kept nor matter.
+#pragma unroll
+        for (int k = 0; k < CAP; ++k) {
+            const bool sv = ok[k] && dbits(vE[k]) < A.e;
+            const uint64_t m = __ballot(sv);
+            if (sv) {
+                const int pos = base + __popcll(m & below);
+                L.bT[pos] = dbits(vT[k]);
+                L.bE[pos] = dbits(vE[k]);
+                L.bI[pos] = vI[k];
+            }
+            base += __popcll(m);
+        }
+        __syncthreads();
+        lds_sort_keys(L.bT, L.bE, L.bI, total);
+        return 1 + lds_frontier_scan(L.bT, L.bE, L.bI, total, oT + 1, oE + 1, oI + 1);
+    }
+    if (L.defer) return -1;
     // many survivors: repeat the block-wide minimum over the registers
     uint64_t bound = A.e;
     int n = 1;

@@ -77,14 +77,20 @@ __device__ __forceinline__ int find_segment(const int64_t *unit_base, int n_seg,
     return lo;
 }
 
-// Exact frontier of one tile of up to 2,048 consecutive points of a segment.
+// Exact frontier of one tile of up to KR_TILE consecutive points of a segment.  The
+// first pass holds KR_SURV_CAP survivors in LDS and defers (count -1) a tile with more;
+// the second pass takes only deferred tiles, with LDS for the whole tile, and sorts
+// their survivors.
+template <bool BIG>
 __global__ void __launch_bounds__(KR_BLOCK)
 pareto_tile_kernel(const double *T, const double *E, SegLayout L, UnitOut o)
 {
+    static_assert(KR_TILE == 8 * KR_BLOCK, "a tile is 8 points per thread");
     extern __shared__ double tile_lds[];
     __shared__ FilterShared fsh;
     const int64_t w = blockIdx.x;
     if (w >= L.unit_base[L.n_seg]) return;
+    if (BIG && o.cnt[w] >= 0) return;  // done by the first pass
     const int g = find_segment(L.unit_base, L.n_seg, w);
     const int64_t s0 = L.seg_off[g];
     const int64_t start = s0 + (w - L.unit_base[g]) * L.unit_stride;
@@ -94,6 +100,14 @@ pareto_tile_kernel(const double *T, const double *E, SegLayout L, UnitOut o)
     fl.sT = (uint64_t *)tile_lds;
     fl.sE = fl.sT + KR_SURV_CAP;
     fl.sI = (int32_t *)(fl.sE + KR_SURV_CAP);
+    if (BIG) {
+        fl.bT = (uint64_t *)tile_lds;
+        fl.bE = fl.bT + KR_TILE;
+        fl.bI = (int32_t *)(fl.bE + KR_TILE);
+        fl.big_cap = KR_TILE;
+    } else {
+        fl.defer = true;
+    }
     double vT[8], vE[8];
     int32_t vI[8];
     bool ok[8];
@@ -115,9 +129,11 @@ hipError_t launch_pareto_tiles(const double *T, const double *E, const SegLayout
                                int64_t n_units_bound, const UnitOut &o, hipStream_t st)
 {
     if (n_units_bound == 0) return hipSuccess;
-    const size_t lds = (size_t)KR_SURV_CAP * 20;
-    hipLaunchKernelGGL(pareto_tile_kernel, dim3((unsigned)n_units_bound), dim3(KR_BLOCK), lds, st,
-                       T, E, L, o);
+    const size_t lds = (size_t)KR_SURV_CAP * 20, lds_big = (size_t)KR_TILE * 20;
+    hipLaunchKernelGGL(pareto_tile_kernel<false>, dim3((unsigned)n_units_bound), dim3(KR_BLOCK),
+                       lds, st, T, E, L, o);
+    hipLaunchKernelGGL(pareto_tile_kernel<true>, dim3((unsigned)n_units_bound), dim3(KR_BLOCK),
+                       lds_big, st, T, E, L, o);
     return hipGetLastError();
 }
 

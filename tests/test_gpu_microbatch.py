@@ -124,3 +124,48 @@ def test_microbatch_llama_layers(kr):
     assert n > 10
     assert _compare_exact(kr, rseg, np.array(rT), np.array(rE), K, F, seq, cT, cE,
                           "llama layers") > 10
+
+
+def test_microbatch_kept_buffers(kr):
+    """Calls given kept buffers and check=False return the same points as the default
+    calls, also when the buffers are used again with other inputs of the same shape."""
+    rng = np.random.default_rng(41)
+    K, F, B = 3, 4, 512
+    seq = [0, 1, 2, 1, 0]
+    seg_off, T, E = _random_case(rng, K, F, 6)
+    cT = rng.uniform(1e-4, 5e-4, (2, F))
+    cE = rng.uniform(0.05, 0.2, (2, F))
+    cT_d, cE_d = torch.from_numpy(cT).cuda(), torch.from_numpy(cE).cuda()
+    sizes = np.diff(seg_off).reshape(K, F)
+    n_cfg = int(np.sum(np.prod(sizes, axis=0)))
+    gbuf = kr.microbatch_buffers(seg_off, K, F * B)
+    xbuf = kr.microbatch_buffers(seg_off, K, n_cfg)
+    for rep in range(2):
+        T2 = T * (1.0 + 0.25 * rep)
+        T_d, E_d = torch.from_numpy(T2).cuda(), torch.from_numpy(E).cuda()
+        ref = kr.microbatch_frontier(seg_off, T_d, E_d, K, F, seq, cT_d, cE_d, n_bins=B)
+        got = kr.microbatch_frontier(seg_off, T_d, E_d, K, F, seq, cT_d, cE_d, n_bins=B,
+                                     check=False, out=gbuf)
+        n = int(got.n.item())
+        assert n == ref.T.numel()
+        np.testing.assert_array_equal(got.T[:n].cpu().numpy(), ref.T.cpu().numpy())
+        np.testing.assert_array_equal(got.E[:n].cpu().numpy(), ref.E.cpu().numpy())
+        np.testing.assert_array_equal(got.choice[:n].cpu().numpy(), ref.choice.cpu().numpy())
+        refx = kr.microbatch_enumerate(seg_off, T_d, E_d, K, F, seq, cT_d, cE_d)
+        gotx = kr.microbatch_enumerate(seg_off, T_d, E_d, K, F, seq, cT_d, cE_d, check=False,
+                                       out=xbuf)
+        assert int(gotx.status.item()) == kr.KR_OK
+        n = int(gotx.n.item())
+        assert n == refx.T.numel()
+        np.testing.assert_array_equal(gotx.T[:n].cpu().numpy(), refx.T.cpu().numpy())
+        np.testing.assert_array_equal(gotx.f[:n].cpu().numpy(), refx.f.cpu().numpy())
+        np.testing.assert_array_equal(gotx.choice[:n].cpu().numpy(), refx.choice.cpu().numpy())
+        # and the checked call on the kept buffers trims as the default one does
+        chk = kr.microbatch_enumerate(seg_off, T_d, E_d, K, F, seq, cT_d, cE_d, out=xbuf)
+        np.testing.assert_array_equal(chk.E.cpu().numpy(), refx.E.cpu().numpy())
+    # buffers made for other segments are refused
+    seg2, T3, E3 = _random_case(np.random.default_rng(42), K, F, 6)
+    assert not np.array_equal(seg2, seg_off)
+    with pytest.raises(ValueError):
+        kr.microbatch_enumerate(seg2, torch.from_numpy(T3).cuda(), torch.from_numpy(E3).cuda(),
+                                K, F, seq, cT_d, cE_d, out=xbuf)
