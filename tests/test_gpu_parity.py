@@ -224,6 +224,31 @@ def test_pareto_filter(kr, oracle_lib, kind):
         check_frontier(fr, g, (ix, Tg[ix], Eg[ix]), "%s seg %d (n=%d)" % (kind, g, lens[g]))
 
 
+@pytest.mark.parametrize("n_below", [0, 1, 255, 256, 257, 1000, 2047])
+def test_pareto_filter_tile_survivor_paths(kr, oracle_lib, n_below):
+    """One 2,048-point tile whose least-time point A has n_below points with lower energy.
+    Up to 256 such survivors take the LDS survivor list; more defer the tile to the
+    second pass, which sorts them.  Half of the survivors are dominated by others, and
+    a second tile of the segment is all on one staircase."""
+    rng = np.random.default_rng(500 + n_below)
+    n = 2048
+    T = 1.0 + rng.permutation(n).astype(np.float64)  # distinct; A is the point with T = 1
+    E = np.empty(n)
+    a = int(np.argmin(T))
+    E[a] = 100.0
+    others = np.delete(np.arange(n), a)
+    pick = rng.choice(others, n_below, replace=False)
+    E[others] = rng.uniform(100.0, 200.0, n - 1)  # at or above A: never kept
+    E[pick] = rng.uniform(1.0, 99.0, n_below)
+    T2 = np.sort(rng.uniform(5000.0, 6000.0, 900))
+    E2 = np.linspace(50.0, 1.0, 900)
+    T, E = np.concatenate([T, T2]), np.concatenate([E, E2])
+    seg = np.array([0, len(T)], dtype=np.int64)
+    fr = kr.pareto_filter(torch.from_numpy(T).cuda(), torch.from_numpy(E).cuda(), seg)
+    ix = oracle_lib.pareto(T, E)
+    check_frontier(fr, 0, (ix, T[ix], E[ix]), "tile survivors %d" % n_below)
+
+
 def test_pareto_filter_capacity(kr):
     T = torch.linspace(1.0, 2.0, 5000, dtype=torch.float64).cuda()
     E = torch.linspace(2.0, 1.0, 5000, dtype=torch.float64).cuda()
