@@ -32,8 +32,14 @@
  *    outputs are unspecified but no memory outside the documented extents is written.
  *  - fp64 everywhere; no FMA contraction; every rounding follows the documented
  *    order, so results are reproducible bit for bit across runs and launch shapes.
- *  - Inputs must be finite; times strictly positive, powers and comm times >= 0.
- *    Non-finite inputs give unspecified (memory-safe) results.
+ *  - Inputs must be finite and non-negative: times, powers, energies (-0.0 counts as 0).
+ *    The entry points that take cost tables or point sets accept an optional device
+ *    status word (status_out, NULL to skip): when given, a check pass reads every input
+ *    value first and the word receives KR_OK, or KR_ENONFINITE if some value is NaN,
+ *    infinite or negative (the check reads the inputs once more, so callers that
+ *    validated them already pass NULL).  kr_compose_frontiers always checks its points
+ *    while it reads them.  With invalid inputs the other outputs are unspecified but
+ *    memory-safe.
  */
 #ifndef KAREUS_H
 #define KAREUS_H
@@ -48,6 +54,7 @@ extern "C" {
 typedef int32_t kr_status;
 #define KR_OK 0
 #define KR_EINVAL (-1)       /* null pointer, size out of range, inconsistent shape */
+#define KR_ENONFINITE (-2)   /* an input time, power or energy is NaN, infinite or negative */
 #define KR_ECAPACITY (-3)    /* workspace or output capacity too small (host-known) */
 #define KR_EHIP (-4)         /* a HIP runtime call or kernel launch failed */
 #define KR_EUNSUPPORTED (-5) /* shape beyond the kernels' on-chip limits */
@@ -103,13 +110,14 @@ typedef struct kr_space {
  * (Section 4.1 decision variables; cost model above).
  *   T_out, E_out  [P][C] with C = F * (n_pos * S) for M = 1, F * (n_pp * S * S) for
  *                 M = 2, indexed by the candidate index above.
+ *   status_out    device [1] or NULL: input check (conventions above)
  * Limits: the per-(partition, frequency) table slab staged on chip,
  * 8 * (2N(S+1) + 2(N+1)(S+1) + 2MS) bytes plus 4 bytes per launch-position pair when
  * M = 2, must fit in 64 KiB, else KR_EUNSUPPORTED.  No workspace.
  */
 kr_status kr_evaluate_partition(const kr_space *space, const double *t, const double *pw,
                                 const double *tc, const double *pc, double *T_out,
-                                double *E_out, void *stream);
+                                double *E_out, int32_t *status_out, void *stream);
 
 /* Candidates per partition of `space` (0 if the space is invalid). */
 int64_t kr_candidates_per_partition(const kr_space *space);
@@ -123,7 +131,7 @@ int64_t kr_candidates_per_partition(const kr_space *space);
  * (T, E) duplicates the smallest index is kept.  The output per segment is a strict
  * staircase in ascending T (T strictly increasing, E strictly decreasing).
  *   n_total        host; = seg_off[n_seg]
- *   T, E           [n_total] device; T > 0 and E >= 0, finite
+ *   T, E           [n_total] device; finite, >= 0 (-0.0 is read, and reported, as +0.0)
  *   seg_off        device [n_seg + 1]: non-decreasing, seg_off[0] = 0,
  *                  seg_off[n_seg] = n_total, every segment shorter than 2^31 (trusted:
  *                  the host does not read it)
@@ -132,13 +140,14 @@ int64_t kr_candidates_per_partition(const kr_space *space);
  *                  out_off[n_seg] = total frontier points, even if > cap
  *   out_idx        device [cap] point index relative to its segment start
  *   out_T, out_E   device [cap]
+ *   status_out     device [1] or NULL: input check of T and E (conventions above)
  * If the total exceeds cap, only the first cap points are written; check
  * out_off[n_seg] after the stream completes.
  */
 kr_status kr_pareto_filter(int64_t n_total, const double *T, const double *E,
                            const int64_t *seg_off, int32_t n_seg, int64_t cap, int64_t *out_off,
-                           int32_t *out_idx, double *out_T, double *out_E, void *ws,
-                           size_t ws_bytes, void *stream);
+                           int32_t *out_idx, double *out_T, double *out_E, int32_t *status_out,
+                           void *ws, size_t ws_bytes, void *stream);
 size_t kr_pareto_filter_workspace(int64_t n_total, int32_t n_seg);
 
 /*
@@ -150,7 +159,8 @@ size_t kr_pareto_filter_workspace(int64_t n_total, int32_t n_seg);
 kr_status kr_evaluate_and_filter(const kr_space *space, const double *t, const double *pw,
                                  const double *tc, const double *pc, int64_t cap,
                                  int64_t *out_off, int32_t *out_idx, double *out_T,
-                                 double *out_E, void *ws, size_t ws_bytes, void *stream);
+                                 double *out_E, int32_t *status_out, void *ws, size_t ws_bytes,
+                                 void *stream);
 size_t kr_evaluate_and_filter_workspace(const kr_space *space);
 
 /*
@@ -159,7 +169,7 @@ size_t kr_evaluate_and_filter_workspace(const kr_space *space);
  * discretised time axis, plus the non-dominated bins of the result.
  *
  * Partition k's points are [off[k], off[k+1]) of T/E (any finite set with E >= 0,
- * not necessarily sorted or strict).  With bin width delta, point j of partition k sits
+ * not necessarily sorted or strict; -0.0 energies are binned as +0.0).  With bin width delta, point j of partition k sits
  * at offset off_k[j] = floor((T[j] - tmin_k) / delta); e_k[b] = least E at offset b
  * (ties: smallest point index).  F_1 = e_1 and
  *   F_k[b] = min over b2 of F_{k-1}[b - b2] + e_k[b2]   (ties: smallest b2),
@@ -180,8 +190,10 @@ size_t kr_evaluate_and_filter_workspace(const kr_space *space);
  *                                 bin, their lower time edge tmin_sum + b*delta, F_P[b]
  *   n_stair      device [1]       number of staircase bins
  *   status_out   device [1]       KR_OK, or KR_ECAPACITY if the caller's delta needs
- *                                 more than B bins, or KR_EINVAL for an empty partition
- *                                 (then nothing else is meaningful)
+ *                                 more than B bins, KR_EINVAL for an empty partition, or
+ *                                 KR_ENONFINITE for a non-finite time or an energy that
+ *                                 is not a finite value >= 0 (then nothing else is
+ *                                 meaningful and n_stair is 0)
  */
 kr_status kr_compose_frontiers(int32_t n_parts, const int64_t *off, const double *T,
                                const double *E, int32_t n_bins, double delta, double *F_out,

@@ -112,14 +112,25 @@ def pareto(T, E):
     return out[: n_out.value].copy()
 
 
-def evaluate_and_filter(space, t, pw, tc, pc, parts: Optional[range] = None):
-    """Per partition: (frontier candidate indices, T, E)."""
-    res = []
-    for p in (parts if parts is not None else range(space.n_parts)):
+def evaluate_and_filter(space, t, pw, tc, pc, parts: Optional[range] = None,
+                        threads: int = 1):
+    """Per partition: (frontier candidate indices, T, E).  With threads > 1 the partitions
+    (independent) are spread over that many threads; each partition still runs the plain
+    single-threaded evaluation and GetFrontier, so the results are the same."""
+    ps = list(parts if parts is not None else range(space.n_parts))
+
+    def one(p):
         T, E = evaluate_partition(space, t, pw, tc, pc, p)
         idx = pareto(T, E)
-        res.append((idx, T[idx], E[idx]))
-    return res
+        return idx, T[idx], E[idx]
+
+    if threads <= 1:
+        return [one(p) for p in ps]
+    import concurrent.futures as cf
+
+    _load()  # load once, before the threads
+    with cf.ThreadPoolExecutor(max_workers=threads) as ex:
+        return list(ex.map(one, ps))
 
 
 class Composed:

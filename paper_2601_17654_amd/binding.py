@@ -22,7 +22,7 @@ if not os.path.exists(_LIB_PATH):
                       "python paper_2601_17654_amd/build.py)")
 _lib = ctypes.CDLL(_LIB_PATH)
 
-KR_OK, KR_EINVAL, KR_ECAPACITY, KR_EHIP, KR_EUNSUPPORTED = 0, -1, -3, -4, -5
+KR_OK, KR_EINVAL, KR_ENONFINITE, KR_ECAPACITY, KR_EHIP, KR_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 
 
 class KrSpace(ctypes.Structure):
@@ -36,13 +36,13 @@ _vp, _i32, _i64, _f64, _sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
                               ctypes.c_double, ctypes.c_size_t)
 _SP = ctypes.POINTER(KrSpace)
 _SIGS = {
-    "kr_evaluate_partition": (_i32, [_SP, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "kr_evaluate_partition": (_i32, [_SP, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "kr_candidates_per_partition": (_i64, [_SP]),
-    "kr_pareto_filter": (_i32, [_i64, _vp, _vp, _vp, _i32, _i64, _vp, _vp, _vp, _vp, _vp, _sz,
-                                _vp]),
+    "kr_pareto_filter": (_i32, [_i64, _vp, _vp, _vp, _i32, _i64, _vp, _vp, _vp, _vp, _vp, _vp,
+                                _sz, _vp]),
     "kr_pareto_filter_workspace": (_sz, [_i64, _i32]),
-    "kr_evaluate_and_filter": (_i32, [_SP, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _sz,
-                                      _vp]),
+    "kr_evaluate_and_filter": (_i32, [_SP, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp,
+                                      _vp, _sz, _vp]),
     "kr_evaluate_and_filter_workspace": (_sz, [_SP]),
     "kr_compose_frontiers": (_i32, [_i32, _vp, _vp, _vp, _i32, _f64, _vp, _vp, _vp, _vp, _vp, _vp,
                                     _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
@@ -91,6 +91,18 @@ def status_string(status: int) -> str:
 def _check(fn: str, status: int) -> None:
     if status != KR_OK:
         raise KrError(fn, status)
+
+
+def _status_word(validate: bool):
+    """Device status word for an entry point's input check, or None to skip it."""
+    return torch.empty(1, dtype=torch.int32, device="cuda") if validate else None
+
+
+def _check_status(fn: str, status: Optional[torch.Tensor]) -> None:
+    """Raises KrError if the device status word of an input check is not KR_OK (reads it
+    back, so the stream is synchronised)."""
+    if status is not None:
+        _check(fn, int(status.item()))
 
 
 def _space(space) -> KrSpace:
@@ -142,8 +154,10 @@ def candidates_per_partition(space) -> int:
     return int(_lib.kr_candidates_per_partition(ctypes.byref(_space(space))))
 
 
-def evaluate_partition(space, t, pw, tc, pc, T_out=None, E_out=None):
-    """Time and energy of every candidate: (T, E), float64 [P][C] on the device."""
+def evaluate_partition(space, t, pw, tc, pc, T_out=None, E_out=None, validate: bool = True):
+    """Time and energy of every candidate: (T, E), float64 [P][C] on the device.  With
+    validate, the library checks the tables first and a non-finite or negative value
+    raises KrError(KR_ENONFINITE) (the call then waits for the stream)."""
     sp = _space(space)
     C = candidates_per_partition(space)
     t, pw = _dev(t, torch.float64, "t"), _dev(pw, torch.float64, "pw")
@@ -153,9 +167,11 @@ def evaluate_partition(space, t, pw, tc, pc, T_out=None, E_out=None):
         T_out = torch.empty((space.n_parts, C), dtype=torch.float64, device="cuda")
     if E_out is None:
         E_out = torch.empty((space.n_parts, C), dtype=torch.float64, device="cuda")
+    status = _status_word(validate)
     _check("kr_evaluate_partition",
            _lib.kr_evaluate_partition(ctypes.byref(sp), _ptr(t), _ptr(pw), _ptr(tc), _ptr(pc),
-                                      _ptr(T_out), _ptr(E_out), _stream()))
+                                      _ptr(T_out), _ptr(E_out), _ptr(status), _stream()))
+    _check_status("kr_evaluate_partition", status)
     return T_out, E_out
 
 
@@ -186,8 +202,10 @@ def _finish_frontier(off, idx, T, E, cap, sync):
     return Frontier(off, idx[:total], T[:total], E[:total]), True
 
 
-def pareto_filter(T, E, seg_off, cap: Optional[int] = None, sync: bool = True) -> Frontier:
-    """GetFrontier of every segment [seg_off[g], seg_off[g+1]) of (T, E)."""
+def pareto_filter(T, E, seg_off, cap: Optional[int] = None, sync: bool = True,
+                  validate: Optional[bool] = None) -> Frontier:
+    """GetFrontier of every segment [seg_off[g], seg_off[g+1]) of (T, E).  validate
+    (default: sync) has the library check T and E, raising KrError(KR_ENONFINITE)."""
     seg_host = np.asarray(seg_off.cpu() if isinstance(seg_off, torch.Tensor) else seg_off,
                           dtype=np.int64)
     n_seg = len(seg_host) - 1
@@ -207,9 +225,12 @@ def pareto_filter(T, E, seg_off, cap: Optional[int] = None, sync: bool = True) -
         oE = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
         wsb = _lib.kr_pareto_filter_workspace(n_total, n_seg)
         ws = _workspace(wsb)
+        status = _status_word(sync if validate is None else validate)
         _check("kr_pareto_filter",
                _lib.kr_pareto_filter(n_total, _ptr(T), _ptr(E), _ptr(seg_dev), n_seg, c, _ptr(off),
-                                     _ptr(idx), _ptr(oT), _ptr(oE), _ptr(ws), wsb, _stream()))
+                                     _ptr(idx), _ptr(oT), _ptr(oE), _ptr(status), _ptr(ws), wsb,
+                                     _stream()))
+        _check_status("kr_pareto_filter", status)
         fr, ok = _finish_frontier(off, idx, oT, oE, c, sync)
         if fr is not None:
             return fr
@@ -217,8 +238,10 @@ def pareto_filter(T, E, seg_off, cap: Optional[int] = None, sync: bool = True) -
 
 
 def evaluate_and_filter(space, t, pw, tc, pc, cap: Optional[int] = None,
-                        sync: bool = True) -> Frontier:
-    """Fused evaluation + GetFrontier, one segment per partition; idx = candidate index."""
+                        sync: bool = True, validate: Optional[bool] = None) -> Frontier:
+    """Fused evaluation + GetFrontier, one segment per partition; idx = candidate index.
+    validate (default: sync) has the library check the tables first, raising
+    KrError(KR_ENONFINITE)."""
     sp = _space(space)
     t, pw = _dev(t, torch.float64, "t"), _dev(pw, torch.float64, "pw")
     tc, pc = _dev(tc, torch.float64, "tc"), _dev(pc, torch.float64, "pc")
@@ -234,10 +257,12 @@ def evaluate_and_filter(space, t, pw, tc, pc, cap: Optional[int] = None,
         oT = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
         oE = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
         ws = _workspace(wsb)
+        status = _status_word(sync if validate is None else validate)
         _check("kr_evaluate_and_filter",
                _lib.kr_evaluate_and_filter(ctypes.byref(sp), _ptr(t), _ptr(pw), _ptr(tc), _ptr(pc),
-                                           c, _ptr(off), _ptr(idx), _ptr(oT), _ptr(oE), _ptr(ws),
-                                           wsb, _stream()))
+                                           c, _ptr(off), _ptr(idx), _ptr(oT), _ptr(oE),
+                                           _ptr(status), _ptr(ws), wsb, _stream()))
+        _check_status("kr_evaluate_and_filter", status)
         fr, ok = _finish_frontier(off, idx, oT, oE, c, sync)
         if fr is not None:
             return fr

@@ -140,6 +140,17 @@ bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)
     return true;
 }
 
+// The input check of the cost tables, when the caller asks for a status word.
+hipError_t check_tables(const kr_space *s, const double *t, const double *pw, const double *tc,
+                        const double *pc, int32_t *status, hipStream_t st)
+{
+    const int64_t slabs = (int64_t)s->n_parts * s->n_freq;
+    const int64_t nt = slabs * s->n_kernels * (s->n_sm + 1), nc = slabs * s->n_comm * s->n_sm;
+    const double *xs[4] = {t, pw, tc, pc};
+    const int64_t n[4] = {nt, nt, nc, nc};
+    return launch_check(xs, n, 4, status, st);
+}
+
 // Caller-owned events recorded around a phase (kr_set_phase_events).
 hipEvent_t g_phase_ev[6][2] = {};
 
@@ -201,7 +212,7 @@ int64_t kr_candidates_per_partition(const kr_space *space)
 
 kr_status kr_evaluate_partition(const kr_space *space, const double *t, const double *pw,
                                 const double *tc, const double *pc, double *T_out, double *E_out,
-                                void *stream)
+                                int32_t *status_out, void *stream)
 {
     if (!space_ok(space) || !t || !pw || !tc || !pc || !T_out || !E_out) return KR_EINVAL;
     EvalArgs a;
@@ -212,6 +223,8 @@ kr_status kr_evaluate_partition(const kr_space *space, const double *t, const do
     a.pc = pc;
     a.T_out = T_out;
     a.E_out = E_out;
+    if (status_out && check_tables(space, t, pw, tc, pc, status_out, (hipStream_t)stream) != hipSuccess)
+        return KR_EHIP;
     return launch_eval(a, (hipStream_t)stream) == hipSuccess ? KR_OK : KR_EHIP;
 }
 
@@ -226,8 +239,8 @@ size_t kr_pareto_filter_workspace(int64_t n_total, int32_t n_seg)
 
 kr_status kr_pareto_filter(int64_t n_total, const double *T, const double *E,
                            const int64_t *seg_off, int32_t n_seg, int64_t cap, int64_t *out_off,
-                           int32_t *out_idx, double *out_T, double *out_E, void *ws,
-                           size_t ws_bytes, void *stream)
+                           int32_t *out_idx, double *out_T, double *out_E, int32_t *status_out,
+                           void *ws, size_t ws_bytes, void *stream)
 {
     if (n_total < 0 || n_seg < 0 || cap < 0 || !seg_off || !out_off ||
         (n_total > 0 && (!T || !E)) || (cap > 0 && (!out_idx || !out_T || !out_E)) || !ws)
@@ -235,6 +248,11 @@ kr_status kr_pareto_filter(int64_t n_total, const double *T, const double *E,
     if (ws_bytes < kr_pareto_filter_workspace(n_total, n_seg)) return KR_ECAPACITY;
     hipStream_t st = (hipStream_t)stream;
     const int64_t n_units = (n_total + KR_TILE - 1) / KR_TILE + n_seg;
+    if (status_out) {
+        const double *xs[2] = {T, E};
+        const int64_t n[2] = {n_total, n_total};
+        if (launch_check(xs, n, 2, status_out, st) != hipSuccess) return KR_EHIP;
+    }
     Carve c(ws);
     FilterWs w = carve_filter(c, n_total, n_seg, n_units, false);
     SegLayout L;
@@ -260,8 +278,8 @@ size_t kr_evaluate_and_filter_workspace(const kr_space *space)
 
 kr_status kr_evaluate_and_filter(const kr_space *space, const double *t, const double *pw,
                                  const double *tc, const double *pc, int64_t cap, int64_t *out_off,
-                                 int32_t *out_idx, double *out_T, double *out_E, void *ws,
-                                 size_t ws_bytes, void *stream)
+                                 int32_t *out_idx, double *out_T, double *out_E,
+                                 int32_t *status_out, void *ws, size_t ws_bytes, void *stream)
 {
     if (!space_ok(space) || !t || !pw || !tc || !pc || cap < 0 || !out_off ||
         (cap > 0 && (!out_idx || !out_T || !out_E)) || !ws)
@@ -282,6 +300,8 @@ kr_status kr_evaluate_and_filter(const kr_space *space, const double *t, const d
     UnitOut o{w.buf[0].T, w.buf[0].E, w.buf[0].I, w.ucnt};
     a.dma16 = a.wave && (a.N * (a.S + 1)) % 2 == 0 && (uintptr_t)t % 16 == 0 &&
               (uintptr_t)pw % 16 == 0;
+    if (status_out && check_tables(space, t, pw, tc, pc, status_out, st) != hipSuccess)
+        return KR_EHIP;
     phase_mark(KR_PHASE_EVAL_TILE, 0, st);
     if ((a.wave ? launch_eval_filter_wave(a, o, st) : launch_eval_filter(a, o, st)) != hipSuccess)
         return KR_EHIP;
@@ -311,9 +331,8 @@ size_t kr_compose_frontiers_workspace(int32_t n_parts, int32_t n_bins)
     c.take<int32_t>(B + 8 * P);
     c.take<double>(B + 8 * P);
     c.take<int32_t>(P);
-    c.take<double>(B);
-    c.take<double>(B);
     c.take<double>(P * B);
+    c.take<int32_t>(1);
     c.take<double>((B + KR_ST_CHUNK - 1) / KR_ST_CHUNK);
     c.take<int32_t>((B + KR_ST_CHUNK - 1) / KR_ST_CHUNK);
     return c.used;
@@ -346,9 +365,8 @@ kr_status kr_compose_frontiers(int32_t n_parts, const int64_t *off, const double
     w.oarg = c.take<int32_t>(B + 8 * P);
     w.oe = c.take<double>(B + 8 * P);
     w.occ = c.take<int32_t>(P);
-    w.F0 = c.take<double>(B);
-    w.F1 = c.take<double>(B);
     w.Fh = c.take<double>(P * B);
+    w.ticket = c.take<int32_t>(1);
     w.chmin = c.take<double>((B + KR_ST_CHUNK - 1) / KR_ST_CHUNK);
     w.chcnt = c.take<int32_t>((B + KR_ST_CHUNK - 1) / KR_ST_CHUNK);
     ComposeArgs a;
@@ -513,8 +531,8 @@ kr_status kr_microbatch_frontier(int32_t n_types, int32_t n_freq, const int64_t 
     const int64_t S = (int64_t)n_freq * n_bins;
     if (launch_mb_seg(w.seg, S, st) != hipSuccess) return KR_EHIP;
     const kr_status rc = kr_pareto_filter(S, w.slot_T, w.slot_E, w.seg, 1, S, w.front_off,
-                                          w.front_idx, w.front_T, w.front_E, w.pws, w.pws_bytes,
-                                          stream);
+                                          w.front_idx, w.front_T, w.front_E, nullptr, w.pws,
+                                          w.pws_bytes, stream);
     if (rc != KR_OK) return rc;
     return launch_mb_gather(a, w.front_off, w.front_idx, cap, out_T, out_E, out_f, out_choice,
                             n_out, st) == hipSuccess
@@ -606,8 +624,8 @@ kr_status kr_microbatch_enumerate(int32_t n_types, int32_t n_freq, const int64_t
     if (launch_mb_enum(a, w.base, n_configs, w.status, st) != hipSuccess) return KR_EHIP;
     if (launch_mb_seg(w.seg, n_configs, st) != hipSuccess) return KR_EHIP;
     const kr_status rc = kr_pareto_filter(n_configs, w.slot_T, w.slot_E, w.seg, 1, n_configs,
-                                          w.front_off, w.front_idx, w.front_T, w.front_E, w.pws,
-                                          w.pws_bytes, stream);
+                                          w.front_off, w.front_idx, w.front_T, w.front_E, nullptr,
+                                          w.pws, w.pws_bytes, stream);
     if (rc != KR_OK) return rc;
     if (launch_mb_enum_gather(a, w.base, w.status, w.front_off, w.front_idx, cap, out_T, out_E,
                               out_f, out_choice, n_out, n_configs, st) != hipSuccess)
@@ -852,6 +870,7 @@ const char *kr_status_string(kr_status status)
     switch (status) {
     case KR_OK: return "ok";
     case KR_EINVAL: return "invalid argument";
+    case KR_ENONFINITE: return "non-finite or negative input";
     case KR_ECAPACITY: return "workspace or output capacity too small";
     case KR_EHIP: return "HIP runtime error";
     case KR_EUNSUPPORTED: return "shape exceeds the kernels' on-chip limits";

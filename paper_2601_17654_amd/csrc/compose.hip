@@ -45,9 +45,21 @@ __device__ __forceinline__ double load_l2(const double *p)
                                    __HIP_MEMORY_SCOPE_AGENT));
 }
 
-__global__ void compose_init_kernel(ComposeArgs a)
+__device__ __forceinline__ void store_dev(uint64_t *p, uint64_t v)
 {
-    if (threadIdx.x == 0) *a.status = KR_OK;
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_dev(int32_t *p, int32_t v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__global__ void compose_init_kernel(ComposeArgs a, ComposeWs w)
+{
+    if (threadIdx.x == 0) {
+        *a.status = KR_OK;
+        *w.ticket = 0;
+    }
 }
 
 // Per-partition time range.
@@ -61,11 +73,14 @@ __global__ void __launch_bounds__(KR_BLOCK) compose_range_kernel(ComposeArgs a, 
         return;
     }
     double mn = INFINITY, mx = -INFINITY;
+    bool bad = false;  // a non-finite time, or an energy that is not a finite value >= 0
     for (int64_t j = lo + threadIdx.x; j < hi; j += KR_BLOCK) {
         const double t = a.T[j];
         mn = t < mn ? t : mn;
         mx = t > mx ? t : mx;
+        bad = bad || !(dbits(fabs(t)) < KR_INF_BITS) || !(dbits(a.E[j] + 0.0) < KR_INF_BITS);
     }
+    if (__ballot(bad) && (threadIdx.x & 63) == 0) store_dev(a.status, (int32_t)KR_ENONFINITE);
     mn = block_reduce(mn, (double)INFINITY, MinF64(), sc);
     mx = block_reduce(mx, -(double)INFINITY, MaxF64(), sc);
     if (threadIdx.x == 0) {
@@ -185,12 +200,13 @@ __device__ __forceinline__ void bin_partition(const ComposeArgs &a, const Compos
         const double x = floor((a.T[j] - tmin) / delta);
         const int64_t o = !(x > 0.0) ? 0 : (x < (double)M ? (int64_t)x : M);
         a.pt_bin[j] = (int32_t)o;
-        atomicMin((unsigned long long *)&eb[o], (unsigned long long)dbits(a.E[j]));
+        atomicMin((unsigned long long *)&eb[o], (unsigned long long)dbits(a.E[j] + 0.0));
     }
     __syncthreads();
     for (int64_t j = lo + threadIdx.x; j < hi; j += KR_BLOCK) {
         const int32_t o = a.pt_bin[j];
-        if (dbits(a.E[j]) == load_l2((const uint64_t *)&eb[o])) atomicMin((int32_t *)&ea[o], (int32_t)(j - lo));
+        if (dbits(a.E[j] + 0.0) == load_l2((const uint64_t *)&eb[o]))
+            atomicMin((int32_t *)&ea[o], (int32_t)(j - lo));
     }
     __syncthreads();
     int32_t carry = 0;
@@ -232,111 +248,6 @@ __global__ void __launch_bounds__(KR_BLOCK) compose_bin_kernel(ComposeArgs a, Co
         bin_partition(a, w, k, w.ebits + w.eoff[k], w.earg + w.eoff[k], sc);
 }
 
-// F_1 and the first row of back-pointers.
-__global__ void compose_first_kernel(ComposeArgs a, ComposeWs w, double *F)
-{
-    const int64_t b = (int64_t)blockIdx.x * KR_BLOCK + threadIdx.x;
-    if (*a.status != KR_OK) return;
-    if (b >= a.B) return;
-    double v = INFINITY;
-    int32_t who = -1;
-    if (b <= w.Mk[0]) {
-        const int32_t arg = w.earg[b];
-        if (arg != 0x7FFFFFFF) {
-            v = bitsd(w.ebits[b]);
-            who = arg;
-        }
-    }
-    F[b] = v;
-    a.bp[b] = who;
-}
-
-// One min-plus step on a tile of KR_MP_W output bins, for offsets up to KR_MP_HCAP:
-// the window F_{k-1}[b0 - M_k, b0 + KR_MP_W) and partition k's occupied records are
-// staged in LDS; the KR_MP_Q quarters of the block each take a contiguous (so
-// ascending in b2) quarter of the records, and the partial minima are combined in
-// quarter order with strict comparisons, so ties still go to the smallest b2.
-
-struct MinplusLds {
-    double win[KR_MP_W + KR_MP_HCAP];
-    double e[KR_MP_HCAP + 1];
-    int32_t off8[KR_MP_HCAP + 1];  // b2 * 8: byte offset into the window
-    int32_t arg[KR_MP_HCAP + 1];
-    double pbest[KR_MP_Q][KR_MP_W];
-    int32_t pwho[KR_MP_Q][KR_MP_W];
-};
-
-__global__ void __launch_bounds__(KR_MP_W *KR_MP_Q)
-minplus_tile_kernel(ComposeArgs a, ComposeWs w, int k, const double *Fprev, double *Fcur)
-{
-    __shared__ MinplusLds sm;
-    if (*a.status != KR_OK) return;
-    const int tid = threadIdx.x, t = tid % KR_MP_W, qtr = tid / KR_MP_W;
-    const int64_t b0 = (int64_t)blockIdx.x * KR_MP_W;
-    const int64_t Lprev = w.Lk[k - 1], Lcur = w.Lk[k];
-    const int64_t M = w.Mk[k];
-    const int cnt = w.occ[k];
-    const int64_t base = w.eoff[k];
-    double best = INFINITY;
-    int32_t who = -1;
-    if (M > KR_MP_HCAP) {
-        // offsets beyond the window: every quarter-0 thread walks all records itself
-        if (qtr == 0 && b0 + t < Lcur) {
-            const int64_t b = b0 + t;
-            for (int x = 0; x < cnt; ++x) {
-                const int64_t src = b - w.ob2[base + x];
-                if (src >= 0 && src < Lprev) {
-                    const double v = Fprev[src] + w.oe[base + x];
-                    if (v < best) {
-                        best = v;
-                        who = w.oarg[base + x];
-                    }
-                }
-            }
-        }
-    } else {
-        for (int i = tid; i < KR_MP_W + M; i += KR_MP_W * KR_MP_Q) {
-            const int64_t src = b0 - M + i;
-            sm.win[i] = src >= 0 && src < Lprev ? Fprev[src] : INFINITY;
-        }
-        for (int i = tid; i < cnt; i += KR_MP_W * KR_MP_Q) {
-            sm.e[i] = w.oe[base + i];
-            sm.off8[i] = w.ob2[base + i] * 8;
-            sm.arg[i] = w.oarg[base + i];
-        }
-        __syncthreads();
-        const int x0 = cnt * qtr / KR_MP_Q, x1 = cnt * (qtr + 1) / KR_MP_Q;
-        const char *wl = (const char *)(sm.win + t + M);  // window entry of bin b0 + t
-        int bx = -1;
-#pragma unroll 4
-        for (int x = x0; x < x1; ++x) {
-            const double v = *(const double *)(wl - sm.off8[x]) + sm.e[x];
-            bx = v < best ? x : bx;
-            best = v < best ? v : best;
-        }
-        sm.pbest[qtr][t] = best;
-        sm.pwho[qtr][t] = bx >= 0 ? sm.arg[bx] : -1;
-        __syncthreads();
-        if (qtr == 0) {
-            who = sm.pwho[0][t];
-#pragma unroll
-            for (int q = 1; q < KR_MP_Q; ++q) {
-                const double v = sm.pbest[q][t];
-                if (v < best) {
-                    best = v;
-                    who = sm.pwho[q][t];
-                }
-            }
-        }
-    }
-    const int64_t b = b0 + t;
-    if (qtr == 0 && b < a.B) {
-        const bool live = b < Lcur;
-        Fcur[b] = live ? best : INFINITY;
-        a.bp[(int64_t)k * a.B + b] = live ? who : -1;
-    }
-}
-
 // All min-plus steps in one launch, as a wavefront over (tile, step).  Block g owns
 // the KR_MP_W bins of tile g for every step: F_k of its own bins stays in LDS from one
 // step to the next, and the halo F_{k-1}[b0 - M_k, b0) comes from the tiles on its
@@ -348,22 +259,17 @@ minplus_tile_kernel(ComposeArgs a, ComposeWs w, int k, const double *Fprev, doub
 // its left have finished step k - 1, so the tiles advance as a diagonal front.  The
 // next step's halo and records are loaded while the current step computes.
 //
-// The grid is launched cooperatively (every block resident), so a wait always ends; a
-// wait that still exceeds KR_WF_POLLS polls sets the status to KR_EHIP, and every other
-// waiter gives up as soon as it sees that status.  Entries are written and read with
+// Tiles are handed out by an atomic ticket taken when a block starts, not by block
+// index, so the tile a block waits on (always further left, a smaller ticket) belongs to
+// a block that started earlier and is resident or finished: the waits end without any
+// guarantee that the whole grid is resident at once, and without a cooperative launch.
+// A wait that still exceeds KR_WF_POLLS polls sets the status to KR_EHIP, and every
+// other waiter gives up as soon as it sees that status.  Entries are written and read with
 // device-scope relaxed atomic accesses, which are coherent across the chip without
 // cache maintenance; each is written at most once per launch, after the fill kernel.
 #define KR_WF_POLLS (1 << 22)
 #define KR_UNSET 0x7FF4B1A5C0DE0000ull
 
-__device__ __forceinline__ void store_dev(uint64_t *p, uint64_t v)
-{
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void store_dev(int32_t *p, int32_t v)
-{
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 // Whether bin x of row k is read by another tile: within M_{k+1} of its tile's right
 // edge and below L_k (M1 = M_{k+1}, L = L_k).
@@ -402,6 +308,7 @@ struct WavefrontLds {
     int32_t pidx[KR_WF_S][KR_MP_W];  // their 8-offset group (dense) or point (sparse)
     int4 meta[2][KR_WF_MC];  // (M_k, L_k, first record, records) at [(k / MC) & 1][k % MC]
     int32_t bad;             // a wait was given up
+    int32_t tile;            // this block's tile (its ticket)
 };
 
 // Whether step k scans its dense offset table (about 2.25 instructions per pair) rather
@@ -426,7 +333,9 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
     const bool loader = qtr != 0;
     const int s = tid - KR_MP_W;  // loader index
     const int P = a.P, B = a.B;
-    const int64_t b0 = (int64_t)blockIdx.x * KR_MP_W, b = b0 + t;
+    if (tid == 0) sm.tile = atomicAdd(w.ticket, 1);
+    __syncthreads();
+    const int64_t b0 = (int64_t)sm.tile * KR_MP_W, b = b0 + t;
     uint64_t *const Fh = (uint64_t *)w.Fh;
     auto window = [&](int k) { return sm.win[k & 1] + LO + H; };  // window(k)[i] = F_{k-1}[b0 + i]
 
@@ -867,60 +776,19 @@ __global__ void staircase_skip_kernel(ComposeArgs a)
     if (*a.status != KR_OK) *a.n_stair = 0;
 }
 
-// Whether G wavefront blocks can all be resident at once on the current device (a
-// cooperative launch needs it); asked once per device.
-static bool wavefront_fits(int G)
-{
-    static int cap[64];
-    static bool known[64];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
-    if (!known[dev]) {
-        int coop = 0, cus = 0, per_cu = 0;
-        cap[dev] = 0;
-        if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess &&
-            coop &&
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                &per_cu, (const void *)minplus_wavefront_kernel, KR_MP_W * KR_MP_Q, 0) == hipSuccess)
-            cap[dev] = per_cu * cus;
-        known[dev] = true;
-    }
-    return G <= cap[dev];
-}
-
 hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipEvent_t *minplus_ev,
                           hipStream_t st)
 {
-    hipLaunchKernelGGL(compose_init_kernel, dim3(1), dim3(64), 0, st, a);
+    hipLaunchKernelGGL(compose_init_kernel, dim3(1), dim3(64), 0, st, a, w);
     hipLaunchKernelGGL(compose_range_kernel, dim3(a.P), dim3(KR_BLOCK), 0, st, a, w);
     hipLaunchKernelGGL(compose_setup_kernel, dim3(1), dim3(KR_BLOCK), 0, st, a, w);
     hipLaunchKernelGGL(compose_bin_kernel, dim3(a.P), dim3(KR_BLOCK), 0, st, a, w);
     const int G = (a.B + KR_MP_W - 1) / KR_MP_W;
-    if (w.Fh && wavefront_fits(G)) {
-        if (a.P > 1)
-            hipLaunchKernelGGL(wavefront_fill_kernel, dim3(a.P - 1), dim3(KR_BLOCK), 0, st, a, w);
-        if (minplus_ev) (void)hipEventRecord(minplus_ev[0], st);
-        void *args[] = {(void *)&a, (void *)&w};
-        const hipError_t e = hipLaunchCooperativeKernel((const void *)minplus_wavefront_kernel,
-                                                        dim3(G), dim3(KR_MP_W * KR_MP_Q), args,
-                                                        0, st);
-        if (e != hipSuccess) return e;
-        if (minplus_ev) (void)hipEventRecord(minplus_ev[1], st);
-    } else {
-        const dim3 grid((a.B + KR_BLOCK - 1) / KR_BLOCK);
-        double *buf[2] = {w.F0, w.F1};
-        double *prev = a.P == 1 ? a.F_out : buf[0];
-        hipLaunchKernelGGL(compose_first_kernel, grid, dim3(KR_BLOCK), 0, st, a, w, prev);
-        if (minplus_ev) (void)hipEventRecord(minplus_ev[0], st);
-        for (int k = 1; k < a.P; ++k) {
-            double *cur = (k == a.P - 1) ? a.F_out : buf[k % 2];
-            hipLaunchKernelGGL(minplus_tile_kernel, dim3(G), dim3(KR_MP_W * KR_MP_Q), 0, st, a, w,
-                               k, (const double *)prev, cur);
-            prev = cur;
-        }
-        if (minplus_ev) (void)hipEventRecord(minplus_ev[1], st);
-    }
+    if (a.P > 1)
+        hipLaunchKernelGGL(wavefront_fill_kernel, dim3(a.P - 1), dim3(KR_BLOCK), 0, st, a, w);
+    if (minplus_ev) (void)hipEventRecord(minplus_ev[0], st);
+    hipLaunchKernelGGL(minplus_wavefront_kernel, dim3(G), dim3(KR_MP_W * KR_MP_Q), 0, st, a, w);
+    if (minplus_ev) (void)hipEventRecord(minplus_ev[1], st);
     {
         const int nb = (a.B + KR_ST_CHUNK - 1) / KR_ST_CHUNK;
         hipLaunchKernelGGL(staircase_min_kernel, dim3(nb), dim3(KR_ST_NT), 0, st, a, w);

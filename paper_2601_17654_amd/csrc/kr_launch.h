@@ -97,8 +97,8 @@ struct ComposeWs {
     int32_t *ob2, *oarg;   // [B + 8P] occupied offsets / point index
     double *oe;            // [B + 8P]
     int32_t *occ;          // [P]
-    double *F0, *F1;       // [B]
-    double *Fh;            // [P][B] step history of the wavefront min-plus (or null)
+    double *Fh;            // [P][B] step history of the wavefront min-plus
+    int32_t *ticket;       // [1] tile tickets of the wavefront min-plus (reset per call)
     double *chmin;         // [ceil(B / KR_ST_CHUNK)] least value of each staircase chunk
     int32_t *chcnt;        // [ceil(B / KR_ST_CHUNK)] staircase bins of each chunk
 };
@@ -114,6 +114,11 @@ struct ComposeArgs {
     int32_t *L_out, *stair_bin, *n_stair, *status;
     double *stair_Tlo, *stair_E;
 };
+// check.hip: status = KR_ENONFINITE if some value of the arrays is NaN, infinite or
+// negative (-0.0 counts as 0), else KR_OK.
+hipError_t launch_check(const double *const *xs, const int64_t *n, int count, int32_t *status,
+                        hipStream_t st);
+
 hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipEvent_t *minplus_ev,
                           hipStream_t st);
 

@@ -115,8 +115,9 @@ pareto_tile_kernel(const double *T, const double *E, SegLayout L, UnitOut o)
     for (int q = 0; q < 8; ++q) {
         const int64_t x = start + threadIdx.x + q * KR_BLOCK;
         ok[q] = x < end;
-        vT[q] = ok[q] ? T[x] : 0.0;
-        vE[q] = ok[q] ? E[x] : 0.0;
+        // + 0.0 maps -0.0 to +0.0, so that the bit patterns order like the values
+        vT[q] = ok[q] ? T[x] + 0.0 : 0.0;
+        vE[q] = ok[q] ? E[x] + 0.0 : 0.0;
         vI[q] = (int32_t)(x - s0);
     }
     int parity = 0;

@@ -38,6 +38,7 @@ def test_status_strings(lib):
     lib.kr_status_string.restype = ctypes.c_char_p
     assert lib.kr_status_string(0) == b"ok"
     assert b"capacity" in lib.kr_status_string(-3)
+    assert b"non-finite" in lib.kr_status_string(-2)
     assert b"unknown" in lib.kr_status_string(42)
 
 
@@ -49,7 +50,7 @@ def test_host_validation_without_gpu():
     sp = b._space(I.SPACES[0]["space"])
     null = ctypes.c_void_p(0)
     assert L.kr_evaluate_partition(ctypes.byref(sp), null, null, null, null, null, null,
-                                   null) == b.KR_EINVAL
+                                   null, null) == b.KR_EINVAL
     bad = b.KrSpace(1, 4, 3, 1, 1, 5, 90.0)  # three comm kernels
     assert L.kr_candidates_per_partition(ctypes.byref(bad)) == 0
     bad = b.KrSpace(1, 4, 1, 1, 1, 6, 90.0)  # n_pos > N + 1
@@ -58,7 +59,7 @@ def test_host_validation_without_gpu():
     huge = b.KrSpace(1, 400, 1, 1, 40, 401, 90.0)
     one = ctypes.c_void_p(8)
     assert L.kr_evaluate_partition(ctypes.byref(huge), one, one, one, one, one, one,
-                                   null) == b.KR_EUNSUPPORTED
+                                   null, null) == b.KR_EUNSUPPORTED
     assert L.kr_evaluate_and_filter_workspace(ctypes.byref(huge)) == 0
     # workspace sizes grow with the problem
     assert L.kr_pareto_filter_workspace(10, 1) < L.kr_pareto_filter_workspace(10 ** 6, 8)

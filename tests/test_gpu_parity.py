@@ -8,6 +8,7 @@ for bit, and the tests also report how many do not.
 """
 
 import dataclasses
+import os
 
 import numpy as np
 import pytest
@@ -306,37 +307,68 @@ def test_compose_config4(kr, oracle_lib, config4):
         assert_close(Es[q], res, RT_TE, "extract E bin %d" % b)
 
 
-@pytest.mark.parametrize("cfg", [0, 1])
+ORACLE_THREADS = min(16, os.cpu_count() or 1)
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2])
 def test_end_to_end_path(kr, oracle_lib, cfg):
-    """Tables -> fused frontiers -> composition -> staircase -> extracted schedules,
-    against the oracle run on the same tables."""
+    """Tables -> fused frontiers of every partition -> composition -> staircase ->
+    extracted schedule of every staircase bin -> decoded (positions, SM choices,
+    frequency), against the oracle run on the same tables (partition-parallel over the
+    host's cores; each partition is the plain single-threaded oracle)."""
     w = workload(cfg)
-    fr = kr.evaluate_and_filter(w.space, *dev_tables(w))
-    ref_fr = oracle_lib.evaluate_and_filter(w.space, w.t, w.pw, w.tc, w.pc)
-    roff = np.zeros(w.space.n_parts + 1, dtype=np.int64)
+    sp = w.space
+    print("end-to-end cfg %d: %d partitions" % (cfg, sp.n_parts), flush=True)
+    fr = kr.evaluate_and_filter(sp, *dev_tables(w))
+    ref_fr = oracle_lib.evaluate_and_filter(sp, w.t, w.pw, w.tc, w.pc, threads=ORACLE_THREADS)
+    off = fr.off.cpu().numpy()
+    gidx, gT, gE = fr.idx.cpu().numpy(), fr.T.cpu().numpy(), fr.E.cpu().numpy()
+    for p in range(sp.n_parts):
+        lo, hi = int(off[p]), int(off[p + 1])
+        np.testing.assert_array_equal(gidx[lo:hi], ref_fr[p][0], err_msg="cfg%d part %d" % (cfg, p))
+        assert_close(gT[lo:hi], ref_fr[p][1], RT_TE, "cfg%d part %d T" % (cfg, p))
+        assert_close(gE[lo:hi], ref_fr[p][2], RT_TE, "cfg%d part %d E" % (cfg, p))
+    roff = np.zeros(sp.n_parts + 1, dtype=np.int64)
     roff[1:] = np.cumsum([len(x[0]) for x in ref_fr])
+    np.testing.assert_array_equal(off, roff)
     rT = np.concatenate([x[1] for x in ref_fr])
     rE = np.concatenate([x[2] for x in ref_fr])
     ridx = np.concatenate([x[0] for x in ref_fr])
     comp = kr.compose_frontiers(fr.off, fr.T, fr.E, w.bins)
     ref = oracle_lib.compose(roff, rT, rE, w.bins)
     compare_composed(kr, comp, ref, roff, rT, rE, "cfg%d" % cfg)
-    sb, _, _ = comp.staircase()
+    sb, st, se = comp.staircase()
+    rb, rt, re_ = oracle_lib.staircase(ref.F, ref.delta, ref.tmin_sum)
+    np.testing.assert_array_equal(sb.cpu().numpy(), rb)
+    assert_close(st.cpu().numpy(), rt, RT_TE, "cfg%d stair T" % cfg)
+    assert_close(se.cpu().numpy(), re_, RT_MINPLUS, "cfg%d stair E" % cfg)
     ch, cc, Ts, Es, ok = kr.extract_schedule(comp, fr.off, fr.T, fr.E, sb, cand_idx=fr.idx)
     assert ok.cpu().numpy().all()
-    f, pos, sm = kr.decode_candidates(w.space, cc.reshape(-1))
+    ch, cc, Ts, Es = ch.cpu().numpy(), cc.cpu().numpy(), Ts.cpu().numpy(), Es.cpu().numpy()
+    rch = np.empty_like(ch)
+    rts, res = np.empty(len(rb)), np.empty(len(rb))
+    for q, b in enumerate(rb):
+        rch[q], rts[q], res[q] = oracle_lib.extract(roff, rT, rE, ref, int(b))
+    np.testing.assert_array_equal(ch, rch, err_msg="cfg%d extracted choices" % cfg)
+    assert_close(Ts, rts, RT_TE, "cfg%d extracted T" % cfg)
+    assert_close(Es, res, RT_TE, "cfg%d extracted E" % cfg)
+    # the candidates behind every choice, decoded on the GPU and by the oracle
+    pts = roff[:-1][None, :] + rch  # frontier point of every (query, partition)
+    np.testing.assert_array_equal(cc, ridx[pts], err_msg="cfg%d chosen candidates" % cfg)
+    f, pos, sm = kr.decode_candidates(sp, torch.from_numpy(cc.reshape(-1)).cuda())
     f, pos, sm = f.cpu().numpy(), pos.cpu().numpy(), sm.cpu().numpy()
-    cc = cc.cpu().numpy()
-    for q, b in enumerate(sb.cpu().numpy()):
-        rc, rts, res = oracle_lib.extract(roff, rT, rE, ref, int(b))
-        np.testing.assert_array_equal(ch[q].cpu().numpy(), rc)
-        assert Es[q].item() == pytest.approx(res, rel=RT_TE)
-        for k in range(w.space.n_parts):
-            cand = ridx[roff[k] + rc[k]]
-            assert cc[q, k] == cand
-            rf, rpos, rsm = oracle_lib.decode(w.space, int(cand))
-            x = q * w.space.n_parts + k
-            assert (f[x], tuple(pos[x]), tuple(sm[x])) == (rf, rpos, rsm)
+    M = sp.n_comm
+    df = np.full(len(ridx), -1)
+    dpos = np.full((len(ridx), M), -1)
+    dsm = np.full((len(ridx), M), -1)
+    for x in np.unique(pts):  # the oracle's decode of every point some choice uses
+        df[x], dpos[x], dsm[x] = oracle_lib.decode(sp, int(ridx[x]))
+    flat = pts.reshape(-1)
+    np.testing.assert_array_equal(f, df[flat], err_msg="cfg%d decoded frequency" % cfg)
+    np.testing.assert_array_equal(pos.reshape(-1, M), dpos[flat],
+                                  err_msg="cfg%d decoded positions" % cfg)
+    np.testing.assert_array_equal(sm.reshape(-1, M), dsm[flat],
+                                  err_msg="cfg%d decoded SM choices" % cfg)
 
 
 def test_compose_wavefront_modes(kr, oracle_lib):
@@ -479,3 +511,116 @@ def test_pareto_filter_union_paths(kr, oracle_lib, n):
     fr = kr.pareto_filter(torch.from_numpy(T).cuda(), torch.from_numpy(E).cuda(), seg)
     ix = oracle_lib.pareto(T, E)
     check_frontier(fr, 0, (ix, T[ix], E[ix]), "n=%d" % n)
+
+
+@pytest.mark.parametrize("shape", [(6, 7, 96), (16, 17, 96), (4, 5, 256), (8, 9, 130)])
+def test_one_comm_many_sm_choices(kr, oracle_lib, shape):
+    """One comm kernel with more SM choices than a wave has lanes (65 .. 256): the fused
+    block-per-slab kernel with one thread per (SM choice, run of positions), with one
+    tile per frequency (7 positions x 96, 5 x 256) or several (17 x 96, 9 x 130), against
+    the oracle; the unfused evaluation too."""
+    N, n_pos, S = shape
+    K = tuple(1 + (7 * s) % 131 for s in range(S))  # SM counts 1 .. 131, repeats allowed
+    space = I.Space(2, N, 1, n_pos, K, (1005.0, 1492.5, 1980.0))
+    tab = I.make_tables(space, seed=N * 1000 + S, comm_bytes=(4e6, 64e6))
+    d = [torch.from_numpy(tab[k]).cuda() for k in ("t", "pw", "tc", "pc")]
+    fr = kr.evaluate_and_filter(space, *d)
+    T, E = kr.evaluate_partition(space, *d)
+    T, E = T.cpu().numpy(), E.cpu().numpy()
+    for p in range(space.n_parts):
+        Tr, Er = oracle_lib.evaluate_partition(space, tab["t"], tab["pw"], tab["tc"], tab["pc"], p)
+        assert_close(T[p], Tr, RT_TE, "T %s part %d" % (shape, p))
+        assert_close(E[p], Er, RT_TE, "E %s part %d" % (shape, p))
+        ix = oracle_lib.pareto(Tr, Er)
+        check_frontier(fr, p, (ix, Tr[ix], Er[ix]), "frontier %s part %d" % (shape, p))
+
+
+@pytest.mark.parametrize("where,value", [("t", float("nan")), ("t", float("inf")),
+                                         ("t", -1e-6), ("pw", float("nan")), ("pw", -5.0),
+                                         ("tc", float("inf")), ("pc", -0.5)])
+def test_nonfinite_tables_rejected(kr, where, value):
+    """A NaN, infinite or negative table entry gives KR_ENONFINITE from the input check
+    of the evaluation entry points (Sections 2.1, 4.5 define the cost model for finite,
+    non-negative profiles)."""
+    for cfg_space, n_comm in ((0, 1), (2, 2)):
+        space = dataclasses.replace(I.SPACES[cfg_space]["space"], n_parts=2) if n_comm == 1 else \
+            I.Space(2, 5, 2, 4, (4, 8), (1005.0, 1980.0))
+        tab = I.make_tables(space, seed=3, comm_bytes=(4e6, 64e6))
+        arr = tab[where]
+        arr.reshape(-1)[arr.size // 2 + 1] = value
+        d = [torch.from_numpy(tab[k]).cuda() for k in ("t", "pw", "tc", "pc")]
+        with pytest.raises(kr.KrError) as e1:
+            kr.evaluate_partition(space, *d)
+        assert e1.value.status == kr.KR_ENONFINITE
+        with pytest.raises(kr.KrError) as e2:
+            kr.evaluate_and_filter(space, *d)
+        assert e2.value.status == kr.KR_ENONFINITE
+        kr.evaluate_and_filter(space, *d, validate=False)  # unchecked: runs, memory-safe
+        torch.cuda.synchronize()
+
+
+def test_negative_zero_table_entries_accepted(kr, oracle_lib):
+    """-0.0 counts as 0: a table with -0.0 comm powers passes the check and matches the
+    oracle on the same tables."""
+    space = dataclasses.replace(I.SPACES[0]["space"], n_parts=2)
+    tab = I.make_tables(space, seed=5, comm_bytes=(4e6, 64e6))
+    tab["pc"][:, :, :, ::3] = -0.0
+    d = [torch.from_numpy(tab[k]).cuda() for k in ("t", "pw", "tc", "pc")]
+    fr = kr.evaluate_and_filter(space, *d)
+    for p in range(space.n_parts):
+        Tr, Er = oracle_lib.evaluate_partition(space, tab["t"], tab["pw"], tab["tc"], tab["pc"], p)
+        ix = oracle_lib.pareto(Tr, Er)
+        check_frontier(fr, p, (ix, Tr[ix], Er[ix]), "-0 tables part %d" % p)
+
+
+@pytest.mark.parametrize("bad", ["nan_T", "inf_E", "neg_E", "nan_E", "neg_T"])
+def test_nonfinite_points_rejected(kr, bad):
+    """GetFrontier's input check: a NaN or infinite value or a negative one gives
+    KR_ENONFINITE; the composition flags non-finite times and energies that are not
+    finite values >= 0 in its status word and reports no staircase."""
+    rng = np.random.default_rng(9)
+    off = np.array([0, 40, 90, 130], dtype=np.int64)
+    T = rng.uniform(1e-3, 2e-3, 130)
+    E = rng.uniform(1.0, 2.0, 130)
+    x = 57
+    if bad == "nan_T":
+        T[x] = np.nan
+    elif bad == "inf_E":
+        E[x] = np.inf
+    elif bad == "neg_E":
+        E[x] = -1e-9
+    elif bad == "nan_E":
+        E[x] = np.nan
+    else:
+        T[x] = -1e-3
+    Td, Ed = torch.from_numpy(T).cuda(), torch.from_numpy(E).cuda()
+    with pytest.raises(kr.KrError) as e:
+        kr.pareto_filter(Td, Ed, off)
+    assert e.value.status == kr.KR_ENONFINITE
+    comp = kr.compose_frontiers(torch.from_numpy(off).cuda(), Td, Ed, 256)
+    if bad == "neg_T":  # a negative time is finite: composition only shifts by tmin
+        assert int(comp.status.item()) == kr.KR_OK
+    else:
+        assert int(comp.status.item()) == kr.KR_ENONFINITE
+        assert int(comp.n_stair.item()) == 0
+
+
+def test_negative_zero_energies(kr, oracle_lib):
+    """-0.0 energies are read as +0.0: GetFrontier and the composition keep the oracle's
+    points and back-pointers (the oracle compares -0.0 == +0.0)."""
+    rng = np.random.default_rng(10)
+    n = [30, 45, 12, 60]
+    off = np.concatenate([[0], np.cumsum(n)]).astype(np.int64)
+    T = rng.integers(1, 20, off[-1]) * 1e-4
+    E = rng.integers(0, 6, off[-1]) * 0.5
+    E[E == 0.0] = np.where(rng.random(int(np.sum(E == 0.0))) < 0.5, -0.0, 0.0)
+    assert np.any(np.signbit(E) & (E == 0.0))
+    fr = kr.pareto_filter(torch.from_numpy(T).cuda(), torch.from_numpy(E).cuda(), off)
+    for g in range(len(n)):
+        Tg, Eg = T[off[g]:off[g + 1]], E[off[g]:off[g + 1]]
+        ix = oracle_lib.pareto(Tg, Eg)
+        check_frontier(fr, g, (ix, Tg[ix], Eg[ix]), "-0 energies seg %d" % g)
+    comp = kr.compose_frontiers(torch.from_numpy(off).cuda(), torch.from_numpy(T).cuda(),
+                                torch.from_numpy(E).cuda(), 128)
+    ref = oracle_lib.compose(off, T, E, 128)
+    compare_composed(kr, comp, ref, off, T, E, "-0 energies")
