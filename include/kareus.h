@@ -151,6 +151,26 @@ kr_status kr_pareto_filter(int64_t n_total, const double *T, const double *E,
 size_t kr_pareto_filter_workspace(int64_t n_total, int32_t n_seg);
 
 /*
+ * kr_pareto_filter_noalloc -- kr_pareto_filter for callers that cannot allocate device
+ * memory or pass a workspace (code under HIP graph capture, tight serving loops, hosts
+ * that forbid allocation): the same call and results, with its workspace in a fixed
+ * array inside the library (KR_NOALLOC_SCRATCH_MIB MiB of device memory on each device
+ * the call runs on, held until the process ends; nothing is allocated per call).  The
+ * caller still passes inputs and outputs.  Limits: n_total <= KR_NOALLOC_MAX_POINTS and
+ * n_seg <= KR_NOALLOC_MAX_SEGS, else KR_ECAPACITY before any launch.  Every call on a
+ * device shares that device's array: calls that overlap on one device (two streams,
+ * two threads) race and must be serialised by the caller.  KR_EHIP if the array's
+ * device address cannot be obtained.
+ */
+#define KR_NOALLOC_MAX_POINTS (1 << 20)
+#define KR_NOALLOC_MAX_SEGS (1 << 16)
+#define KR_NOALLOC_SCRATCH_MIB 44
+kr_status kr_pareto_filter_noalloc(int64_t n_total, const double *T, const double *E,
+                                   const int64_t *seg_off, int32_t n_seg, int64_t cap,
+                                   int64_t *out_off, int32_t *out_idx, double *out_T,
+                                   double *out_E, int32_t *status_out, void *stream);
+
+/*
  * kr_evaluate_and_filter -- kr_evaluate_partition followed by kr_pareto_filter with
  * one segment per partition, fused: candidate T/E never reach device memory, only
  * tile-local frontiers do.  Arguments as in the two calls; out_idx holds candidate

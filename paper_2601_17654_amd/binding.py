@@ -41,6 +41,8 @@ _SIGS = {
     "kr_pareto_filter": (_i32, [_i64, _vp, _vp, _vp, _i32, _i64, _vp, _vp, _vp, _vp, _vp, _vp,
                                 _sz, _vp]),
     "kr_pareto_filter_workspace": (_sz, [_i64, _i32]),
+    "kr_pareto_filter_noalloc": (_i32, [_i64, _vp, _vp, _vp, _i32, _i64, _vp, _vp, _vp, _vp, _vp,
+                                        _vp]),
     "kr_evaluate_and_filter": (_i32, [_SP, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp,
                                       _vp, _sz, _vp]),
     "kr_evaluate_and_filter_workspace": (_sz, [_SP]),
@@ -202,10 +204,14 @@ def _finish_frontier(off, idx, T, E, cap, sync):
     return Frontier(off, idx[:total], T[:total], E[:total]), True
 
 
+NOALLOC_MAX_POINTS, NOALLOC_MAX_SEGS = 1 << 20, 1 << 16
+
+
 def pareto_filter(T, E, seg_off, cap: Optional[int] = None, sync: bool = True,
-                  validate: Optional[bool] = None) -> Frontier:
+                  validate: Optional[bool] = None, noalloc: bool = False) -> Frontier:
     """GetFrontier of every segment [seg_off[g], seg_off[g+1]) of (T, E).  validate
-    (default: sync) has the library check T and E, raising KrError(KR_ENONFINITE)."""
+    (default: sync) has the library check T and E, raising KrError(KR_ENONFINITE).
+    noalloc calls kr_pareto_filter_noalloc (library-held workspace, bounded sizes)."""
     seg_host = np.asarray(seg_off.cpu() if isinstance(seg_off, torch.Tensor) else seg_off,
                           dtype=np.int64)
     n_seg = len(seg_host) - 1
@@ -223,14 +229,21 @@ def pareto_filter(T, E, seg_off, cap: Optional[int] = None, sync: bool = True,
         idx = torch.empty(max(c, 1), dtype=torch.int32, device="cuda")
         oT = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
         oE = torch.empty(max(c, 1), dtype=torch.float64, device="cuda")
-        wsb = _lib.kr_pareto_filter_workspace(n_total, n_seg)
-        ws = _workspace(wsb)
         status = _status_word(sync if validate is None else validate)
-        _check("kr_pareto_filter",
-               _lib.kr_pareto_filter(n_total, _ptr(T), _ptr(E), _ptr(seg_dev), n_seg, c, _ptr(off),
-                                     _ptr(idx), _ptr(oT), _ptr(oE), _ptr(status), _ptr(ws), wsb,
-                                     _stream()))
-        _check_status("kr_pareto_filter", status)
+        if noalloc:
+            fn = "kr_pareto_filter_noalloc"
+            rc = _lib.kr_pareto_filter_noalloc(n_total, _ptr(T), _ptr(E), _ptr(seg_dev), n_seg, c,
+                                               _ptr(off), _ptr(idx), _ptr(oT), _ptr(oE),
+                                               _ptr(status), _stream())
+        else:
+            fn = "kr_pareto_filter"
+            wsb = _lib.kr_pareto_filter_workspace(n_total, n_seg)
+            ws = _workspace(wsb)
+            rc = _lib.kr_pareto_filter(n_total, _ptr(T), _ptr(E), _ptr(seg_dev), n_seg, c,
+                                       _ptr(off), _ptr(idx), _ptr(oT), _ptr(oE), _ptr(status),
+                                       _ptr(ws), wsb, _stream())
+        _check(fn, rc)
+        _check_status(fn, status)
         fr, ok = _finish_frontier(off, idx, oT, oE, c, sync)
         if fr is not None:
             return fr

@@ -17,7 +17,7 @@ LIB = os.path.join(HERE, "libkareus_mi355x.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["api.hip", "check.hip", "eval.hip", "eval_wave.hip", "pareto.hip", "compose.hip", "microbatch.hip",
            "mbo.hip", "metrics.hip",
-           "launch_dp.hip"]
+           "launch_dp.hip", "noalloc.hip"]
 FLAGS = [
     "--offload-arch=gfx950",
     "-O3",
