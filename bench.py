@@ -13,7 +13,8 @@ the library's stream); `frontier_cells_per_s` is the composition's DP cells (sum
 partitions of the reachable bins) over step 2's time.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--skip-cpu]
-       python bench.py --part eval|compose   (one half only, no bench line: for profilers)
+       python bench.py --part eval|compose|eval2|mbo|dp   (one leg only, no bench line: for
+                                                           profilers)
        python bench.py --copy-calibration   (plain 1 GiB device copy, for counters)
 """
 
@@ -63,6 +64,55 @@ def kernel_source_hash() -> str:
     h.update(_between(api, "bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)",
                       "\n}\n").encode())
     return h.hexdigest()[:16]
+
+
+def read_summary(path: str, source_hash: str):
+    """key=value pairs of a committed counter summary, or None when it is missing or
+    was taken on sources that hash differently from today's."""
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.split("#", 1)[0].strip().split("=", 1)
+            vals[k.strip()] = v.strip()
+    return vals if vals.get("source_hash") == source_hash else None
+
+
+def minplus_source_hash() -> str:
+    """sha256 (first 16 hex) of what the composition kernels are built and launched from."""
+    csrc = os.path.join(ROOT, "paper_2601_17654_amd", "csrc")
+    h = hashlib.sha256()
+    for f in ("compose.hip", "kr_device.h"):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    with open(os.path.join(csrc, "kr_launch.h")) as fh:
+        lh = fh.read()
+    h.update(_between(lh, "struct ComposeArgs {", "\n};\n").encode())
+    h.update(_between(lh, "struct ComposeWs {", "\n};\n").encode())
+    with open(os.path.join(csrc, "api.hip")) as fh:
+        h.update(_between(fh.read(), "kr_status kr_compose_frontiers(", "\n}\n").encode())
+    return h.hexdigest()[:16]
+
+
+def eval2_source_hash() -> str:
+    """sha256 (first 16 hex) of what the block-per-slab evaluation kernel (two comm
+    kernels) is built from and planned by."""
+    csrc = os.path.join(ROOT, "paper_2601_17654_amd", "csrc")
+    h = hashlib.sha256()
+    for f in ("eval.hip", "kr_filter.h", "kr_device.h"):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    with open(os.path.join(csrc, "kr_launch.h")) as fh:
+        h.update(_between(fh.read(), "struct EvalArgs {", "\n};\n").encode())
+    with open(os.path.join(csrc, "api.hip")) as fh:
+        h.update(_between(fh.read(), "bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)",
+                          "\n}\n").encode())
+    return h.hexdigest()[:16]
+
+
+MINPLUS_COUNTERS = os.path.join(ROOT, "profiles", "minplus_counters_compose_stress.txt")
+EVAL2_COUNTERS = os.path.join(ROOT, "profiles", "eval_two_comm_counters.txt")
 
 
 MBO_COUNTERS = os.path.join(ROOT, "profiles", "mbo_counters_eval_stress.txt")
@@ -169,7 +219,8 @@ def main():
     ap.add_argument("--skip-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true")
-    ap.add_argument("--part", choices=["all", "eval", "compose", "mbo", "dp"], default="all",
+    ap.add_argument("--part", choices=["all", "eval", "compose", "eval2", "mbo", "dp"],
+                    default="all",
                     help="profiling aid: run only one half of the step (prints no bench line)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -204,6 +255,10 @@ def main():
     comp = kr.compose_frontiers(off4_d, T4_d, E4_d, B)
     torch.cuda.synchronize()
 
+    if args.part == "eval2":
+        res, _ = bench_eval2(kr, I, torch, args, mk_events)
+        log("eval2: " + json.dumps(res))
+        return
     if args.part == "dp":
         res, _ = bench_dp(kr, I, torch, args, mk_events)
         log("dp: " + json.dumps(res))
@@ -272,6 +327,29 @@ def main():
             "kernel_ms": round(kern_ms, 4), "algorithmic_bytes": table_bytes,
             "traffic_source": tsrc}
 
+    # composition: the min-plus step for partition k pairs each of the L_{k-1} bins
+    # reachable after the partitions before it with each occupied bin of its own
+    # frontier; VALU instruction counts come from the committed counter summary
+    pairs = 0
+    reach = 1 + int(Mk[0])
+    for k in range(1, len(Mk)):
+        occ = len(np.unique(pt[off4[k]:off4[k + 1]]))
+        pairs += min(reach, B) * occ
+        reach += int(Mk[k])
+    mpc = read_summary(MINPLUS_COUNTERS, minplus_source_hash())
+    croof = {"bound": "alu", "kernel": "minplus_wavefront_kernel (min-plus steps, tiles of "
+             "bins taken by ticket)", "kernel_ms": round(mp_ms, 4), "pairs": pairs,
+             "pairs_per_s": pairs / (mp_ms * 1e-3), "peak": VALU_ISSUE_PEAK / 1e9,
+             "unit": "G VALU wave-instructions/s", "achieved": None, "frac": None,
+             "source": "kernel changed since counters were taken" if mpc is None else
+             "profiles/minplus_counters_compose_stress.txt"}
+    if mpc is not None:
+        vi = float(mpc["valu_wave_instructions_per_launch"]) / (mp_ms * 1e-3)
+        croof.update(achieved=round(vi / 1e9, 2), frac=round(vi / VALU_ISSUE_PEAK, 4),
+                     valu_busy=float(mpc["valu_busy"]),
+                     valu_per_pair_lane=round(64 * float(mpc["valu_wave_instructions_per_launch"])
+                                              / pairs, 2))
+
     valu = read_valu()
     if valu is not None:
         vi = valu[0] / (kern_ms * 1e-3)
@@ -307,6 +385,7 @@ def main():
         "minplus_ms": round(mp_ms, 4),
         "extract_ms": round(ex_ms, 4),
         "roofline": roof,
+        "compose_roofline": croof,
     }
 
     # Microbatch frontier (Algorithm 2 with one frequency per microbatch and one
@@ -396,6 +475,11 @@ def main():
         import oracle
 
         oracle.build(force=False)
+        # the single-threaded legs run on one core: this thread is pinned to the first CPU
+        # it may use, and the mask is restored for the partition-parallel leg
+        all_cpus = os.sched_getaffinity(0)
+        pin_cpu = min(all_cpus)
+        os.sched_setaffinity(0, {pin_cpu})
         t0 = time.perf_counter()
         n = 0
         mism = 0
@@ -416,7 +500,8 @@ def main():
         # the interpreter lock), over the batch from its first partition
         import concurrent.futures as cfu
 
-        nthreads = os.cpu_count() or 1
+        os.sched_setaffinity(0, all_cpus)  # worker threads inherit the mask of this thread
+        nthreads = len(all_cpus)
 
         def one(q):
             T, E = oracle.evaluate_partition(sp, w.t, w.pw, w.tc, w.pc, q)
@@ -437,6 +522,7 @@ def main():
                 f.result()
                 done += 1
         el = time.perf_counter() - t0
+        os.sched_setaffinity(0, {pin_cpu})
         out["cpu_baseline_parallel"] = {
             "value": done * sp.n_cand / el, "unit": "candidates/s", "cores": nthreads,
             "kind": "oracle",
@@ -491,14 +577,18 @@ def main():
             "parity": bool(np.array_equal(rc, cm, equal_nan=True))}
         out["launch_timing"]["cpu_baseline"] = dp_cpu_baseline(oracle, dp_ctx, args.cpu_seconds)
         out["eval_two_comm"]["cpu_baseline"] = eval2_cpu_baseline(oracle, e2_ctx, args.cpu_seconds)
-        host = host_info()
+        os.sched_setaffinity(0, all_cpus)
+        host = host_info(pin_cpu)
         for k in ("cpu_baseline", "cpu_baseline_compose"):
             out[k]["host"] = host
     print(json.dumps(out))
 
 
-def host_info():
-    """CPU model, logical CPUs and the oracle's compiler flags."""
+def host_info(pin_cpu):
+    """CPU model, logical CPUs, the core the single-threaded legs ran on, and the
+    oracle's compiler with its version and flags."""
+    import subprocess
+
     model = "unknown"
     try:
         for line in open("/proc/cpuinfo"):
@@ -509,8 +599,15 @@ def host_info():
         pass
     import oracle
 
+    try:
+        gcc = subprocess.run(["gcc", "--version"], capture_output=True, text=True,
+                             timeout=30).stdout.splitlines()[0]
+    except (OSError, IndexError, subprocess.SubprocessError):
+        gcc = "unknown"
     return {"cpu": model, "logical_cpus": os.cpu_count(),
-            "oracle_build": "gcc " + " ".join(oracle.CFLAGS), "threads_used": 1}
+            "usable_cpus": len(os.sched_getaffinity(0)), "pinned_cpu": pin_cpu,
+            "compiler": gcc, "oracle_build": "gcc " + " ".join(oracle.CFLAGS),
+            "threads_used": 1}
 
 
 def bench_eval2(kr, I, torch, args, mk):
@@ -526,17 +623,38 @@ def bench_eval2(kr, I, torch, args, mk):
     torch.cuda.synchronize()
     steps = max(3, args.steps // 4)
     ev = mk(2 * steps)
+    kev = [mk(2) for _ in range(steps)]
+    torch.cuda.synchronize()
     for k in range(steps):
+        kr.set_phase_events(kr.PHASE_EVAL_TILE, *kev[k])
         ev[2 * k].record()
         fr = kr.evaluate_and_filter(sp2, *d2, cap=cap, sync=False)
         ev[2 * k + 1].record()
     torch.cuda.synchronize()
+    kr.set_phase_events(kr.PHASE_EVAL_TILE)
     ms = sorted(ev[2 * k].elapsed_time(ev[2 * k + 1]) for k in range(steps))
+    kms = float(np.median([e[0].elapsed_time(e[1]) for e in kev]))
     n = sp2.n_parts * sp2.n_cand
+    nbytes = sum(x.numel() * 8 for x in d2)
+    c2 = read_summary(EVAL2_COUNTERS, eval2_source_hash())
+    roof = {"bound": "alu", "kernel": "eval_filter_kernel<2,8,false> (block per slab, two "
+            "comm kernels)", "kernel_ms": round(kms, 4), "peak": VALU_ISSUE_PEAK / 1e9,
+            "unit": "G VALU wave-instructions/s", "achieved": None, "frac": None,
+            "hbm_GBps": round(nbytes / (kms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(nbytes / (kms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "algorithmic_bytes": nbytes,
+            "source": "kernel changed since counters were taken" if c2 is None else
+            "profiles/eval_two_comm_counters.txt"}
+    if c2 is not None:
+        vi = float(c2["valu_wave_instructions_per_launch"]) / (kms * 1e-3)
+        roof.update(achieved=round(vi / 1e9, 2), frac=round(vi / VALU_ISSUE_PEAK, 4),
+                    valu_busy=float(c2["valu_busy"]),
+                    valu_per_wave_candidate=round(64 * float(c2["valu_wave_instructions_per_launch"])
+                                                  / n, 1))
     res = {"workload": "two-comm (256 partitions x 1,148,928 candidates: 48 kernels, 561 "
                        "launch-position pairs, 8 x 8 SM choices, 32 frequencies)",
            "candidates": n, "frontier_points": cap, "call_ms_median": round(ms[len(ms) // 2], 4),
-           "candidates_per_s": n / (ms[len(ms) // 2] * 1e-3)}
+           "candidates_per_s": n / (ms[len(ms) // 2] * 1e-3), "roofline": roof}
     return res, dict(w=w2, fr=fr)
 
 

@@ -486,7 +486,9 @@ kr_status kr_decode_candidates(const kr_space *space, const int32_t *idx, int64_
  * method).  When both events are non-NULL, later calls record `start_event` on their
  * stream right before the phase's first kernel and `stop_event` right after its last
  * one; NULL events switch the phase's recording off.  Events are hipEvent_t handles
- * owned by the caller.  Library-global setting, not thread-safe.
+ * owned by the caller, who must switch the phase off (NULL, NULL) before destroying
+ * them.  The setting is per host thread: it applies to later calls made from the
+ * thread that set it, and no other thread sees it.
  *   KR_PHASE_EVAL_TILE  the fused evaluation + tile-frontier kernel of
  *                       kr_evaluate_and_filter
  *   KR_PHASE_MERGE      its staircase merges and output compaction

@@ -1,7 +1,6 @@
 // C ABI of libkareus_mi355x.so: argument checks, workspace layout and launch order.
 // Declarations and contracts: include/kareus.h.
 #include <algorithm>
-#include <cstdlib>
 #include <cstring>
 
 #include "../../include/kareus.h"
@@ -84,41 +83,6 @@ bool wave_plan(EvalArgs *a)
     return true;
 }
 
-// One comm kernel and 32 SM choices: one 128-thread block per slab with the running-sum
-// tables in LDS.  The walk positions (all of them, or all but position N when n_pos =
-// N + 1, which the closed form takes) form 8 runs of span; thread (s, g) takes SM choice
-// s and runs g and g + 4.
-bool table_plan(EvalArgs *a)
-{
-    constexpr int kS = 32, kRuns = 8;
-    if (a->M != 1 || a->S != kS) return false;
-    const int64_t rs = a->N + 1 + 4;
-    // AB, TPW, D0 and the output list (KR_TB_OL entries of 20 bytes)
-    const int64_t lds =
-        2 * (a->S + 1) * rs + 2 * (a->S + 1) * (a->N + 1) + 2 * (a->N + 2) + 96 * 20 / 8;
-    if ((size_t)lds * 8 > kLdsBudget) return false;
-    const int64_t ne = ((int64_t)a->N * (a->S + 1) + 127) / 128;
-    a->tclosed = a->n_pos == a->N + 1 ? 1 : 0;
-    a->tq = a->n_pos - a->tclosed;
-    a->span = (a->tq + kRuns - 1) / kRuns;
-    if (ne > 9 || a->tq < 1 || a->span > 5) return false;
-    a->table = 1;
-    a->lds_doubles = (int)lds;
-    // test-only switch: a smaller list (1 .. 96 entries) sends outputs to device memory
-    // sooner, so tests can reach that path with small inputs
-    a->tb_ol = 96;
-    if (const char *e = std::getenv("KR_TEST_TABLE_LIST"))
-        a->tb_ol = std::max(1, std::min(96, std::atoi(e)));
-    // a few times more blocks than fit on the chip at once (LDS-limited)
-    const int64_t resident = std::max<int64_t>(1, std::min<int64_t>(8, kLdsPerCu / (lds * 8 + 512)));
-    const int64_t target = 16 * 256 * resident;
-    int64_t nfb = std::max<int64_t>(1, (target + a->P - 1) / a->P);
-    nfb = std::min<int64_t>(nfb, a->F);
-    a->fb = (int)((a->F + nfb - 1) / nfb);
-    a->nfb = (a->F + a->fb - 1) / a->fb;
-    return true;
-}
-
 // Shape of the evaluation launch; false if the slab does not fit on chip.
 bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)
 {
@@ -136,7 +100,7 @@ bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)
     a->C = cf * s->n_freq;
     a->p_static = s->p_static;
     const int64_t S1 = a->S + 1;
-    if (fused && (table_plan(a) || wave_plan(a))) return true;
+    if (fused && wave_plan(a)) return true;
     const int64_t staged = 2 * a->N * S1 + 2 * a->M * a->S;  // t, pw, tc, pc
     const int64_t sums = 2 * (a->N + 1) * S1;
     const int64_t pairs = a->M == 2 ? (a->n_pp * 4 + 7) / 8 : 0;
@@ -187,8 +151,9 @@ hipError_t check_tables(const kr_space *s, const double *t, const double *pw, co
     return launch_check(xs, n, 4, status, st);
 }
 
-// Caller-owned events recorded around a phase (kr_set_phase_events).
-hipEvent_t g_phase_ev[6][2] = {};
+// Caller-owned events recorded around a phase (kr_set_phase_events), one setting per
+// host thread: a call reads only its own thread's entries, so threads never race on them.
+thread_local hipEvent_t g_phase_ev[6][2] = {};
 
 void phase_mark(int phase, int which, hipStream_t st)
 {
@@ -339,9 +304,7 @@ kr_status kr_evaluate_and_filter(const kr_space *space, const double *t, const d
     if (status_out && check_tables(space, t, pw, tc, pc, status_out, st) != hipSuccess)
         return KR_EHIP;
     phase_mark(KR_PHASE_EVAL_TILE, 0, st);
-    const hipError_t le = a.table  ? launch_eval_filter_table(a, o, st)
-                          : a.wave ? launch_eval_filter_wave(a, o, st)
-                                   : launch_eval_filter(a, o, st);
+    const hipError_t le = a.wave ? launch_eval_filter_wave(a, o, st) : launch_eval_filter(a, o, st);
     if (le != hipSuccess) return KR_EHIP;
     phase_mark(KR_PHASE_EVAL_TILE, 1, st);
     SegLayout L;

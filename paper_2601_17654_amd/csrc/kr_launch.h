@@ -35,11 +35,6 @@ struct EvalArgs {
     int w_pw, w_a0;         // LDS offsets (doubles) of the power slab and the column sums
     int dma16;              // 16-byte direct copies (slab length even, tables 16-byte aligned)
     int wcap;               // candidates the wave filter's LDS scratch holds
-    // one block per slab with running-sum tables (one comm kernel, 32 SM choices):
-    // tq walk positions in 8 runs of span (the last runs may repeat position tq - 1), and
-    // tclosed: position N (= tq) taken by the closed form
-    int table, tq, tclosed;
-    int tb_ol;              // filter outputs the table kernel keeps in LDS per block
 };
 
 // Per-unit frontiers written by the fused kernel or the tile kernel.
@@ -73,7 +68,6 @@ struct PointBufs {
 hipError_t launch_eval(const EvalArgs &a, hipStream_t st);
 hipError_t launch_eval_filter(const EvalArgs &a, const UnitOut &o, hipStream_t st);
 hipError_t launch_eval_filter_wave(const EvalArgs &a, const UnitOut &o, hipStream_t st);
-hipError_t launch_eval_filter_table(const EvalArgs &a, const UnitOut &o, hipStream_t st);
 hipError_t launch_decode(const DecodeArgs &d, hipStream_t st);
 
 // pareto.hip

@@ -629,10 +629,10 @@ def test_negative_zero_energies(kr, oracle_lib):
 @pytest.mark.parametrize("shape", [(32, 33, 5), (8, 9, 3), (20, 17, 2), (35, 36, 2), (40, 41, 2),
                                    (12, 8, 4), (1, 2, 3)])
 @pytest.mark.parametrize("tc_scale", [1.0, 1e-3, 30.0])
-def test_table_kernel_shapes(kr, oracle_lib, shape, tc_scale):
-    """One comm kernel with 32 SM choices (the running-sum table kernel, eight runs of
-    launch positions per SM choice, the last run taking the rest): kernel counts 1 to 40,
-    launch positions from 2 to N + 1, short and long comm, against the oracle."""
+def test_fused_32_sm_choices_shapes(kr, oracle_lib, shape, tc_scale):
+    """One comm kernel with 32 SM choices (the SM-choice count of the evaluation stress
+    workload): kernel counts 1 to 40, launch positions from 2 to N + 1, short and long
+    comm, every partition's fused frontier against the oracle."""
     N, n_pos, F = shape
     K = tuple(range(1, 33))
     freqs = tuple(1005.0 + 975.0 * q / max(F - 1, 1) for q in range(F))
@@ -644,18 +644,13 @@ def test_table_kernel_shapes(kr, oracle_lib, shape, tc_scale):
     for p in range(space.n_parts):
         Tr, Er = oracle_lib.evaluate_partition(space, tab["t"], tab["pw"], tab["tc"], tab["pc"], p)
         ix = oracle_lib.pareto(Tr, Er)
-        check_frontier(fr, p, (ix, Tr[ix], Er[ix]), "table %s x%g part %d" % (shape, tc_scale, p))
+        check_frontier(fr, p, (ix, Tr[ix], Er[ix]), "S=32 %s x%g part %d" % (shape, tc_scale, p))
 
 
-@pytest.mark.parametrize("list_cap", [None, "3", "40"])
-def test_table_kernel_many_box_members(kr, oracle_lib, monkeypatch, list_cap):
+def test_fused_many_box_members(kr, oracle_lib):
     """32 SM choices with comm time dominating and comm energy falling steeply with comm
-    time: most candidates are frontier points (thousands per partition).  With the
-    test-only switch KR_TEST_TABLE_LIST the table kernel keeps only that many filter
-    outputs per block in LDS and sends the rest to device memory, where they are sorted
-    with the list at the block's end."""
-    if list_cap is not None:
-        monkeypatch.setenv("KR_TEST_TABLE_LIST", list_cap)
+    time: most candidates are frontier points (thousands per partition), so the fused
+    filter's per-wave outputs overflow every on-chip list."""
     space = I.Space(2, 4, 1, 5, tuple(range(1, 33)), tuple(1005.0 + 15.0 * j for j in range(64)),
                     p_static=0.0)
     tab = I.make_tables(space, seed=23, comm_bytes=(4e6, 64e6))
