@@ -96,18 +96,20 @@ def minplus_source_hash() -> str:
 
 
 def eval2_source_hash() -> str:
-    """sha256 (first 16 hex) of what the block-per-slab evaluation kernel (two comm
-    kernels) is built from and planned by."""
+    """sha256 (first 16 hex) of what the one-wave-per-slab two-comm evaluation kernel is
+    built from and planned by."""
     csrc = os.path.join(ROOT, "paper_2601_17654_amd", "csrc")
     h = hashlib.sha256()
-    for f in ("eval.hip", "kr_filter.h", "kr_device.h"):
+    for f in ("eval_pair.hip", "kr_wave.h", "kr_filter.h", "kr_device.h"):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(fh.read())
     with open(os.path.join(csrc, "kr_launch.h")) as fh:
         h.update(_between(fh.read(), "struct EvalArgs {", "\n};\n").encode())
     with open(os.path.join(csrc, "api.hip")) as fh:
-        h.update(_between(fh.read(), "bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)",
-                          "\n}\n").encode())
+        api = fh.read()
+    h.update(_between(api, "bool pair_plan(EvalArgs *a)", "\n}\n").encode())
+    h.update(_between(api, "bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)",
+                      "\n}\n").encode())
     return h.hexdigest()[:16]
 
 
@@ -637,8 +639,8 @@ def bench_eval2(kr, I, torch, args, mk):
     n = sp2.n_parts * sp2.n_cand
     nbytes = sum(x.numel() * 8 for x in d2)
     c2 = read_summary(EVAL2_COUNTERS, eval2_source_hash())
-    roof = {"bound": "alu", "kernel": "eval_filter_kernel<2,8,false> (block per slab, two "
-            "comm kernels)", "kernel_ms": round(kms, 4), "peak": VALU_ISSUE_PEAK / 1e9,
+    roof = {"bound": "alu", "kernel": "eval_filter_pair_kernel<8,16> (one wave per slab, "
+            "two comm kernels)", "kernel_ms": round(kms, 4), "peak": VALU_ISSUE_PEAK / 1e9,
             "unit": "G VALU wave-instructions/s", "achieved": None, "frac": None,
             "hbm_GBps": round(nbytes / (kms * 1e-3) / 1e9, 1),
             "hbm_frac": round(nbytes / (kms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),

@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libkareus_mi355x.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-SOURCES = ["api.hip", "check.hip", "eval.hip", "eval_wave.hip", "pareto.hip", "compose.hip", "microbatch.hip",
+SOURCES = ["api.hip", "check.hip", "eval.hip", "eval_wave.hip", "eval_pair.hip", "pareto.hip", "compose.hip", "microbatch.hip",
            "mbo.hip", "metrics.hip",
            "launch_dp.hip", "noalloc.hip"]
 FLAGS = [

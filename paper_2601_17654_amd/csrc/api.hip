@@ -1,6 +1,7 @@
 // C ABI of libkareus_mi355x.so: argument checks, workspace layout and launch order.
 // Declarations and contracts: include/kareus.h.
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 
 #include "../../include/kareus.h"
@@ -83,6 +84,37 @@ bool wave_plan(EvalArgs *a)
     return true;
 }
 
+// Two comm kernels and at most 8 SM choices: one wave per slab, lane (s1, s2).
+bool pair_plan(EvalArgs *a)
+{
+    if (a->M != 2 || a->S > 8) return false;
+    const int64_t S1 = a->S + 1;
+    const int64_t slab16 = ((int64_t)a->N * S1 + 1) / 2 * 2;
+    a->q_pw = (int)slab16;
+    a->q_ab = (int)(2 * slab16);
+    a->q_f = (int)(a->q_ab + 2 * (a->N + 1) * S1);  // {A, B} records
+    a->q_c = (int)(a->q_f + 6 * (int64_t)a->n_pos * a->S);  // 6-double records
+    a->q_sc = a->q_c + 6 * 64;
+    const int64_t lds = a->q_sc + 64 + 64 + 32;  // scratch T, E, indices
+    if ((size_t)lds * 8 > kLdsBudget) return false;
+    a->pair = 1;
+    a->lds_doubles = (int)lds;
+    // the slab-end reduction sorts in the second-phase tables (20 bytes per point); a
+    // test-only switch lowers the cap (0: never), so tests reach the unreduced path
+    a->pair_scap = (a->q_sc - a->q_f) * 8 / 20;
+    if (const char *e = std::getenv("KR_TEST_PAIR_SORT_CAP"))
+        a->pair_scap = std::max(0, std::min(a->pair_scap, std::atoi(e)));
+    // a slab is tens of thousands of candidates: one wave per slab unless there are too
+    // few slabs to fill the chip a few times over
+    const int64_t resident = std::max<int64_t>(1, std::min<int64_t>(16, kLdsPerCu / (lds * 8)));
+    const int64_t target = 4 * 256 * resident;
+    int64_t nfb = std::max<int64_t>(1, (target + a->P - 1) / a->P);
+    nfb = std::min<int64_t>(nfb, a->F);
+    a->fb = (int)((a->F + nfb - 1) / nfb);
+    a->nfb = (a->F + a->fb - 1) / a->fb;
+    return true;
+}
+
 // Shape of the evaluation launch; false if the slab does not fit on chip.
 bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)
 {
@@ -100,7 +132,7 @@ bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)
     a->C = cf * s->n_freq;
     a->p_static = s->p_static;
     const int64_t S1 = a->S + 1;
-    if (fused && wave_plan(a)) return true;
+    if (fused && (wave_plan(a) || pair_plan(a))) return true;
     const int64_t staged = 2 * a->N * S1 + 2 * a->M * a->S;  // t, pw, tc, pc
     const int64_t sums = 2 * (a->N + 1) * S1;
     const int64_t pairs = a->M == 2 ? (a->n_pp * 4 + 7) / 8 : 0;
@@ -299,12 +331,14 @@ kr_status kr_evaluate_and_filter(const kr_space *space, const double *t, const d
     if (launch_uniform_layout(w.seg_off, w.unit_base, a.P, a.C, a.nfb, st) != hipSuccess)
         return KR_EHIP;
     UnitOut o{w.buf[0].T, w.buf[0].E, w.buf[0].I, w.ucnt};
-    a.dma16 = a.wave && (a.N * (a.S + 1)) % 2 == 0 && (uintptr_t)t % 16 == 0 &&
+    a.dma16 = (a.wave || a.pair) && (a.N * (a.S + 1)) % 2 == 0 && (uintptr_t)t % 16 == 0 &&
               (uintptr_t)pw % 16 == 0;
     if (status_out && check_tables(space, t, pw, tc, pc, status_out, st) != hipSuccess)
         return KR_EHIP;
     phase_mark(KR_PHASE_EVAL_TILE, 0, st);
-    const hipError_t le = a.wave ? launch_eval_filter_wave(a, o, st) : launch_eval_filter(a, o, st);
+    const hipError_t le = a.wave   ? launch_eval_filter_wave(a, o, st)
+                          : a.pair ? launch_eval_filter_pair(a, o, st)
+                                   : launch_eval_filter(a, o, st);
     if (le != hipSuccess) return KR_EHIP;
     phase_mark(KR_PHASE_EVAL_TILE, 1, st);
     SegLayout L;

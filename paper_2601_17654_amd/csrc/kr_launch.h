@@ -35,6 +35,12 @@ struct EvalArgs {
     int w_pw, w_a0;         // LDS offsets (doubles) of the power slab and the column sums
     int dma16;              // 16-byte direct copies (slab length even, tables 16-byte aligned)
     int wcap;               // candidates the wave filter's LDS scratch holds
+    // one wave per slab (two comm kernels, at most 8 SM choices): LDS offsets (doubles)
+    // of the power slab, the running sums, the fresh and continuing second-phase
+    // records and the filter scratch
+    int pair;
+    int q_pw, q_ab, q_f, q_c, q_sc;
+    int pair_scap;          // most chunk outputs of a slab reduced to its frontier on chip
 };
 
 // Per-unit frontiers written by the fused kernel or the tile kernel.
@@ -68,6 +74,7 @@ struct PointBufs {
 hipError_t launch_eval(const EvalArgs &a, hipStream_t st);
 hipError_t launch_eval_filter(const EvalArgs &a, const UnitOut &o, hipStream_t st);
 hipError_t launch_eval_filter_wave(const EvalArgs &a, const UnitOut &o, hipStream_t st);
+hipError_t launch_eval_filter_pair(const EvalArgs &a, const UnitOut &o, hipStream_t st);
 hipError_t launch_decode(const DecodeArgs &d, hipStream_t st);
 
 // pareto.hip

@@ -79,10 +79,15 @@ def small_spaces():
     # two register chunks per frequency
     spaces.append(I.Space(2, 32, 1, 33, tuple(range(1, 41)), (1005.0, 1500.0, 1980.0)))
     spaces.append(I.Space(2, 32, 1, 33, tuple(range(2, 98, 2)), (1005.0, 1980.0)))
+    # two comm kernels beyond the one-wave kernel's reach (more than 8 SM choices, or a
+    # slab whose tables do not fit its LDS): the block-per-slab kernel
+    spaces.append(I.Space(2, 9, 2, 10, tuple(range(1, 10)), (1005.0, 1980.0)))
+    spaces.append(I.Space(2, 6, 2, 7, tuple(range(2, 26, 2)), (1500.0,)))
+    spaces.append(I.Space(1, 206, 2, 5, tuple(range(2, 18, 2)), (1500.0,)))
     return spaces
 
 
-@pytest.mark.parametrize("case", range(16))
+@pytest.mark.parametrize("case", range(19))
 @pytest.mark.parametrize("tc_scale", [1.0, 1e-3, 1e3])
 def test_evaluate_small_spaces(kr, oracle_lib, case, tc_scale):
     space = small_spaces()[case]
@@ -667,3 +672,25 @@ def test_fused_many_box_members(kr, oracle_lib):
         sizes.append(len(ix))
         check_frontier(fr, p, (ix, Tr[ix], Er[ix]), "many box members part %d" % p)
     assert min(sizes) > 1000
+
+
+@pytest.mark.parametrize("sort_cap", [None, "0", "5", "40"])
+def test_two_comm_slab_reduction(kr, oracle_lib, monkeypatch, sort_cap):
+    """Two comm kernels with at most 8 SM choices (one wave per slab): each slab's chunk
+    frontiers are reduced to the slab's frontier on chip when they fit the sort room.
+    The test-only switch KR_TEST_PAIR_SORT_CAP lowers that room (0: never reduce), so
+    slabs with more chunk outputs keep them all and the merge after the kernel sees
+    them; every partition's frontier against the oracle either way."""
+    if sort_cap is not None:
+        monkeypatch.setenv("KR_TEST_PAIR_SORT_CAP", sort_cap)
+    for k, space in enumerate([I.Space(4, 24, 2, 17, tuple(range(4, 36, 4)), (1005.0, 1500.0, 1980.0)),
+                               I.Space(3, 7, 2, 8, (2, 5, 9), (1200.0, 1700.0))]):
+        tab = I.make_tables(space, seed=40 + k, comm_bytes=(8e6, 512e6))
+        d = [torch.from_numpy(tab[x]).cuda() for x in ("t", "pw", "tc", "pc")]
+        fr = kr.evaluate_and_filter(space, *d)
+        for p in range(space.n_parts):
+            Tr, Er = oracle_lib.evaluate_partition(space, tab["t"], tab["pw"], tab["tc"],
+                                                   tab["pc"], p)
+            ix = oracle_lib.pareto(Tr, Er)
+            check_frontier(fr, p, (ix, Tr[ix], Er[ix]), "cap %s space %d part %d" % (sort_cap, k, p))
+
