@@ -94,24 +94,32 @@ bool pair_plan(EvalArgs *a)
     a->q_ab = (int)(2 * slab16);
     a->q_f = (int)(a->q_ab + 2 * (a->N + 1) * S1);  // {A, B} records
     a->q_c = (int)(a->q_f + 6 * (int64_t)a->n_pos * a->S);  // 6-double records
-    a->q_sc = a->q_c + 6 * 64;
-    const int64_t lds = a->q_sc + 64 + 64 + 32;  // scratch T, E, indices
+    a->q_sc = a->q_c + 2 * 6 * 64;                           // one set per wave
+    const int64_t lds = a->q_sc + 2 * (64 + 64 + 32);        // scratch T, E, indices per wave
     if ((size_t)lds * 8 > kLdsBudget) return false;
     a->pair = 1;
     a->lds_doubles = (int)lds;
-    // the slab-end reduction sorts in the second-phase tables (20 bytes per point); a
-    // test-only switch lowers the cap (0: never), so tests reach the unreduced path
-    a->pair_scap = (a->q_sc - a->q_f) * 8 / 20;
+    // each wave's slab-end reduction sorts in its half of the second-phase tables (20
+    // bytes per point); a test-only switch lowers the cap (0: never), so tests reach the
+    // unreduced path
+    a->pair_scap = (a->q_sc - a->q_f) / 2 * 8 / 20;
     if (const char *e = std::getenv("KR_TEST_PAIR_SORT_CAP"))
         a->pair_scap = std::max(0, std::min(a->pair_scap, std::atoi(e)));
-    // a slab is tens of thousands of candidates: one wave per slab unless there are too
-    // few slabs to fill the chip a few times over
+    // a slab is tens of thousands of candidates: one block per slab unless there are too
+    // few slabs to fill the chip many times over (short tails)
     const int64_t resident = std::max<int64_t>(1, std::min<int64_t>(16, kLdsPerCu / (lds * 8)));
-    const int64_t target = 4 * 256 * resident;
+    const int64_t target = 8 * 256 * resident;
     int64_t nfb = std::max<int64_t>(1, (target + a->P - 1) / a->P);
     nfb = std::min<int64_t>(nfb, a->F);
     a->fb = (int)((a->F + nfb - 1) / nfb);
     a->nfb = (a->F + a->fb - 1) / a->fb;
+    // two units per block, wave w holding the pairs whose p1 has parity w: a unit's slot
+    // holds every candidate the larger half has in fb slabs
+    int64_t half[2] = {0, 0};
+    for (int p1 = 0; p1 < a->n_pos; ++p1) half[p1 & 1] += a->n_pos - p1;
+    a->uper = 2 * (int64_t)a->nfb;
+    a->ustride = (int64_t)a->fb * std::max(half[0], half[1]) * a->S * a->S;
+    a->useg = a->uper * a->ustride;
     return true;
 }
 
@@ -132,7 +140,13 @@ bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)
     a->C = cf * s->n_freq;
     a->p_static = s->p_static;
     const int64_t S1 = a->S + 1;
-    if (fused && (wave_plan(a) || pair_plan(a))) return true;
+    if (fused && wave_plan(a)) {
+        a->useg = a->C;
+        a->uper = a->nfb;
+        a->ustride = (int64_t)a->fb * a->Cf;
+        return true;
+    }
+    if (fused && pair_plan(a)) return true;
     const int64_t staged = 2 * a->N * S1 + 2 * a->M * a->S;  // t, pw, tc, pc
     const int64_t sums = 2 * (a->N + 1) * S1;
     const int64_t pairs = a->M == 2 ? (a->n_pp * 4 + 7) / 8 : 0;
@@ -169,6 +183,9 @@ bool eval_plan(const kr_space *s, bool fused, EvalArgs *a)
     nfb = std::min<int64_t>(nfb, a->F);
     a->fb = (int)((a->F + nfb - 1) / nfb);
     a->nfb = (a->F + a->fb - 1) / a->fb;
+    a->useg = a->C;
+    a->uper = a->nfb;
+    a->ustride = (int64_t)a->fb * a->Cf;
     return true;
 }
 
@@ -305,7 +322,7 @@ size_t kr_evaluate_and_filter_workspace(const kr_space *space)
     EvalArgs a;
     if (!space_ok(space) || !eval_plan(space, true, &a)) return 0;
     Carve c(nullptr);
-    carve_filter(c, (int64_t)a.P * a.C, a.P, (int64_t)a.P * a.nfb, true);
+    carve_filter(c, (int64_t)a.P * a.useg, a.P, (int64_t)a.P * a.uper, true);
     return c.used;
 }
 
@@ -327,8 +344,8 @@ kr_status kr_evaluate_and_filter(const kr_space *space, const double *t, const d
     a.tc = tc;
     a.pc = pc;
     Carve c(ws);
-    FilterWs w = carve_filter(c, (int64_t)a.P * a.C, a.P, (int64_t)a.P * a.nfb, true);
-    if (launch_uniform_layout(w.seg_off, w.unit_base, a.P, a.C, a.nfb, st) != hipSuccess)
+    FilterWs w = carve_filter(c, (int64_t)a.P * a.useg, a.P, (int64_t)a.P * a.uper, true);
+    if (launch_uniform_layout(w.seg_off, w.unit_base, a.P, a.useg, a.uper, st) != hipSuccess)
         return KR_EHIP;
     UnitOut o{w.buf[0].T, w.buf[0].E, w.buf[0].I, w.ucnt};
     a.dma16 = (a.wave || a.pair) && (a.N * (a.S + 1)) % 2 == 0 && (uintptr_t)t % 16 == 0 &&
@@ -345,7 +362,7 @@ kr_status kr_evaluate_and_filter(const kr_space *space, const double *t, const d
     L.seg_off = w.seg_off;
     L.unit_base = w.unit_base;
     L.n_seg = a.P;
-    L.unit_stride = (int64_t)a.fb * a.Cf;
+    L.unit_stride = a.ustride;
     return finish_segments(L, w, cap, out_off, out_idx, out_T, out_E, st);
 }
 

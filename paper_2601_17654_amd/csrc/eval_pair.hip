@@ -132,7 +132,7 @@ __device__ inline void wave_sort_keys(uint64_t *sT, uint64_t *sE, int32_t *sI, i
         const int k = 1 << lk;
         for (int lj = lk - 1; lj >= 0; --lj) {
             const int j = 1 << lj;
-            for (int q = threadIdx.x; q < (m >> 1); q += 64) {
+            for (int q = threadIdx.x & 63; q < (m >> 1); q += 64) {
                 int lo, hi;
                 if (lj == lk - 1) {
                     const int blk = q >> lj, r = q & (j - 1);
@@ -166,7 +166,7 @@ __device__ inline void wave_sort_keys(uint64_t *sT, uint64_t *sE, int32_t *sI, i
 __device__ inline int wave_frontier_scan(const uint64_t *sT, const uint64_t *sE, const int32_t *sI,
                                          int n, double *oT, double *oE, int32_t *oI)
 {
-    const int lane = threadIdx.x;
+    const int lane = threadIdx.x & 63;
     const int per = (n + 63) / 64;
     const int q0 = min(n, lane * per), q1 = min(n, q0 + per);
     uint64_t m = KR_INF_BITS;
@@ -208,87 +208,113 @@ __device__ inline int wave_frontier_scan(const uint64_t *sT, const uint64_t *sE,
     return total;
 }
 
-// Block (p, b): one wave, partition p, frequencies [b*fb, min(F, (b+1)*fb)).  LDS (in
-// doubles): t slab [N][S1] at 0, pw slab at q_pw, running sums {A, B} [N + 1][S1] at
-// q_ab (column 0 the all-SM state), the fresh second-phase table [n_pos][S] at q_f,
-// each lane's continuing second phase [64] at q_c, the filter scratch at q_sc.
+// Copy n doubles from global memory into LDS by the block's two waves, W bytes per lane
+// and instruction (W = 16 needs n even and both addresses 16-byte aligned).
+template <int W>
+__device__ __forceinline__ void copy_to_lds2(const double *g, double *l, int n)
+{
+    const int units = n * 8 / W;
+    const int lane = threadIdx.x & 63, w0 = threadIdx.x & ~63;
+    for (int u0 = w0; u0 < units; u0 += 128) {
+        const int u = u0 + lane;
+        if (u < units) {
+            const void *src = (const char *)g + (size_t)u * W;
+            lds_void *dst = (lds_void *)((char *)l + (size_t)u0 * W);
+            if constexpr (W == 16)
+                __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+            else
+                __builtin_amdgcn_global_load_lds(src, dst, 4, 0, 0);
+        }
+    }
+}
+
+// Block (p, b): two waves sharing the slabs of partition p, frequencies [b*fb,
+// min(F, (b+1)*fb)), one slab at a time.  LDS (in doubles): t slab [N][S1] at 0, pw slab
+// at q_pw, running sums {A, B} [N + 1][S1] at q_ab (column 0 the all-SM state), the
+// fresh second-phase table [n_pos][S] at q_f, each wave's continuing second phases [64]
+// at q_c, each wave's filter scratch at q_sc.  Wave w takes the pairs whose p1 has the
+// parity of w and is a unit of its own (slot and count), so the two never share output.
 // Round r of a chunk evaluates pair (p1, c0 + r) for every lane; pairs past the last
 // position are clamped for the loads and give +inf.  Each chunk's frontier goes to the
-// unit slot; at the end of a slab those points (usually many times the slab's own
+// wave's slot; at the end of a slab those points (usually many times the slab's own
 // frontier) are read back into the second-phase tables, idle by then, sorted, and
 // replaced in place by their frontier, when they fit there.
 template <int R, int W>
-__global__ void __launch_bounds__(64) eval_filter_pair_kernel(EvalArgs a, UnitOut o)
+__global__ void __launch_bounds__(128) eval_filter_pair_kernel(EvalArgs a, UnitOut o)
 {
     extern __shared__ __attribute__((aligned(16))) double lds[];
     const int N = a.N, S = a.S, S1 = S + 1, SS = S * S, slab = N * S1, np = a.n_pos;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     double *const Lt = lds, *const Lp = lds + a.q_pw;
     ColRec *const AB = (ColRec *)(lds + a.q_ab);
     PairRec *const Fr = (PairRec *)(lds + a.q_f);
-    PairRec *const Cr = (PairRec *)(lds + a.q_c);
-    const Scratch sc{lds + a.q_sc, lds + a.q_sc + 64, (int32_t *)(lds + a.q_sc + 128), 64};
-    const int lane = threadIdx.x;
+    PairRec *const Cw = (PairRec *)(lds + a.q_c) + 64 * wave;
+    double *const scw = lds + a.q_sc + 160 * wave;
+    const Scratch sc{scw, scw + 64, (int32_t *)(scw + 128), 64};
     const int p = blockIdx.x / a.nfb, fbk = blockIdx.x - p * a.nfb;
     const int f0 = fbk * a.fb, f1 = min(a.F, f0 + a.fb);
     const bool live = lane < SS;
     const int s1 = live ? lane / S : 0, s2 = live ? lane - (lane / S) * S : 0;
-    // rows of the fresh table this lane forms: SM choice sF, positions g, g + G, ...
-    const int G = 64 / S, g = lane / S, sF = lane - g * S;
-    const size_t slot0 = (size_t)p * a.C + (size_t)f0 * a.Cf;
+    // rows of the fresh table this thread forms: SM choice sF, positions g, g + G, ...
+    const int G = 128 / S, g = tid / S, sF = tid - g * S;
+    const int64_t unit = (int64_t)blockIdx.x * 2 + wave;
+    const size_t slot0 = (size_t)p * a.useg + (size_t)(unit - (int64_t)p * a.uper) * a.ustride;
     double *const oT = o.T + slot0, *const oE = o.E + slot0;
     int32_t *const oI = o.I + slot0;
     int count = 0;
     const double p_static = a.p_static;
-
-    // sort room of the slab-end reduction: the fresh and continuing tables
+    // sort room of the slab-end reduction: this wave's half of the fresh and continuing
+    // tables
     const int scap = a.pair_scap;
+    uint64_t *const sT = (uint64_t *)(lds + a.q_f) + (size_t)wave * (a.q_sc - a.q_f) / 2;
+    uint64_t *const sE = sT + scap;
+    int32_t *const sI = (int32_t *)(sE + scap);
+
     for (int f = f0; f < f1; ++f) {
         const size_t pf = (size_t)p * a.F + f;
         const int cs = count;  // first output of this slab
-        if (f > f0) {  // every LDS read of the previous slab has returned
-            wave_lds_fence();
-            __builtin_amdgcn_s_waitcnt(KR_WAIT_LGKM0);
-        }
-        copy_to_lds<W>(a.t + pf * slab, Lt, slab);
-        copy_to_lds<W>(a.pw + pf * slab, Lp, slab);
+        // every LDS read of the previous slab has returned (both waves: the barrier
+        // before the reduction, or none yet)
+        copy_to_lds2<W>(a.t + pf * slab, Lt, slab);
+        copy_to_lds2<W>(a.pw + pf * slab, Lp, slab);
         const double *const cm = a.tc + pf * 2 * S, *const cpw = a.pc + pf * 2 * S;
         const double tc1 = cm[s1], tc2 = cm[S + s2], tcF = cm[S + sF];
         const double ct1 = cpw[s1] * tc1, ct2 = cpw[S + s2] * tc2;
-        __builtin_amdgcn_s_waitcnt(KR_WAIT_VM0);  // slab f is in LDS
-        wave_lds_fence();
+        __builtin_amdgcn_s_waitcnt(KR_WAIT_VM0);  // this wave's part of slab f is in LDS
+        __syncthreads();                          // and the other wave's part
 
-        // Running sums, lane c < S1 forming column c left to right (8 rows of loads
+        // Running sums, thread c < S1 forming column c left to right (8 rows of loads
         // ahead of the additions).
-        if (lane < S1) {
+        if (tid < S1) {
             double sa = 0.0, sb = 0.0;
-            AB[lane] = ColRec{0.0, 0.0};
+            AB[tid] = ColRec{0.0, 0.0};
             for (int i0 = 0; i0 < N; i0 += 8) {
                 double vt[8], vw[8];
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
                     const int i = min(i0 + q, N - 1);
-                    vt[q] = Lt[i * S1 + lane];
-                    vw[q] = Lp[i * S1 + lane];
+                    vt[q] = Lt[i * S1 + tid];
+                    vw[q] = Lp[i * S1 + tid];
                 }
 #pragma unroll
                 for (int q = 0; q < 8; ++q)
                     if (i0 + q < N) {
                         sa = sa + vt[q];
                         sb = sb + vw[q] * vt[q];
-                        AB[(i0 + q + 1) * S1 + lane] = ColRec{sa, sb};
+                        AB[(i0 + q + 1) * S1 + tid] = ColRec{sa, sb};
                     }
             }
         }
-        wave_lds_fence();
+        __syncthreads();
         // Second comm phases that start fresh at kernel q.  Row q = N (a comm kernel
         // launched after the last compute kernel) adds nothing: all +0.
         if (g < G)
             for (int q = g; q < np; q += G)
                 Fr[q * S + sF] = q < N ? pair_phase(Lt, Lp, AB, S1, N, sF + 1, q, 1.0, tcF)
                                        : PairRec{0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
-        wave_lds_fence();
+        __syncthreads();
 
-        for (int p1 = 0; p1 < np; ++p1) {
+        for (int p1 = wave; p1 < np; p1 += 2) {
             // compute up to p1 in the all-SM state, then the first comm phase
             const int sa1 = s1 + 1;
             const ColRec z0 = AB[p1 * S1], zp = AB[p1 * S1 + sa1];
@@ -314,7 +340,7 @@ __global__ void __launch_bounds__(64) eval_filter_pair_kernel(EvalArgs a, UnitOu
             }
             const ColRec zi2 = AB[i2 * S1];
             // the second comm phase continuing the first one's progress (p2 <= j1)
-            Cr[lane] = j1 < N ? pair_phase(Lt, Lp, AB, S1, N, s2 + 1, j1, w1, tc2)
+            Cw[lane] = j1 < N ? pair_phase(Lt, Lp, AB, S1, N, s2 + 1, j1, w1, tc2)
                               : PairRec{0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
             wave_lds_fence();
             const int ppb = p1 * np - p1 * (p1 - 1) / 2 - p1;  // pair rank of (p1, p2): ppb + p2
@@ -327,7 +353,7 @@ __global__ void __launch_bounds__(64) eval_filter_pair_kernel(EvalArgs a, UnitOu
                     const bool valid = live && c0 + r < np;
                     const bool fresh = j1 < p2;
                     const ColRec z2 = AB[p2 * S1];
-                    const PairRec q = *(fresh ? Fr + p2 * S + s2 : Cr + lane);
+                    const PairRec q = *(fresh ? Fr + p2 * S + s2 : Cw + lane);
                     const double EcF = Eca + (z2.b - zi2.b);
                     const double stF = tau1 + (used2 + (z2.a - zi2.a));
                     double Ec = fresh ? EcF : Ec1;
@@ -353,12 +379,11 @@ __global__ void __launch_bounds__(64) eval_filter_pair_kernel(EvalArgs a, UnitOu
             }
             wave_lds_fence();  // the continuing phase of this p1 is read
         }
+        __syncthreads();  // both waves are done with the slab's tables
         const int ns = count - cs;
         if (ns > 1 && ns <= scap) {
             // this wave's own stores, complete after the wait: plain loads see them
             __builtin_amdgcn_s_waitcnt(KR_WAIT_VM0);
-            uint64_t *const sT = (uint64_t *)(lds + a.q_f), *const sE = sT + scap;
-            int32_t *const sI = (int32_t *)(sE + scap);
             for (int x = lane; x < ns; x += 64) {
                 sT[x] = dbits(oT[cs + x]);
                 sE[x] = dbits(oE[cs + x]);
@@ -367,16 +392,16 @@ __global__ void __launch_bounds__(64) eval_filter_pair_kernel(EvalArgs a, UnitOu
             wave_lds_fence();
             wave_sort_keys(sT, sE, sI, ns);
             count = cs + wave_frontier_scan(sT, sE, sI, ns, oT + cs, oE + cs, oI + cs);
-            wave_lds_fence();
         }
+        __syncthreads();  // the sort room is free again, and Lt, Lp may be overwritten
     }
-    if (lane == 0) o.cnt[blockIdx.x] = count;
+    if (lane == 0) o.cnt[unit] = count;
 }
 
 hipError_t launch_eval_filter_pair(const EvalArgs &a, const UnitOut &o, hipStream_t st)
 {
     const size_t lds = (size_t)a.lds_doubles * sizeof(double);
-    const dim3 grid(a.P * a.nfb), block(64);
+    const dim3 grid(a.P * a.nfb), block(128);
     if (a.dma16)
         hipLaunchKernelGGL((eval_filter_pair_kernel<8, 16>), grid, block, lds, st, a, o);
     else

@@ -40,7 +40,10 @@ struct EvalArgs {
     // records and the filter scratch
     int pair;
     int q_pw, q_ab, q_f, q_c, q_sc;
-    int pair_scap;          // most chunk outputs of a slab reduced to its frontier on chip
+    int pair_scap;          // most chunk outputs of a slab a wave reduces to its frontier on chip
+    // unit slots of the fused launch: points per partition segment, units per segment,
+    // points per unit
+    int64_t useg, uper, ustride;
 };
 
 // Per-unit frontiers written by the fused kernel or the tile kernel.

@@ -76,9 +76,9 @@ __device__ __forceinline__ void wave_lds_fence()
 #define KR_WAIT_VM0 0x0F70
 #define KR_WAIT_LGKM0 0xC07F
 
-// Copy n doubles from global memory into LDS, W bytes per lane and instruction (W = 16
-// needs n even and both addresses 16-byte aligned).  Lane i of an instruction writes
-// LDS bytes [base + W*i, base + W*(i+1)).
+// Copy n doubles from global memory into LDS by a one-wave block, W bytes per lane and
+// instruction (W = 16 needs n even and both addresses 16-byte aligned).  Lane i of an
+// instruction writes LDS bytes [base + W*i, base + W*(i+1)).
 template <int W>
 __device__ __forceinline__ void copy_to_lds(const double *g, double *l, int n)
 {
@@ -99,7 +99,7 @@ __device__ __forceinline__ void copy_to_lds(const double *g, double *l, int n)
 
 __device__ __forceinline__ void emit(const Key &k, int n, double *oT, double *oE, int32_t *oI)
 {
-    if (threadIdx.x == 0) {
+    if ((threadIdx.x & 63) == 0) {
         oT[n] = bitsd(k.t);
         oE[n] = bitsd(k.e);
         oI[n] = k.i;
@@ -158,7 +158,7 @@ __device__ inline int wave_frontier(const double (&vT)[R], const double (&vE)[R]
                                     double el, int ibase, int S, const Scratch &sc, double *oT,
                                     double *oE, int32_t *oI)
 {
-    const int lane = threadIdx.x;
+    const int lane = threadIdx.x & 63;
     wave_min2_f64(tl, el);
     const uint64_t tab = dbits(tl), ezb = dbits(el);
     if (tab >= KR_INF_BITS) return 0;  // no valid candidate
