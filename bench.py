@@ -639,7 +639,7 @@ def bench_eval2(kr, I, torch, args, mk):
     n = sp2.n_parts * sp2.n_cand
     nbytes = sum(x.numel() * 8 for x in d2)
     c2 = read_summary(EVAL2_COUNTERS, eval2_source_hash())
-    roof = {"bound": "alu", "kernel": "eval_filter_pair_kernel<8,16> (two waves per slab, "
+    roof = {"bound": "alu", "kernel": "eval_filter_pair_kernel<8,16,4> (four waves per slab, "
             "two comm kernels)", "kernel_ms": round(kms, 4), "peak": VALU_ISSUE_PEAK / 1e9,
             "unit": "G VALU wave-instructions/s", "achieved": None, "frac": None,
             "hbm_GBps": round(nbytes / (kms * 1e-3) / 1e9, 1),

@@ -94,15 +94,16 @@ bool pair_plan(EvalArgs *a)
     a->q_ab = (int)(2 * slab16);
     a->q_f = (int)(a->q_ab + 2 * (a->N + 1) * S1);  // {A, B} records
     a->q_c = (int)(a->q_f + 6 * (int64_t)a->n_pos * a->S);  // 6-double records
-    a->q_sc = a->q_c + 2 * 6 * 64;                           // one set per wave
-    const int64_t lds = a->q_sc + 2 * (64 + 64 + 32);        // scratch T, E, indices per wave
+    constexpr int NW = KR_PAIR_WAVES;
+    a->q_sc = a->q_c + NW * 6 * 64;                     // one set per wave
+    const int64_t lds = a->q_sc + NW * (64 + 64 + 32);  // scratch T, E, indices per wave
     if ((size_t)lds * 8 > kLdsBudget) return false;
     a->pair = 1;
     a->lds_doubles = (int)lds;
-    // each wave's slab-end reduction sorts in its half of the second-phase tables (20
+    // each wave's slab-end reduction sorts in its share of the second-phase tables (20
     // bytes per point); a test-only switch lowers the cap (0: never), so tests reach the
     // unreduced path
-    a->pair_scap = (a->q_sc - a->q_f) / 2 * 8 / 20;
+    a->pair_scap = (a->q_sc - a->q_f) / NW * 8 / 20;
     if (const char *e = std::getenv("KR_TEST_PAIR_SORT_CAP"))
         a->pair_scap = std::max(0, std::min(a->pair_scap, std::atoi(e)));
     // a slab is tens of thousands of candidates: one block per slab unless there are too
@@ -113,12 +114,12 @@ bool pair_plan(EvalArgs *a)
     nfb = std::min<int64_t>(nfb, a->F);
     a->fb = (int)((a->F + nfb - 1) / nfb);
     a->nfb = (a->F + a->fb - 1) / a->fb;
-    // two units per block, wave w holding the pairs whose p1 has parity w: a unit's slot
-    // holds every candidate the larger half has in fb slabs
-    int64_t half[2] = {0, 0};
-    for (int p1 = 0; p1 < a->n_pos; ++p1) half[p1 & 1] += a->n_pos - p1;
-    a->uper = 2 * (int64_t)a->nfb;
-    a->ustride = (int64_t)a->fb * std::max(half[0], half[1]) * a->S * a->S;
+    // NW units per block, one per wave with the launch positions it owns: a unit's slot
+    // holds every candidate the largest share has in fb slabs
+    int64_t share[NW] = {};
+    for (int p1 = 0; p1 < a->n_pos; ++p1) share[pair_owner_host(p1, NW)] += a->n_pos - p1;
+    a->uper = NW * (int64_t)a->nfb;
+    a->ustride = (int64_t)a->fb * *std::max_element(share, share + NW) * a->S * a->S;
     a->useg = a->uper * a->ustride;
     return true;
 }

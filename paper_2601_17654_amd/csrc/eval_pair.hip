@@ -208,14 +208,21 @@ __device__ inline int wave_frontier_scan(const uint64_t *sT, const uint64_t *sE,
     return total;
 }
 
-// Copy n doubles from global memory into LDS by the block's two waves, W bytes per lane
+// The wave of a block of NW waves that takes launch position p1 (snake order).
+__host__ __device__ __forceinline__ int pair_owner(int p1, int NW)
+{
+    const int r = p1 % (2 * NW);
+    return r < NW ? r : 2 * NW - 1 - r;
+}
+
+// Copy n doubles from global memory into LDS by the block's NW waves, W bytes per lane
 // and instruction (W = 16 needs n even and both addresses 16-byte aligned).
-template <int W>
-__device__ __forceinline__ void copy_to_lds2(const double *g, double *l, int n)
+template <int W, int NW>
+__device__ __forceinline__ void copy_to_lds_nw(const double *g, double *l, int n)
 {
     const int units = n * 8 / W;
     const int lane = threadIdx.x & 63, w0 = threadIdx.x & ~63;
-    for (int u0 = w0; u0 < units; u0 += 128) {
+    for (int u0 = w0; u0 < units; u0 += 64 * NW) {
         const int u = u0 + lane;
         if (u < units) {
             const void *src = (const char *)g + (size_t)u * W;
@@ -228,19 +235,21 @@ __device__ __forceinline__ void copy_to_lds2(const double *g, double *l, int n)
     }
 }
 
-// Block (p, b): two waves sharing the slabs of partition p, frequencies [b*fb,
+// Block (p, b): NW waves sharing the slabs of partition p, frequencies [b*fb,
 // min(F, (b+1)*fb)), one slab at a time.  LDS (in doubles): t slab [N][S1] at 0, pw slab
 // at q_pw, running sums {A, B} [N + 1][S1] at q_ab (column 0 the all-SM state), the
 // fresh second-phase table [n_pos][S] at q_f, each wave's continuing second phases [64]
-// at q_c, each wave's filter scratch at q_sc.  Wave w takes the pairs whose p1 has the
-// parity of w and is a unit of its own (slot and count), so the two never share output.
+// at q_c, each wave's filter scratch at q_sc.  Launch positions p1 go to the waves in
+// snake order (0, 1, .., NW - 1, NW - 1, .., 0, 0, 1, ..), which evens out the pairs
+// each wave takes; a wave is a unit of its own (slot and count), so waves never share
+// output.
 // Round r of a chunk evaluates pair (p1, c0 + r) for every lane; pairs past the last
 // position are clamped for the loads and give +inf.  Each chunk's frontier goes to the
 // wave's slot; at the end of a slab those points (usually many times the slab's own
 // frontier) are read back into the second-phase tables, idle by then, sorted, and
 // replaced in place by their frontier, when they fit there.
-template <int R, int W>
-__global__ void __launch_bounds__(128) eval_filter_pair_kernel(EvalArgs a, UnitOut o)
+template <int R, int W, int NW>
+__global__ void __launch_bounds__(64 * NW) eval_filter_pair_kernel(EvalArgs a, UnitOut o)
 {
     extern __shared__ __attribute__((aligned(16))) double lds[];
     const int N = a.N, S = a.S, S1 = S + 1, SS = S * S, slab = N * S1, np = a.n_pos;
@@ -256,8 +265,8 @@ __global__ void __launch_bounds__(128) eval_filter_pair_kernel(EvalArgs a, UnitO
     const bool live = lane < SS;
     const int s1 = live ? lane / S : 0, s2 = live ? lane - (lane / S) * S : 0;
     // rows of the fresh table this thread forms: SM choice sF, positions g, g + G, ...
-    const int G = 128 / S, g = tid / S, sF = tid - g * S;
-    const int64_t unit = (int64_t)blockIdx.x * 2 + wave;
+    const int G = 64 * NW / S, g = tid / S, sF = tid - g * S;
+    const int64_t unit = (int64_t)blockIdx.x * NW + wave;
     const size_t slot0 = (size_t)p * a.useg + (size_t)(unit - (int64_t)p * a.uper) * a.ustride;
     double *const oT = o.T + slot0, *const oE = o.E + slot0;
     int32_t *const oI = o.I + slot0;
@@ -266,22 +275,22 @@ __global__ void __launch_bounds__(128) eval_filter_pair_kernel(EvalArgs a, UnitO
     // sort room of the slab-end reduction: this wave's half of the fresh and continuing
     // tables
     const int scap = a.pair_scap;
-    uint64_t *const sT = (uint64_t *)(lds + a.q_f) + (size_t)wave * (a.q_sc - a.q_f) / 2;
+    uint64_t *const sT = (uint64_t *)(lds + a.q_f) + (size_t)wave * ((a.q_sc - a.q_f) / NW);
     uint64_t *const sE = sT + scap;
     int32_t *const sI = (int32_t *)(sE + scap);
 
     for (int f = f0; f < f1; ++f) {
         const size_t pf = (size_t)p * a.F + f;
         const int cs = count;  // first output of this slab
-        // every LDS read of the previous slab has returned (both waves: the barrier
-        // before the reduction, or none yet)
-        copy_to_lds2<W>(a.t + pf * slab, Lt, slab);
-        copy_to_lds2<W>(a.pw + pf * slab, Lp, slab);
+        // every LDS read of the previous slab has returned (all waves: the barrier
+        // after the reduction, or none yet)
+        copy_to_lds_nw<W, NW>(a.t + pf * slab, Lt, slab);
+        copy_to_lds_nw<W, NW>(a.pw + pf * slab, Lp, slab);
         const double *const cm = a.tc + pf * 2 * S, *const cpw = a.pc + pf * 2 * S;
         const double tc1 = cm[s1], tc2 = cm[S + s2], tcF = cm[S + sF];
         const double ct1 = cpw[s1] * tc1, ct2 = cpw[S + s2] * tc2;
         __builtin_amdgcn_s_waitcnt(KR_WAIT_VM0);  // this wave's part of slab f is in LDS
-        __syncthreads();                          // and the other wave's part
+        __syncthreads();                          // and the other waves' parts
 
         // Running sums, thread c < S1 forming column c left to right (8 rows of loads
         // ahead of the additions).
@@ -314,7 +323,8 @@ __global__ void __launch_bounds__(128) eval_filter_pair_kernel(EvalArgs a, UnitO
                                        : PairRec{0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
         __syncthreads();
 
-        for (int p1 = wave; p1 < np; p1 += 2) {
+        for (int p1 = 0; p1 < np; ++p1) {
+            if (pair_owner(p1, NW) != wave) continue;
             // compute up to p1 in the all-SM state, then the first comm phase
             const int sa1 = s1 + 1;
             const ColRec z0 = AB[p1 * S1], zp = AB[p1 * S1 + sa1];
@@ -379,7 +389,7 @@ __global__ void __launch_bounds__(128) eval_filter_pair_kernel(EvalArgs a, UnitO
             }
             wave_lds_fence();  // the continuing phase of this p1 is read
         }
-        __syncthreads();  // both waves are done with the slab's tables
+        __syncthreads();  // every wave is done with the slab's tables
         const int ns = count - cs;
         if (ns > 1 && ns <= scap) {
             // this wave's own stores, complete after the wait: plain loads see them
@@ -398,14 +408,17 @@ __global__ void __launch_bounds__(128) eval_filter_pair_kernel(EvalArgs a, UnitO
     if (lane == 0) o.cnt[unit] = count;
 }
 
+int pair_owner_host(int p1, int NW) { return pair_owner(p1, NW); }
+
 hipError_t launch_eval_filter_pair(const EvalArgs &a, const UnitOut &o, hipStream_t st)
 {
     const size_t lds = (size_t)a.lds_doubles * sizeof(double);
-    const dim3 grid(a.P * a.nfb), block(128);
+    constexpr int NW = KR_PAIR_WAVES;
+    const dim3 grid(a.P * a.nfb), block(64 * NW);
     if (a.dma16)
-        hipLaunchKernelGGL((eval_filter_pair_kernel<8, 16>), grid, block, lds, st, a, o);
+        hipLaunchKernelGGL((eval_filter_pair_kernel<8, 16, NW>), grid, block, lds, st, a, o);
     else
-        hipLaunchKernelGGL((eval_filter_pair_kernel<8, 4>), grid, block, lds, st, a, o);
+        hipLaunchKernelGGL((eval_filter_pair_kernel<8, 4, NW>), grid, block, lds, st, a, o);
     return hipGetLastError();
 }
 

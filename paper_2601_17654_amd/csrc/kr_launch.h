@@ -7,6 +7,7 @@
 #include "../../include/kareus.h"
 
 #define KR_FIN_CAP 2560    // points the finalize kernel sorts in LDS
+#define KR_PAIR_WAVES 4    // waves per block of the two-comm evaluation kernel
 #define KR_FIN_UNITS 2048  // units per segment the finalize kernel's LDS path takes
 #define KR_TILE 2048       // points per tile of the stand-alone filter
 #define KR_PAD 4           // rows the wave kernel's end-cursor search reads per step
@@ -78,6 +79,8 @@ hipError_t launch_eval(const EvalArgs &a, hipStream_t st);
 hipError_t launch_eval_filter(const EvalArgs &a, const UnitOut &o, hipStream_t st);
 hipError_t launch_eval_filter_wave(const EvalArgs &a, const UnitOut &o, hipStream_t st);
 hipError_t launch_eval_filter_pair(const EvalArgs &a, const UnitOut &o, hipStream_t st);
+// The wave of a two-comm evaluation block of NW waves that takes launch position p1.
+int pair_owner_host(int p1, int NW);
 hipError_t launch_decode(const DecodeArgs &d, hipStream_t st);
 
 // pareto.hip
