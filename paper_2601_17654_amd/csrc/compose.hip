@@ -583,8 +583,29 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
                     best0 = vmin(best0, m0v);
                     best1 = vmin(best1, m1v);
                 };
-                // Two groups a round, their loads issued together; an odd last round
-                // repeats its group, which cannot lower a minimum twice.
+                // A slice of three groups (17 to 24 groups over 8 slices) takes them in
+                // one round, all loads issued together, so the slowest slice pays one
+                // load latency like the others.  Otherwise two groups a round; an odd
+                // last round repeats its group, which cannot lower a minimum twice.
+                if (g1 - g0 == 3) {  // wave-uniform
+                    const double *wa = wc + 2 * j - 8 * g0 - 7;
+                    double xa[9], xb[9], xc[9], ea[8], eb[8], ec[8];
+#pragma unroll
+                    for (int d = 0; d < 9; ++d) {
+                        xa[d] = wa[d];
+                        xb[d] = wa[d - 8];
+                        xc[d] = wa[d - 16];
+                    }
+#pragma unroll
+                    for (int o = 0; o < 8; ++o) {
+                        ea[o] = et[8 * g0 + o];
+                        eb[o] = et[8 * g0 + 8 + o];
+                        ec[o] = et[8 * g0 + 16 + o];
+                    }
+                    group(g0, xa, ea);
+                    group(g0 + 1, xb, eb);
+                    group(g0 + 2, xc, ec);
+                } else
                 for (int g = g0; g < g1; g += 2) {
                     const int h = min(g + 1, g1 - 1);
                     const double *wa = wc + 2 * j - 8 * g - 7, *wb = wc + 2 * j - 8 * h - 7;

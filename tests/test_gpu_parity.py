@@ -694,3 +694,23 @@ def test_two_comm_slab_reduction(kr, oracle_lib, monkeypatch, sort_cap):
             ix = oracle_lib.pareto(Tr, Er)
             check_frontier(fr, p, (ix, Tr[ix], Er[ix]), "cap %s space %d part %d" % (sort_cap, k, p))
 
+
+@pytest.mark.parametrize("shape", [(1, 1, 1), (1, 2, 8), (3, 1, 8), (5, 6, 3), (12, 13, 8),
+                                   (20, 9, 7), (48, 33, 8), (9, 10, 2)])
+@pytest.mark.parametrize("tc_scale", [1.0, 1e-3, 30.0])
+def test_two_comm_wave_kernel_shapes(kr, oracle_lib, shape, tc_scale):
+    """Two comm kernels on the one-wave-per-lane-pair kernel (at most 8 SM choices):
+    one or all launch positions, one kernel, one SM choice (lanes past S * S idle),
+    short and long comm, every partition's fused frontier against the oracle."""
+    N, n_pos, S = shape
+    K = tuple(4 * (i + 1) for i in range(S))
+    space = I.Space(3, N, 2, n_pos, K, (1005.0, 1490.0, 1980.0))
+    tab = I.make_tables(space, seed=N * 11 + n_pos + S, comm_bytes=(8e6, 512e6))
+    tab["tc"] = tab["tc"] * tc_scale
+    d = [torch.from_numpy(tab[x]).cuda() for x in ("t", "pw", "tc", "pc")]
+    fr = kr.evaluate_and_filter(space, *d)
+    for p in range(space.n_parts):
+        Tr, Er = oracle_lib.evaluate_partition(space, tab["t"], tab["pw"], tab["tc"], tab["pc"], p)
+        ix = oracle_lib.pareto(Tr, Er)
+        check_frontier(fr, p, (ix, Tr[ix], Er[ix]), "M=2 %s x%g part %d" % (shape, tc_scale, p))
+
