@@ -1,10 +1,10 @@
-// Two-comm candidate evaluation and frontier filter, one wavefront per slab (gfx950).
+// Two-comm candidate evaluation and frontier filter, a few waves per slab (gfx950).
 //
 // With two comm kernels the candidates of a (partition, frequency) slab are the
-// launch-position pairs p1 <= p2 times the SM choices (s1, s2) (Sections 4.1, 4.5).  A
-// 64-lane wave owns a slab at a time: lane s1 * S + s2 takes SM choices (s1, s2) (at
-// most 8 SM choices, so S * S <= 64) and steps through the pairs in candidate order,
-// one pair per round for every lane.
+// launch-position pairs p1 <= p2 times the SM choices (s1, s2) (Sections 4.1, 4.5).  The
+// waves of a block share one slab's tables in LDS and split its launch positions p1;
+// lane s1 * S + s2 takes SM choices (s1, s2) (at most 8 SM choices, so S * S <= 64) and
+// steps through a wave's pairs in candidate order, one pair per round for every lane.
 //
 // The walk of the partition cost model (fluid SM-share reading of Sections 3.2, 4.2
 // and 4.5; the comm kernels share one stream in launch order) falls into phases whose
@@ -272,7 +272,7 @@ __global__ void __launch_bounds__(64 * NW) eval_filter_pair_kernel(EvalArgs a, U
     int32_t *const oI = o.I + slot0;
     int count = 0;
     const double p_static = a.p_static;
-    // sort room of the slab-end reduction: this wave's half of the fresh and continuing
+    // sort room of the slab-end reduction: this wave's share of the fresh and continuing
     // tables
     const int scap = a.pair_scap;
     uint64_t *const sT = (uint64_t *)(lds + a.q_f) + (size_t)wave * ((a.q_sc - a.q_f) / NW);

@@ -676,8 +676,8 @@ def test_fused_many_box_members(kr, oracle_lib):
 
 @pytest.mark.parametrize("sort_cap", [None, "0", "5", "40"])
 def test_two_comm_slab_reduction(kr, oracle_lib, monkeypatch, sort_cap):
-    """Two comm kernels with at most 8 SM choices (one wave per slab): each slab's chunk
-    frontiers are reduced to the slab's frontier on chip when they fit the sort room.
+    """Two comm kernels with at most 8 SM choices (the wave kernel): each wave's chunk
+    frontiers of a slab are reduced to their frontier on chip when they fit the sort room.
     The test-only switch KR_TEST_PAIR_SORT_CAP lowers that room (0: never reduce), so
     slabs with more chunk outputs keep them all and the merge after the kernel sees
     them; every partition's frontier against the oracle either way."""
@@ -699,9 +699,10 @@ def test_two_comm_slab_reduction(kr, oracle_lib, monkeypatch, sort_cap):
                                    (20, 9, 7), (48, 33, 8), (9, 10, 2)])
 @pytest.mark.parametrize("tc_scale", [1.0, 1e-3, 30.0])
 def test_two_comm_wave_kernel_shapes(kr, oracle_lib, shape, tc_scale):
-    """Two comm kernels on the one-wave-per-lane-pair kernel (at most 8 SM choices):
-    one or all launch positions, one kernel, one SM choice (lanes past S * S idle),
-    short and long comm, every partition's fused frontier against the oracle."""
+    """Two comm kernels with at most 8 SM choices (the wave kernel whose lanes are SM
+    choice pairs): one or all launch positions, one kernel, one SM choice (lanes past
+    S * S idle), short and long comm, every partition's fused frontier against the
+    oracle."""
     N, n_pos, S = shape
     K = tuple(4 * (i + 1) for i in range(S))
     space = I.Space(3, N, 2, n_pos, K, (1005.0, 1490.0, 1980.0))
