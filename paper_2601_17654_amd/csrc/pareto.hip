@@ -350,42 +350,53 @@ __device__ __forceinline__ void merge_segment(int g, int n, const SegLayout &L,
             sh.I[q0 + j] = k[j].i;
         }
     lds_barrier();
+    // Sorted runs of width w -> width 2w by merge path: the thread owning output
+    // positions [q0, q0 + PER) of a pair of runs (A, then B) finds how many of the first
+    // q0 - base outputs come from A (a binary search along that diagonal of the merge),
+    // then merges its PER outputs from there, holding the next key of each run.
     int cur = 0;
-    for (int w = PER; w < n; w <<= 1) {  // sorted runs of width w -> width 2w
+    for (int w = PER; w < n; w <<= 1) {
         const uint64_t *inT = sh.T[cur];
         const uint16_t *inI = sh.id[cur];
-        // this thread's points all lie in one run; its partner is [p0, p0 + plen)
-        const int a0 = q0 & ~(2 * w - 1);
-        const bool in_a = q0 - a0 < w;
-        const int p0 = in_a ? min(n, a0 + w) : a0;
-        const int plen = in_a ? min(n, a0 + 2 * w) - p0 : w;
-        const int own0 = in_a ? a0 : a0 + w;
-        uint64_t t[PER];
-        int x[PER], r[PER];
-#pragma unroll
-        for (int j = 0; j < PER; ++j) {
-            const int q = min(q0 + j, n - 1);
-            t[j] = inT[q];
-            x[j] = inI[q];
-            r[j] = 0;
-        }
-        // rank in the partner: the number of its points below the key (lifting search)
-        if (q0 < q1)
-            for (int step = w; step >= 1; step >>= 1)
-#pragma unroll
-                for (int j = 0; j < PER; ++j) {
-                    const int c = r[j] + step;
-                    if (c <= plen &&
-                        pos_less(inT[p0 + c - 1], inI[p0 + c - 1], t[j], x[j], sh.E, sh.I))
-                        r[j] = c;
-                }
-#pragma unroll
-        for (int j = 0; j < PER; ++j)
-            if (q0 + j < q1) {
-                const int dst = a0 + (q0 + j - own0) + r[j];
-                sh.T[cur ^ 1][dst] = t[j];
-                sh.id[cur ^ 1][dst] = (uint16_t)x[j];
+        if (q0 < q1) {
+            const int base = q0 & ~(2 * w - 1);
+            const int la = min(w, n - base), lb = max(0, min(w, n - base - w));
+            const uint64_t *AT = inT + base, *BT = inT + base + w;
+            const uint16_t *AI = inI + base, *BI = inI + base + w;
+            const int d = q0 - base;
+            int lo = max(0, d - lb), hi = min(d, la);
+            while (lo < hi) {  // the least i with A[i] after B[d - 1 - i]
+                const int mid = (lo + hi) >> 1;
+                const int jb = d - 1 - mid;
+                if (pos_less(AT[mid], AI[mid], BT[jb], BI[jb], sh.E, sh.I)) lo = mid + 1;
+                else hi = mid;
             }
+            int i = lo, j = d - lo;
+            uint64_t at = i < la ? AT[i] : 0, bt = j < lb ? BT[j] : 0;
+            int ai = i < la ? AI[i] : 0, bi = j < lb ? BI[j] : 0;
+            uint64_t *const oT = sh.T[cur ^ 1] + q0;
+            uint16_t *const oI = sh.id[cur ^ 1] + q0;
+            for (int u = 0; u < q1 - q0; ++u) {
+                const bool fromA = i < la && (j >= lb || pos_less(at, ai, bt, bi, sh.E, sh.I));
+                if (fromA) {
+                    oT[u] = at;
+                    oI[u] = (uint16_t)ai;
+                    ++i;
+                    if (i < la) {
+                        at = AT[i];
+                        ai = AI[i];
+                    }
+                } else {
+                    oT[u] = bt;
+                    oI[u] = (uint16_t)bi;
+                    ++j;
+                    if (j < lb) {
+                        bt = BT[j];
+                        bi = BI[j];
+                    }
+                }
+            }
+        }
         cur ^= 1;
         lds_barrier();
     }
