@@ -477,40 +477,32 @@ kr_status kr_extract_schedule(int32_t n_parts, int32_t n_bins, const int32_t *bp
 
 // Workspace of the microbatch frontier; every pointer is null when base is null.
 struct MbWs {
-    int64_t *off_f, *seg, *front_off;
-    double *Ts, *Es, *F, *info, *stair_Tlo, *stair_E, *slot_T, *slot_E, *front_T, *front_E;
-    int32_t *bp, *pt_bin, *L, *stair_bin, *n_stair, *status, *slot_choice, *front_idx;
-    void *cws, *pws;
-    size_t cws_bytes, pws_bytes;
+    int64_t *seg, *front_off;
+    double *slot_T, *slot_E, *front_T, *front_E;
+    int32_t *slot_choice, *front_idx;
+    MbGridWs g;
+    void *pws;
+    size_t pws_bytes;
 };
 
-static MbWs carve_mb(Carve &c, int K, int F, int64_t n_points, int B)
+static MbWs carve_mb(Carve &c, int K, int F, int B)
 {
     MbWs w;
     const int64_t S = (int64_t)F * B;
-    w.off_f = c.take<int64_t>(K + 1);
     w.seg = c.take<int64_t>(2);
     w.front_off = c.take<int64_t>(2);
-    w.Ts = c.take<double>(n_points + 1);
-    w.Es = c.take<double>(n_points + 1);
-    w.F = c.take<double>(B);
-    w.info = c.take<double>(2);
-    w.stair_Tlo = c.take<double>(B);
-    w.stair_E = c.take<double>(B);
     w.slot_T = c.take<double>(S);
     w.slot_E = c.take<double>(S);
     w.front_T = c.take<double>(S);
     w.front_E = c.take<double>(S);
-    w.bp = c.take<int32_t>((size_t)K * B);
-    w.pt_bin = c.take<int32_t>(n_points + 1);
-    w.L = c.take<int32_t>(1);
-    w.stair_bin = c.take<int32_t>(B);
-    w.n_stair = c.take<int32_t>(1);
-    w.status = c.take<int32_t>(1);
     w.slot_choice = c.take<int32_t>((size_t)S * K);
     w.front_idx = c.take<int32_t>(S);
-    w.cws_bytes = kr_compose_frontiers_workspace(K, B);
-    w.cws = c.take<char>(w.cws_bytes);
+    w.g.ob2 = c.take<int32_t>(S);
+    w.g.oarg = c.take<int32_t>(S);
+    w.g.oe = c.take<double>(S);
+    w.g.F = c.take<double>(2 * S);
+    w.g.bp = c.take<int32_t>((size_t)S * K);
+    w.g.stair = c.take<int32_t>(S);
     w.pws_bytes = kr_pareto_filter_workspace(S, 1);
     w.pws = c.take<char>(w.pws_bytes);
     return w;
@@ -523,7 +515,7 @@ size_t kr_microbatch_frontier_workspace(int32_t n_types, int32_t n_freq, int64_t
         n_seq > KR_MB_MAX_SEQ || n_bins < 2)
         return 0;
     Carve c(nullptr);
-    carve_mb(c, n_types, n_freq, n_points, n_bins);
+    carve_mb(c, n_types, n_freq, n_bins);
     return c.used;
 }
 
@@ -568,19 +560,11 @@ kr_status kr_microbatch_frontier(int32_t n_types, int32_t n_freq, const int64_t 
     for (int i = 0; i < n_seq; ++i) a.seq_u[i] = (uint8_t)uidx[seq[i]];
     hipStream_t st = (hipStream_t)stream;
     Carve c(ws);
-    MbWs w = carve_mb(c, n_types, n_freq, n_points, n_bins);
+    MbWs w = carve_mb(c, n_types, n_freq, n_bins);
     a.slot_T = w.slot_T;
     a.slot_E = w.slot_E;
     a.slot_choice = w.slot_choice;
-    for (int f = 0; f < n_freq; ++f) {
-        if (launch_mb_scale(a, f, w.off_f, w.Ts, w.Es, st) != hipSuccess) return KR_EHIP;
-        const kr_status rc = kr_compose_frontiers(
-            a.Ku, w.off_f, w.Ts, w.Es, n_bins, 0.0, w.F, w.bp, w.pt_bin, w.info, w.L, w.stair_bin,
-            w.stair_Tlo, w.stair_E, w.n_stair, w.status, w.cws, w.cws_bytes, stream);
-        if (rc != KR_OK) return rc;
-        MbComp mc{w.off_f, w.bp, w.pt_bin, w.stair_bin, w.n_stair, w.status};
-        if (launch_mb_walk(a, f, mc, st) != hipSuccess) return KR_EHIP;
-    }
+    if (launch_mb_grid(a, w.g, st) != hipSuccess) return KR_EHIP;
     const int64_t S = (int64_t)n_freq * n_bins;
     if (launch_mb_seg(w.seg, S, st) != hipSuccess) return KR_EHIP;
     const kr_status rc = kr_pareto_filter(S, w.slot_T, w.slot_E, w.seg, 1, S, w.front_off,

@@ -159,14 +159,16 @@ struct MbArgs {
     double *slot_T, *slot_E;         // [F * B]
     int32_t *slot_choice;            // [F * B][K]
 };
-// One frequency's composition outputs.
-struct MbComp {
-    const int64_t *off;  // [Ku + 1]
-    const int32_t *bp, *pt_bin, *stair_bin, *n_stair, *status;
+// Per-frequency workspace of the grid microbatch frontier (region f of each array is
+// frequency f's): the occupied offsets of the type being binned [B] (offset, least
+// energy, point), the composite arrays of two steps [2][B], the back-pointers [K][B] and
+// the staircase bins [B].
+struct MbGridWs {
+    int32_t *ob2, *oarg;
+    double *oe, *F;
+    int32_t *bp, *stair;
 };
-hipError_t launch_mb_scale(const MbArgs &a, int f, int64_t *off_f, double *Ts, double *Es,
-                           hipStream_t st);
-hipError_t launch_mb_walk(const MbArgs &a, int f, const MbComp &c, hipStream_t st);
+hipError_t launch_mb_grid(const MbArgs &a, const MbGridWs &w, hipStream_t st);
 hipError_t launch_mb_seg(int64_t *seg, int64_t n, hipStream_t st);
 hipError_t launch_mb_gather(const MbArgs &a, const int64_t *front_off, const int32_t *front_idx,
                             int64_t cap, double *out_T, double *out_E, int32_t *out_f,

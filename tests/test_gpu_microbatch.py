@@ -80,6 +80,18 @@ def test_microbatch_random(kr, seed):
     _compare_exact(kr, seg_off, T, E, K, F, seq, cT, cE, "random %d" % seed)
 
 
+@pytest.mark.parametrize("B", [4097, 9000, 20000])
+def test_microbatch_wide_grids(kr, B):
+    """More bins than one on-chip binning window (4,096 offsets) and thousands of points
+    per type and frequency: a type's offsets are binned in several windows, and its
+    occupied offsets run to thousands."""
+    rng = np.random.default_rng(B)
+    K, F = 2, 3
+    seg_off, T, E = _random_case(rng, K, F, 3000)
+    _compare(kr, seg_off, T, E, K, F, [0, 1, 0], None, None, B, "wide grid %d" % B)
+    _compare(kr, seg_off, T, E, K, F, [1], None, None, B, "wide grid %d, one type" % B)
+
+
 def test_microbatch_degenerate(kr):
     rng = np.random.default_rng(17)
     K, F = 3, 4
