@@ -308,11 +308,12 @@ def main():
     kr.set_phase_events(kr.PHASE_EVAL_TILE)
     kr.set_phase_events(kr.PHASE_MINPLUS)
 
-    ef_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    co_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    ex_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
-    kern_ms = float(np.mean([p[0][0].elapsed_time(p[0][1]) for p in pev]))
-    mp_ms = float(np.mean([p[1][0].elapsed_time(p[1][1]) for p in pev]))
+    # per-part times: medians over the timed steps (HIP events on the library's stream)
+    ef_ms = float(np.median([e[0].elapsed_time(e[1]) for e in evs]))
+    co_ms = float(np.median([e[1].elapsed_time(e[2]) for e in evs]))
+    ex_ms = float(np.median([e[2].elapsed_time(e[3]) for e in evs]))
+    kern_ms = float(np.median([p[0][0].elapsed_time(p[0][1]) for p in pev]))
+    mp_ms = float(np.median([p[1][0].elapsed_time(p[1][1]) for p in pev]))
     ms_per_step = wall * 1e3 / args.steps
     assert int(comp.status.item()) == 0 and int(fr.off[-1].item()) == cap
 
@@ -327,6 +328,7 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
             "kernel": "eval_filter_wave_kernel (fused evaluation + frontier, one wave per slab)",
             "kernel_ms": round(kern_ms, 4), "algorithmic_bytes": table_bytes,
+            "traffic_GBps": None if traffic is None else round(traffic / (kern_ms * 1e-3) / 1e9, 1),
             "traffic_source": tsrc}
 
     # composition: the min-plus step for partition k pairs each of the L_{k-1} bins
@@ -422,7 +424,7 @@ def main():
                                check=False, out=mbuf)
         mev[2 * k + 1].record()
     torch.cuda.synchronize()
-    mb_ms = float(np.mean([mev[2 * k].elapsed_time(mev[2 * k + 1]) for k in range(args.steps)]))
+    mb_ms = float(np.median([mev[2 * k].elapsed_time(mev[2 * k + 1]) for k in range(args.steps)]))
     mres = kr.microbatch_frontier(mseg, mfr.T, mfr.E, mK, mF, mseq, mcT_d, mcE_d,
                                   n_bins=MB_BINS, out=mbuf)
     kr.microbatch_enumerate(mseg, mfr.T, mfr.E, mK, mF, mseq, mcT_d, mcE_d, check=False,
@@ -434,7 +436,7 @@ def main():
                                 out=xbuf)
         mev[2 * k + 1].record()
     torch.cuda.synchronize()
-    mx_ms = float(np.mean([mev[2 * k].elapsed_time(mev[2 * k + 1]) for k in range(args.steps)]))
+    mx_ms = float(np.median([mev[2 * k].elapsed_time(mev[2 * k + 1]) for k in range(args.steps)]))
     mexa = kr.microbatch_enumerate(mseg, mfr.T, mfr.E, mK, mF, mseq, mcT_d, mcE_d, out=xbuf)
     out["microbatch"] = {
         "workload": "microbatch-llama: 4 partition types (llama-layer tables), 16 layers of "
@@ -458,7 +460,7 @@ def main():
         kr.compare_frontiers(cA_T, cA_E, cB_T, cB_E, out=cmp_out)
         cev[2 * k + 1].record()
     torch.cuda.synchronize()
-    cmp_ms = float(np.mean([cev[2 * k].elapsed_time(cev[2 * k + 1]) for k in range(args.steps)]))
+    cmp_ms = float(np.median([cev[2 * k].elapsed_time(cev[2 * k + 1]) for k in range(args.steps)]))
     cm = cmp_out.cpu().numpy()
     out["frontier_metrics"] = {
         "workload": "eval-stress frontier points (%d) against the same points x (0.97 T, "
@@ -697,7 +699,7 @@ def bench_dp(kr, I, torch, args, mk):
         ev[2 * k + 1].record()
     torch.cuda.synchronize()
     assert int(res.status.item()) == 0
-    ms = float(np.mean([ev[2 * k].elapsed_time(ev[2 * k + 1]) for k in range(args.steps)]))
+    ms = float(np.median([ev[2 * k].elapsed_time(ev[2 * k + 1]) for k in range(args.steps)]))
     n = ops.shape[0]
     cells = n * ((len(k1) + 1) * (len(k2) + 1) - 1)
     sizes = res.n.cpu().numpy()
@@ -798,8 +800,8 @@ def bench_mbo(kr, I, torch, sp, d, args, mk):
     for p in (kr.PHASE_HVI, kr.PHASE_UNC, kr.PHASE_SELECT):
         kr.set_phase_events(p)
     assert int(sc.status.item()) == 0 and int(bt.status.item()) == 0
-    step_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
-    hvi_ms, unc_ms, sel_ms = (float(np.mean([q[i][0].elapsed_time(q[i][1]) for q in ph]))
+    step_ms = float(np.median([e[0].elapsed_time(e[1]) for e in ev]))
+    hvi_ms, unc_ms, sel_ms = (float(np.median([q[i][0].elapsed_time(q[i][1]) for q in ph]))
                               for i in range(3))
 
     traffic, tsrc = read_mbo_traffic()
