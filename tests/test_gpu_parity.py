@@ -431,6 +431,18 @@ def test_compose_edge_cases(kr, oracle_lib):
                   rng.integers(1, 4, off[-1]) * 0.25, 40, 0.0))
     # a caller-given width
     cases.append((off, rng.uniform(1e-3, 4e-3, off[-1]), rng.uniform(1, 2, off[-1]), 64, 2.5e-4))
+    # dense min-plus steps with exact ties: times on a binary grid with the bin width as
+    # its step, offset ranges M_k of 128, 122, 64, 200 and 5 (full groups of 8 offsets
+    # with and without leftovers), energies on a coarse grid
+    spans = [128, 122, 64, 200, 5] * 4
+    Ts, Es = [], []
+    for m in spans:
+        k = rng.integers(0, m + 1, 90)
+        k[:2] = (0, m)
+        Ts.append((k + 3) * 2.0 ** -10)
+        Es.append(rng.integers(1, 6, 90) * 0.25)
+    offd = np.concatenate([[0], np.cumsum([len(x) for x in Ts])])
+    cases.append((offd, np.concatenate(Ts), np.concatenate(Es), sum(spans) + 8, 2.0 ** -10))
     for i, (off, T, E, B, delta) in enumerate(cases):
         off = off.astype(np.int64)
         comp = kr.compose_frontiers(torch.from_numpy(off).cuda(), torch.from_numpy(T).cuda(),
