@@ -105,6 +105,46 @@ def test_evaluate_small_spaces(kr, oracle_lib, case, tc_scale):
         check_frontier(fr, p, (ix, Tr[ix], Er[ix]), "frontier case %d part %d" % (case, p))
 
 
+def quantised_tables(space, seed):
+    """Tables with many exact ties and zeros: times on a coarse binary grid (kernels of
+    equal length), powers of 0, 100 or 200 W, comm times of 0 for some SM choices and
+    comm powers of 0 for others."""
+    rng = np.random.default_rng(seed)
+    tab = I.make_tables(space, seed=seed, comm_bytes=(4e6, 64e6))
+    tab["t"] = rng.integers(1, 5, tab["t"].shape) * 2.0 ** -12
+    tab["pw"] = rng.integers(0, 3, tab["pw"].shape) * 100.0
+    tc = rng.integers(0, 4, tab["tc"].shape) * 2.0 ** -11
+    tc[..., ::3] = 0.0
+    tab["tc"] = tc
+    pc = rng.integers(0, 3, tab["pc"].shape) * 50.0
+    pc[..., 1::4] = 0.0
+    tab["pc"] = pc
+    return tab
+
+
+@pytest.mark.parametrize("case", range(4))
+def test_evaluate_degenerate_tables(kr, oracle_lib, case):
+    """Exact ties everywhere (equal kernels, equal comm times, zero powers and zero comm
+    times) on each evaluation kernel: the one-comm wave kernel, the two-comm pair kernel,
+    and the block kernel for each comm count.  Time and energy match the oracle and the
+    frontier indices (smallest index among exact duplicates) are bit-exact."""
+    space = [I.Space(3, 12, 1, 13, tuple(range(1, 17)), (1005.0, 1500.0, 1980.0)),
+             I.Space(3, 9, 2, 10, (4, 8, 12, 16), (1005.0, 1980.0)),
+             I.Space(2, 7, 2, 8, tuple(range(1, 10)), (1500.0,)),
+             I.Space(2, 5, 1, 6, tuple(range(1, 70)), (1500.0, 1980.0))][case]
+    tab = quantised_tables(space, 40 + case)
+    d = [torch.from_numpy(tab[k]).cuda() for k in ("t", "pw", "tc", "pc")]
+    T, E = kr.evaluate_partition(space, *d)
+    fr = kr.evaluate_and_filter(space, *d)
+    T, E = T.cpu().numpy(), E.cpu().numpy()
+    for p in range(space.n_parts):
+        Tr, Er = oracle_lib.evaluate_partition(space, tab["t"], tab["pw"], tab["tc"], tab["pc"], p)
+        assert_close(T[p], Tr, RT_TE, "T case %d part %d" % (case, p))
+        assert_close(E[p], Er, RT_TE, "E case %d part %d" % (case, p))
+        ix = oracle_lib.pareto(Tr, Er)
+        check_frontier(fr, p, (ix, Tr[ix], Er[ix]), "frontier case %d part %d" % (case, p))
+
+
 @pytest.mark.parametrize("cfg", [0, 1])
 def test_evaluate_and_filter_full(kr, oracle_lib, cfg):
     w = workload(cfg)
