@@ -82,15 +82,19 @@ __device__ __forceinline__ void finish_tail(const Tail &q, double p_static, doub
 // rows loaded one round earlier; the loads for its tail and for the next round are
 // issued right after the search, and the previous round's tail is finished while they
 // are in flight.  Cursors of a lane past its last position keep moving (their results
-// are discarded); only their LDS addresses are clamped.
-template <int R, int W, int SC>
+// are discarded); only their LDS addresses are clamped.  FX (32 kernels, 32 SM choices,
+// every lane on one run of at least R - 1 positions) makes the LDS offsets immediates
+// and lets every round but the last skip the validity selects.
+template <int R, int W, int SC, bool FX>
 __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOut o)
 {
     constexpr int K = KR_PAD;
     extern __shared__ double lds[];
+    static_assert(!FX || (SC == 32 && R == 17), "the fixed layout is the 32 x 32 one");
     const int N = a.N, S = SC > 0 ? SC : a.S, S1 = S + 1, slab = N * S1;
-    double *Lt = lds, *Lp = lds + a.w_pw;
-    ColRec *C0 = (ColRec *)(lds + a.w_a0);
+    const int pwo = FX ? KR_FIX32_PW : a.w_pw;  // power table offset (doubles)
+    double *Lt = lds, *Lp = lds + pwo;
+    ColRec *C0 = (ColRec *)(lds + (FX ? 2 * KR_FIX32_PW : a.w_a0));
     const int lane = threadIdx.x;
     const int p = blockIdx.x / a.nfb, fbk = blockIdx.x - p * a.nfb;
     const int f0 = fbk * a.fb, f1 = min(a.F, f0 + a.fb);
@@ -102,8 +106,7 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
     double *oT = o.T + slot0, *oE = o.E + slot0;
     int32_t *oI = o.I + slot0;
     int count = 0;
-    const double *Ct = Lt + sg;  // column sg of the time table; pw at + w_pw
-    const int pwo = a.w_pw;
+    const double *Ct = Lt + sg;  // column sg of the time table; pw at + pwo
     // filter scratch, all in the pad rows (restored after use): T in the time pad, E
     // in the power pad, indices after E in the power pad (a power pad of zeros reads
     // back the same whether as doubles or as pairs of zero ints).  The column sums
@@ -212,7 +215,7 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 const int pp = c0 + r;
-                const bool valid = r < nv;
+                const bool valid = (FX && r < R - 1) || r < nv;
                 if (r > 0 || ch > 0) {  // launch cursor: A[pp], B[pp] of column sg
                     pA = pA + qt;
                     pB = pB + qw * qt;
@@ -305,20 +308,21 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
     if (lane == 0) o.cnt[blockIdx.x] = count;
 }
 
-template <int R, int SC>
+template <int R, int SC, bool FX = false>
 static void launch_wave_r(const EvalArgs &a, const UnitOut &o, size_t lds, hipStream_t st)
 {
     const dim3 grid(a.P * a.nfb), block(64);
     if (a.dma16)
-        hipLaunchKernelGGL((eval_filter_wave_kernel<R, 16, SC>), grid, block, lds, st, a, o);
+        hipLaunchKernelGGL((eval_filter_wave_kernel<R, 16, SC, FX>), grid, block, lds, st, a, o);
     else
-        hipLaunchKernelGGL((eval_filter_wave_kernel<R, 4, SC>), grid, block, lds, st, a, o);
+        hipLaunchKernelGGL((eval_filter_wave_kernel<R, 4, SC, FX>), grid, block, lds, st, a, o);
 }
 
 hipError_t launch_eval_filter_wave(const EvalArgs &a, const UnitOut &o, hipStream_t st)
 {
     const size_t lds = (size_t)a.lds_doubles * sizeof(double);
-    if (a.S == 32 && a.R == 17) launch_wave_r<17, 32>(a, o, lds, st);
+    if (a.S == 32 && a.R == 17 && a.fixed32) launch_wave_r<17, 32, true>(a, o, lds, st);
+    else if (a.S == 32 && a.R == 17) launch_wave_r<17, 32>(a, o, lds, st);
     else if (a.S == 16 && a.R == 8) launch_wave_r<8, 16>(a, o, lds, st);
     else if (a.S == 8 && a.R == 8) launch_wave_r<8, 8>(a, o, lds, st);
     else {

@@ -11,6 +11,9 @@
 #define KR_FIN_UNITS 2048  // units per segment the finalize kernel's LDS path takes
 #define KR_TILE 2048       // points per tile of the stand-alone filter
 #define KR_PAD 4           // rows the wave kernel's end-cursor search reads per step
+// Power-slab offset (doubles) of the one-wave layout with 32 kernels and 32 SM choices:
+// t slab and pad rows, rounded up to keep the second table 16-byte aligned.
+#define KR_FIX32_PW (((32 + KR_PAD) * 33 + 1) / 2 * 2)
 
 namespace kr {
 
@@ -36,6 +39,11 @@ struct EvalArgs {
     int w_pw, w_a0;         // LDS offsets (doubles) of the power slab and the column sums
     int dma16;              // 16-byte direct copies (slab length even, tables 16-byte aligned)
     int wcap;               // candidates the wave filter's LDS scratch holds
+    // 32 kernels and 32 SM choices with every lane on one run of at least R - 1 = 16
+    // positions in one chunk (the evaluation stress shape): the kernel instance that
+    // takes the LDS layout and the validity of all but the last round as compile-time
+    // facts
+    int fixed32;
     // one wave per slab (two comm kernels, at most 8 SM choices): LDS offsets (doubles)
     // of the power slab, the running sums, the fresh and continuing second-phase
     // records and the filter scratch
