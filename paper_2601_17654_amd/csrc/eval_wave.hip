@@ -112,6 +112,10 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
     // back the same whether as doubles or as pairs of zero ints).  The column sums
     // are not touched: a run of several chunks reads them again after a filter.
     const Scratch sc{Lt + slab, Lp + slab, (int32_t *)(Lp + slab + a.wcap), a.wcap};
+    // Row clamps.  With FX every lane's runs end at or before position N and its last
+    // round is its only possibly idle one, so the cursors never pass row N and the
+    // loads one round ahead never pass row N + 1: the clamps hold by construction.
+    auto cap = [&](int x, int hi) { return FX ? x : min(x, hi); };
 
     // pad rows and the zero record (never overwritten by the slab copies)
     for (int x = lane; x < K * S1; x += 64) {
@@ -201,12 +205,12 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
                     bw[k] = b0p[k * S1 + pwo];
                 }
             };
-            load_batch(min(max(j, c0), N));
+            load_batch(cap(max(j, c0), N));
             {
                 const int pr = max(c0 - 1, 0);
                 qt = Ct[__umul24(pr, S1)];
                 qw = Ct[__umul24(pr, S1) + pwo];
-                const ColRec cs = C0[min(c0, N + 1)];
+                const ColRec cs = C0[cap(c0, N + 1)];
                 sA = cs.a;
                 sB = cs.b;
             }
@@ -253,7 +257,7 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
                         }
                     }
                 }
-                const int jc = min(j, N);  // j can pass N only on a lane past its positions
+                const int jc = cap(j, N);  // j can pass N only on a lane past its positions
                 Tail cur;
                 cur.j = jc;
                 cur.valid = valid;
@@ -270,11 +274,11 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
                     cur.c1 = C0[jc + 1];
                 }
                 if (r + 1 < R) {
-                    load_batch(min(max(j, pp + 1), N));
-                    const int pr = min(pp, N);
+                    load_batch(cap(max(j, pp + 1), N));
+                    const int pr = cap(pp, N);
                     qt = Ct[__umul24(pr, S1)];
                     qw = Ct[__umul24(pr, S1) + pwo];
-                    const ColRec cs = C0[min(pp + 1, N + 1)];
+                    const ColRec cs = C0[cap(pp + 1, N + 1)];
                     sA = cs.a;
                     sB = cs.b;
                 }
