@@ -144,10 +144,12 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
         {
             const int cc = lane == 0 ? 0 : sg;
             double sa = 0.0, sb = 0.0;
-            for (int i0 = 0; i0 < N; i0 += 8) {
+            const int Nl = FX ? 32 : N;  // FX: 32 kernels
+#pragma unroll 1
+            for (int i0 = 0; i0 < Nl; i0 += 8) {
                 const double *bt = Lt + (i0 * S1 + cc), *bw = Lp + (i0 * S1 + cc);
                 double vt[8], vw[8], ra[8], rb[8];
-                if (i0 + 8 <= N) {
+                if (FX || i0 + 8 <= N) {
 #pragma unroll
                     for (int q = 0; q < 8; ++q) {
                         vt[q] = bt[q * S1];
@@ -175,7 +177,7 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
                     double *c = (double *)(C0 + i0);
 #pragma unroll
                     for (int q = 0; q < 8; ++q)
-                        if (i0 + q < N) {
+                        if (FX || i0 + q < N) {
                             c[2 * q] = ra[q];
                             c[2 * q + 1] = rb[q];
                         }
