@@ -248,12 +248,15 @@ __device__ __forceinline__ void copy_to_lds_nw(const double *g, double *l, int n
 // wave's slot; at the end of a slab those points (usually many times the slab's own
 // frontier) are read back into the second-phase tables, idle by then, sorted, and
 // replaced in place by their frontier, when they fit there.  SC > 0 fixes the number of
-// SM choices at compile time.
-template <int R, int W, int NW, int SC>
+// SM choices at compile time; FN also fixes the two-comm workload's 48 kernels and 33
+// launch positions.
+template <int R, int W, int NW, int SC, bool FN>
 __global__ void __launch_bounds__(64 * NW) eval_filter_pair_kernel(EvalArgs a, UnitOut o)
 {
     extern __shared__ __attribute__((aligned(16))) double lds[];
-    const int N = a.N, S = SC > 0 ? SC : a.S, S1 = S + 1, SS = S * S, slab = N * S1, np = a.n_pos;
+    static_assert(!FN || SC > 0, "the fixed shape fixes the SM choices too");
+    const int N = FN ? 48 : a.N, S = SC > 0 ? SC : a.S, S1 = S + 1, SS = S * S, slab = N * S1;
+    const int np = FN ? 33 : a.n_pos;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     double *const Lt = lds, *const Lp = lds + a.q_pw;
     ColRec *const AB = (ColRec *)(lds + a.q_ab);
@@ -416,12 +419,14 @@ hipError_t launch_eval_filter_pair(const EvalArgs &a, const UnitOut &o, hipStrea
     const size_t lds = (size_t)a.lds_doubles * sizeof(double);
     constexpr int NW = KR_PAIR_WAVES;
     const dim3 grid(a.P * a.nfb), block(64 * NW);
-    if (a.dma16 && a.S == 8)
-        hipLaunchKernelGGL((eval_filter_pair_kernel<8, 16, NW, 8>), grid, block, lds, st, a, o);
+    if (a.dma16 && a.S == 8 && a.N == 48 && a.n_pos == 33)
+        hipLaunchKernelGGL((eval_filter_pair_kernel<8, 16, NW, 8, true>), grid, block, lds, st, a, o);
+    else if (a.dma16 && a.S == 8)
+        hipLaunchKernelGGL((eval_filter_pair_kernel<8, 16, NW, 8, false>), grid, block, lds, st, a, o);
     else if (a.dma16)
-        hipLaunchKernelGGL((eval_filter_pair_kernel<8, 16, NW, 0>), grid, block, lds, st, a, o);
+        hipLaunchKernelGGL((eval_filter_pair_kernel<8, 16, NW, 0, false>), grid, block, lds, st, a, o);
     else
-        hipLaunchKernelGGL((eval_filter_pair_kernel<8, 4, NW, 0>), grid, block, lds, st, a, o);
+        hipLaunchKernelGGL((eval_filter_pair_kernel<8, 4, NW, 0, false>), grid, block, lds, st, a, o);
     return hipGetLastError();
 }
 
