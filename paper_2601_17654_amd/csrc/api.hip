@@ -70,9 +70,9 @@ bool wave_plan(EvalArgs *a)
     const int maxrun = std::max(std::min(a->span, a->n_pos), last);
     a->R = maxrun <= 2 ? 2 : maxrun <= 4 ? 4 : maxrun <= 8 ? 8 : 17;
     a->nch = (maxrun + a->R - 1) / a->R;
-    a->fixed32 = a->N == 32 && a->S == 32 && a->R == 17 && a->nch == 1 && a->H * a->S == 64 &&
-                 std::min(a->span, last) >= a->R - 1 && a->w_pw == KR_FIX32_PW &&
-                 a->w_a0 == 2 * KR_FIX32_PW;
+    a->fixed32 = a->N == 32 && a->S == 32 && a->n_pos == 33 && a->H == 2 && a->span == 16 &&
+                 a->R == 17 && a->nch == 1 && std::min(a->span, last) >= a->R - 1 &&
+                 a->w_pw == KR_FIX32_PW && a->w_a0 == 2 * KR_FIX32_PW;
     // filter scratch: the pad rows of each table
     // (the power pad holds cap doubles of E, then cap ints of indices)
     a->wcap = (int)std::min<int64_t>(64, KR_PAD * (a->S + 1) * 2 / 3);

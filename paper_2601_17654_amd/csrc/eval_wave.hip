@@ -82,16 +82,17 @@ __device__ __forceinline__ void finish_tail(const Tail &q, double p_static, doub
 // rows loaded one round earlier; the loads for its tail and for the next round are
 // issued right after the search, and the previous round's tail is finished while they
 // are in flight.  Cursors of a lane past its last position keep moving (their results
-// are discarded); only their LDS addresses are clamped.  FX (32 kernels, 32 SM choices,
-// every lane on one run of at least R - 1 positions) makes the LDS offsets immediates
-// and lets every round but the last skip the validity selects.
+// are discarded); only their LDS addresses are clamped.  FX (32 kernels, 33 positions,
+// 32 SM choices: runs of 16 and 17 positions) makes the sizes and LDS offsets
+// immediates and lets every round but the last skip the validity selects.
 template <int R, int W, int SC, bool FX>
 __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOut o)
 {
     constexpr int K = KR_PAD;
     extern __shared__ double lds[];
     static_assert(!FX || (SC == 32 && R == 17), "the fixed layout is the 32 x 32 one");
-    const int N = a.N, S = SC > 0 ? SC : a.S, S1 = S + 1, slab = N * S1;
+    const int N = FX ? 32 : a.N, S = SC > 0 ? SC : a.S, S1 = S + 1, slab = N * S1;
+    const int nH = FX ? 2 : a.H, nspan = FX ? 16 : a.span, npos = FX ? 33 : a.n_pos, nch = FX ? 1 : a.nch;
     const int pwo = FX ? KR_FIX32_PW : a.w_pw;  // power table offset (doubles)
     double *Lt = lds, *Lp = lds + pwo;
     ColRec *C0 = (ColRec *)(lds + (FX ? 2 * KR_FIX32_PW : a.w_a0));
@@ -99,9 +100,9 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
     const int p = blockIdx.x / a.nfb, fbk = blockIdx.x - p * a.nfb;
     const int f0 = fbk * a.fb, f1 = min(a.F, f0 + a.fb);
     const int s = lane % S, h = lane / S, sg = s + 1;
-    const bool on = h < a.H;
-    const int plo = on ? min(a.n_pos, h * a.span) : 0;
-    const int phi = on ? (h == a.H - 1 ? a.n_pos : min(a.n_pos, plo + a.span)) : 0;
+    const bool on = h < nH;
+    const int plo = on ? min(npos, h * nspan) : 0;
+    const int phi = on ? (h == nH - 1 ? npos : min(npos, plo + nspan)) : 0;
     const size_t slot0 = (size_t)p * a.C + (size_t)f0 * a.Cf;
     double *oT = o.T + slot0, *oE = o.E + slot0;
     int32_t *oI = o.I + slot0;
@@ -194,7 +195,7 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
 
         int j = plo;  // end cursor
         double jA = pA, jB = pB;
-        for (int ch = 0; ch < a.nch; ++ch) {
+        for (int ch = 0; ch < nch; ++ch) {
             const int c0 = plo + ch * R;
             const int nv = max(0, min(R, phi - c0));
             double vT[R], vE[R];
@@ -296,7 +297,7 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
             finish_tail(prev, a.p_static, ctail, a0, b0, vT[R - 1], vE[R - 1]);
             tl = vmin(tl, vT[R - 1]);
             el = vmin(el, vE[R - 1]);
-            if (ch == a.nch - 1 && f + 1 < f1) {
+            if (ch == nch - 1 && f + 1 < f1) {
                 // every LDS read of this slab has returned: the next slab may land
                 wave_lds_fence();
                 __builtin_amdgcn_s_waitcnt(KR_WAIT_LGKM0);

@@ -39,10 +39,10 @@ struct EvalArgs {
     int w_pw, w_a0;         // LDS offsets (doubles) of the power slab and the column sums
     int dma16;              // 16-byte direct copies (slab length even, tables 16-byte aligned)
     int wcap;               // candidates the wave filter's LDS scratch holds
-    // 32 kernels and 32 SM choices with every lane on one run of at least R - 1 = 16
-    // positions in one chunk (the evaluation stress shape): the kernel instance that
-    // takes the LDS layout and the validity of all but the last round as compile-time
-    // facts
+    // 32 kernels, 33 launch positions and 32 SM choices (the evaluation stress shape):
+    // two runs of 16 and 17 positions per SM choice, one chunk each.  The kernel instance
+    // for it takes the sizes, the LDS layout and the validity of all but the last round
+    // as compile-time facts
     int fixed32;
     // one wave per slab (two comm kernels, at most 8 SM choices): LDS offsets (doubles)
     // of the power slab, the running sums, the fresh and continuing second-phase

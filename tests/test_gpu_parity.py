@@ -683,14 +683,15 @@ def test_negative_zero_energies(kr, oracle_lib):
     compare_composed(kr, comp, ref, off, T, E, "-0 energies")
 
 
-@pytest.mark.parametrize("shape", [(32, 33, 5), (32, 20, 2), (8, 9, 3), (20, 17, 2), (35, 36, 2),
-                                   (40, 41, 2), (12, 8, 4), (1, 2, 3)])
+@pytest.mark.parametrize("shape", [(32, 33, 5), (32, 32, 2), (32, 20, 2), (8, 9, 3), (20, 17, 2),
+                                   (35, 36, 2), (40, 41, 2), (12, 8, 4), (1, 2, 3)])
 @pytest.mark.parametrize("tc_scale", [1.0, 1e-3, 30.0])
 def test_fused_32_sm_choices_shapes(kr, oracle_lib, shape, tc_scale):
     """One comm kernel with 32 SM choices (the SM-choice count of the evaluation stress
     workload): kernel counts 1 to 40, launch positions from 2 to N + 1 (32 kernels with
-    33 positions take the kernel instance with the fixed layout, with 20 the general
-    one), short and long comm, every partition's fused frontier against the oracle."""
+    33 positions take the kernel instance with the fixed sizes, with 32 or 20 the
+    general one), short and long comm, every partition's fused frontier against the
+    oracle."""
     N, n_pos, F = shape
     K = tuple(range(1, 33))
     freqs = tuple(1005.0 + 975.0 * q / max(F - 1, 1) for q in range(F))
