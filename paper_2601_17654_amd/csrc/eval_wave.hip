@@ -92,7 +92,8 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
     extern __shared__ double lds[];
     static_assert(!FX || (SC == 32 && R == 17), "the fixed layout is the 32 x 32 one");
     const int N = FX ? 32 : a.N, S = SC > 0 ? SC : a.S, S1 = S + 1, slab = N * S1;
-    const int nH = FX ? 2 : a.H, nspan = FX ? 16 : a.span, npos = FX ? 33 : a.n_pos, nch = FX ? 1 : a.nch;
+    const int nH = FX ? 2 : a.H, nspan = FX ? 16 : a.span;
+    const int npos = FX ? 33 : a.n_pos, nch = FX ? 1 : a.nch;
     const int pwo = FX ? KR_FIX32_PW : a.w_pw;  // power table offset (doubles)
     double *Lt = lds, *Lp = lds + pwo;
     ColRec *C0 = (ColRec *)(lds + (FX ? 2 * KR_FIX32_PW : a.w_a0));
@@ -145,9 +146,8 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
         {
             const int cc = lane == 0 ? 0 : sg;
             double sa = 0.0, sb = 0.0;
-            const int Nl = FX ? 32 : N;  // FX: 32 kernels
 #pragma unroll 1
-            for (int i0 = 0; i0 < Nl; i0 += 8) {
+            for (int i0 = 0; i0 < N; i0 += 8) {
                 const double *bt = Lt + (i0 * S1 + cc), *bw = Lp + (i0 * S1 + cc);
                 double vt[8], vw[8], ra[8], rb[8];
                 if (FX || i0 + 8 <= N) {
