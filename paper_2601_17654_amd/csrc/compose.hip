@@ -825,21 +825,37 @@ hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipEvent_t *
 // back-pointer) and then the next back-pointer (a load that depends on the offset).  The
 // wave loads the next row's back-pointers for the KR_EX_SPEC bins just below the current
 // one while the offset is in flight, so a step costs one memory latency when the offset
-// is below KR_EX_SPEC (else one more load).
+// is below KR_EX_SPEC (else one more load).  With ST (at most KR_EX_LP partitions) the
+// partition offsets are staged in LDS first and the choices are kept there until the
+// walk ends, so no step waits for an offset load or for a store.
 #define KR_EX_SPEC 128
 #define KR_EX_RS 2048  // partitions per pass of the final sums
+#define KR_EX_LP 2048  // most partitions whose offsets and choices the walk keeps in LDS
 
+template <bool ST>
 __global__ void __launch_bounds__(64) extract_kernel(ExtractArgs a)
 {
     __shared__ double sT[KR_EX_RS], sE[KR_EX_RS];
+    __shared__ int64_t s_off[ST ? KR_EX_LP + 1 : 1];
+    __shared__ int32_t s_ch[ST ? KR_EX_LP : 1];
     const int P = a.P;
     const int q = blockIdx.x, lane = threadIdx.x;
     int32_t *choice = a.choice + (int64_t)q * a.P;
+    auto off_at = [&](int k) -> int64_t {
+        if constexpr (ST) return s_off[k];
+        else return a.off[k];
+    };
+    if constexpr (ST) {
+        for (int k = lane; k <= P; k += 64) s_off[k] = a.off[k];
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+    }
     int64_t b = a.bins[q];
     bool ok = b >= 0 && b < a.B;
     int32_t j = ok ? a.bp[(int64_t)(a.P - 1) * a.B + b] : -1;
+    int64_t lo = off_at(P - 1), hi = off_at(P);
     for (int k = a.P - 1; k >= 0 && ok; --k) {
-        const int64_t lo = a.off[k], n = a.off[k + 1] - lo;
+        const int64_t n = hi - lo;
         if (j < 0 || j >= n) {
             ok = false;
             break;
@@ -852,7 +868,15 @@ __global__ void __launch_bounds__(64) extract_kernel(ExtractArgs a)
             spec[i] = k > 0 && src >= 0 ? row[src] : -1;
         }
         const int64_t b2 = a.pt_bin[lo + j];
-        if (lane == 0) choice[k] = j;
+        if constexpr (ST) {
+            if (lane == 0) s_ch[k] = j;
+        } else {
+            if (lane == 0) choice[k] = j;
+        }
+        if (k > 0) {  // the next partition's offsets, while the loads are in flight
+            hi = lo;
+            lo = off_at(k - 1);
+        }
         b -= b2;
         if (b < 0) {
             ok = false;
@@ -871,15 +895,26 @@ __global__ void __launch_bounds__(64) extract_kernel(ExtractArgs a)
     ok = ok && b == 0;
     // Exact T and E of the choice: the lanes gather the chosen points' values into LDS,
     // one lane adds them in partition order.
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's choice stores are done
+    if constexpr (ST) {
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+    } else {
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's choice stores are done
+    }
     double Ts = 0.0, Es = 0.0;
     for (int k0 = 0; k0 < P; k0 += KR_EX_RS) {
         const int kn = min(P - k0, KR_EX_RS);
         for (int i = lane; i < kn; i += 64) {
             const int kk = k0 + i;
             if (ok) {
-                const int32_t c = load_l2(choice + kk);
-                const int64_t x = a.off[kk] + c;
+                int32_t c;
+                if constexpr (ST) {
+                    c = s_ch[kk];
+                    choice[kk] = c;
+                } else {
+                    c = load_l2(choice + kk);
+                }
+                const int64_t x = off_at(kk) + c;
                 sT[i] = a.T[x];
                 sE[i] = a.E[x];
                 if (a.cand_idx) a.choice_cand[(int64_t)q * P + kk] = a.cand_idx[x];
@@ -907,7 +942,10 @@ __global__ void __launch_bounds__(64) extract_kernel(ExtractArgs a)
 hipError_t launch_extract(const ExtractArgs &a, hipStream_t st)
 {
     if (a.n_q == 0) return hipSuccess;
-    hipLaunchKernelGGL(extract_kernel, dim3(a.n_q), dim3(64), 0, st, a);
+    if (a.P <= KR_EX_LP)
+        hipLaunchKernelGGL(extract_kernel<true>, dim3(a.n_q), dim3(64), 0, st, a);
+    else
+        hipLaunchKernelGGL(extract_kernel<false>, dim3(a.n_q), dim3(64), 0, st, a);
     return hipGetLastError();
 }
 
