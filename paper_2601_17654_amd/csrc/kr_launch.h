@@ -10,7 +10,7 @@
 #define KR_PAIR_WAVES 4    // waves per block of the two-comm evaluation kernel
 #define KR_FIN_UNITS 2048  // units per segment the finalize kernel's LDS path takes
 #define KR_TILE 2048       // points per tile of the stand-alone filter
-#define KR_PAD 4           // rows the wave kernel's end-cursor search reads per step
+#define KR_PAD 3           // rows the wave kernel's end-cursor search reads per step
 // Power-slab offset (doubles) of the one-wave layout with 32 kernels and 32 SM choices:
 // t slab and pad rows, rounded up to keep the second table 16-byte aligned.
 #define KR_FIX32_PW (((32 + KR_PAD) * 33 + 1) / 2 * 2)
