@@ -291,13 +291,17 @@ __global__ void __launch_bounds__(KR_BLOCK) wavefront_fill_kernel(ComposeArgs a,
 }
 
 #define KR_WF_MC 512  // steps per chunk of the block's step-metadata ring
-#define KR_WF_LO 8    // window entries below offset H (read only by padding offsets)
+// Window entries below offset H (read only by padding offsets).  Odd, with an even row
+// length, so that a thread's group reads (which start 7 entries below an even bin)
+// begin at an even index of either row: 16-byte aligned.
+#define KR_WF_LO 9
 #define KR_WF_S 8     // offset slices of the dense scan (block = 128 bin pairs x 8 slices)
 
 struct WavefrontLds {
     // Window of step k in buffer k & 1: win[LO + H + i] = F_{k-1}[b0 + i] for i in
-    // [-M_k, W), the halo and then the tile's own bins.
-    double win[2][KR_WF_LO + KR_MP_HCAP + KR_MP_W];
+    // [-M_k, W), the halo and then the tile's own bins (one spare entry keeps the row
+    // length even).
+    alignas(16) double win[2][KR_WF_LO + KR_MP_HCAP + KR_MP_W + 1];
     // Records of step k in buffer k & 1: the dense least-energy table e_k[0 .. 8
     // ceil((M_k + 1) / 8)) (INFINITY past M_k) with its points, or the occupied offsets
     // only (b2 * 8 in off8).
@@ -555,10 +559,13 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
         if (active) {
             if (dense) {
                 // Thread (pair j, slice q): bins 2j and 2j + 1 over the slice's groups of
-                // 8 offsets.  A group needs 9 window entries and 8 table entries, which
-                // come from memory through the scalar cache (the table does not change
-                // during the launch).  The running minimum takes one v_min per pair; the
-                // group where it last fell is kept and rescanned when combining.
+                // 8 offsets.  A group needs 9 window entries and 8 table entries; the
+                // table comes from memory through the scalar cache (it does not change
+                // during the launch).  The first 8 window entries are four aligned
+                // 16-byte reads: threads 16 bytes apart then read without LDS bank
+                // conflicts (8-byte reads at that stride conflict four ways).  The
+                // running minimum takes one v_min per pair; the group where it last fell
+                // is kept and rescanned when combining.
                 const int j = tid % (KR_MP_W / 2);
                 const int q = __builtin_amdgcn_readfirstlane(tid / (KR_MP_W / 2));
                 const int ng = (mc.x + 8) / 8;
@@ -591,11 +598,20 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
                     const double *wa = wc + 2 * j - 8 * g0 - 7;
                     double xa[9], xb[9], xc[9], ea[8], eb[8], ec[8];
 #pragma unroll
-                    for (int d = 0; d < 9; ++d) {
-                        xa[d] = wa[d];
-                        xb[d] = wa[d - 8];
-                        xc[d] = wa[d - 16];
+                    for (int d = 0; d < 4; ++d) {
+                        const double2 va = ((const double2 *)wa)[d];
+                        const double2 vb = ((const double2 *)(wa - 8))[d];
+                        const double2 vc = ((const double2 *)(wa - 16))[d];
+                        xa[2 * d] = va.x;
+                        xa[2 * d + 1] = va.y;
+                        xb[2 * d] = vb.x;
+                        xb[2 * d + 1] = vb.y;
+                        xc[2 * d] = vc.x;
+                        xc[2 * d + 1] = vc.y;
                     }
+                    xa[8] = wa[8];
+                    xb[8] = wa[0];
+                    xc[8] = wa[-8];
 #pragma unroll
                     for (int o = 0; o < 8; ++o) {
                         ea[o] = et[8 * g0 + o];
@@ -611,10 +627,16 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
                     const double *wa = wc + 2 * j - 8 * g - 7, *wb = wc + 2 * j - 8 * h - 7;
                     double xa[9], xb[9], ea[8], eb[8];  // xa[d]: F at bin 2j + d - 7 - 8g
 #pragma unroll
-                    for (int d = 0; d < 9; ++d) {
-                        xa[d] = wa[d];
-                        xb[d] = wb[d];
+                    for (int d = 0; d < 4; ++d) {
+                        const double2 va = ((const double2 *)wa)[d];
+                        const double2 vb = ((const double2 *)wb)[d];
+                        xa[2 * d] = va.x;
+                        xa[2 * d + 1] = va.y;
+                        xb[2 * d] = vb.x;
+                        xb[2 * d + 1] = vb.y;
                     }
+                    xa[8] = wa[8];
+                    xb[8] = wb[8];
 #pragma unroll
                     for (int o = 0; o < 8; ++o) {
                         ea[o] = et[8 * g + o];
