@@ -382,8 +382,10 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
         return bitsd(v);
     };
 
-    // Loader registers: the next step's records and halo entries.  The loads are
-    // unconditional (a thread with nothing to load reads a valid dummy address).
+    // Loader registers: the next step's records and halo entries.  A wave issues a
+    // round of loads only if some lane of it has an entry in that round (dense steps
+    // skip the occupied-offset list); within such a round the loads are unconditional
+    // (a lane with nothing to load reads a valid dummy address).
     uint64_t hv[2], re[2];
     int32_t ro[2], ra[2];
     auto halo_src = [&](int4 m, int Lprev, int h, int64_t &src) {
@@ -391,18 +393,27 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
         src = b0 - m.x + i;
         return m.x <= H && i < m.x && src >= 0 && src < Lprev;
     };
+    const int ws = __builtin_amdgcn_readfirstlane(s & ~63);  // the wave's first loader index
     auto issue = [&](int k, int4 m, int Lprev) {  // loads for step k
         const bool dense = dense_step(m);
+        const int n = dense ? 8 * ((m.x + 8) / 8) : m.w;
 #pragma unroll
         for (int r = 0; r < 2; ++r) {
+            if (ws + r * NS >= n) continue;  // wave-uniform
             const int i = s + r * NS;
             const int64_t xd = m.z + max(0, min(i, m.x + 7)), xs = m.z + max(0, min(i, m.w - 1));
-            re[r] = dense ? w.ebits[xd] : *(const uint64_t *)(w.oe + xs);
-            ra[r] = *(dense ? w.earg + xd : w.oarg + xs);
-            ro[r] = w.ob2[xs];
+            if (dense) {
+                re[r] = w.ebits[xd];
+                ra[r] = w.earg[xd];
+            } else {
+                re[r] = *(const uint64_t *)(w.oe + xs);
+                ra[r] = w.oarg[xs];
+                ro[r] = w.ob2[xs];
+            }
         }
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
+            if (ws + h * NS >= m.x) continue;  // wave-uniform
             int64_t src;
             const bool need = halo_src(m, Lprev, h, src);
             hv[h] = load_l2(Fh + (int64_t)(k - 1) * B + (need ? src : 0));
@@ -410,13 +421,14 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
     };
     auto stage = [&](int k, int4 m, int Lprev) {  // the loads of issue(k) into LDS
         const int buf = k & 1;
-        const int n = dense_step(m) ? 8 * ((m.x + 8) / 8) : m.w;
+        const bool dense = dense_step(m);
+        const int n = dense ? 8 * ((m.x + 8) / 8) : m.w;
 #pragma unroll
         for (int r = 0; r < 2; ++r) {
             const int i = s + r * NS;
             if (i < n) {
                 sm.e[buf][i] = bitsd(re[r]);
-                sm.off8[buf][i] = ro[r] * 8;
+                if (!dense) sm.off8[buf][i] = ro[r] * 8;
                 sm.arg[buf][i] = ra[r];
             }
         }
@@ -437,7 +449,6 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
     };
     // Whether this loader wave has records or halo entries of step k to move (most
     // loader waves have none when the offset range is short).
-    const int ws = __builtin_amdgcn_readfirstlane(s & ~63);
     auto busy = [&](int4 m) { return ws < max(dense_step(m) ? 8 * ((m.x + 8) / 8) : m.w, m.x); };
     auto publish = [&](int k, double v, int M1, int L) {
         uint64_t bits = dbits(v);
@@ -681,15 +692,24 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
         } else if (!last) {
             // chunk c + 1 replaces chunk c - 1 once step cMC - 1 has read its metadata
             if ((k + 1) % MC == 0) load_meta((k + 1) / MC + 1);
+            // Bring the next step's table into the scalar cache, where the dense scan
+            // reads it: the first and last entry of each group of 8.  A wave's first
+            // group is touched before the staging and consumed after it, so the loads
+            // fly meanwhile; further groups (offset ranges above 12 groups) follow.
+            const bool touch = dense_step(mn) && b0 < mn.y;
+            const_f64 *et = (const_f64 *)(w.ebits + mn.z);
+            const int ng = (mn.x + 8) / 8, g0 = ws / 64;
+            double e0 = 0.0, e7 = 0.0;
+            if (touch && g0 < ng) {
+                e0 = et[8 * g0];
+                e7 = et[8 * g0 + 7];
+            }
             if (moves) stage(k + 1, mn, mc.y);
-            if (dense_step(mn) && b0 < mn.y) {
-                // bring the next step's table into the scalar cache, where the dense
-                // scan reads it: the first and last entry of each group of 8
-                const_f64 *et = (const_f64 *)(w.ebits + mn.z);
-                const int ng = (mn.x + 8) / 8;
-                for (int g = ws / 64; g < ng; g += NS / 64) {
-                    const double e0 = et[8 * g], e7 = et[8 * g + 7];
-                    asm volatile("" ::"s"(e0), "s"(e7));
+            asm volatile("" ::"s"(e0), "s"(e7));
+            if (touch) {
+                for (int g = g0 + NS / 64; g < ng; g += NS / 64) {
+                    const double f0 = et[8 * g], f7 = et[8 * g + 7];
+                    asm volatile("" ::"s"(f0), "s"(f7));
                 }
             }
         }
