@@ -208,7 +208,7 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
                     bw[k] = b0p[k * S1 + pwo];
                 }
             };
-            load_batch(cap(max(j, c0), N));
+            load_batch(cap(j, N));
             {
                 const int pr = max(c0 - 1, 0);
                 qt = Ct[__umul24(pr, S1)];
@@ -227,12 +227,10 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
                     pA = pA + qt;
                     pB = pB + qw * qt;
                 }
-                if (j < pp) {
-                    j = pp;
-                    jA = pA;
-                    jB = pB;
-                }
-                // end cursor: the largest j with A[j] - A[pp] <= tcm
+                // End cursor: the largest j with A[j] - A[pp] <= tcm.  It is at least
+                // pp - 1 here; at pp - 1 the first row of the batch moves it to pp, since
+                // its sum A[pp] is formed by the same additions as the launch cursor's
+                // (the difference is exactly 0, never above the comm time).
                 bool go = valid;
 #pragma unroll
                 for (int k = 0; k < K; ++k) {
@@ -247,17 +245,18 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
                         }
                     }
                 }
-                if (__ballot(go && j < N)) {  // K or more kernels: one row at a time
-                    while (go && j < N) {
-                        const double t1 = Ct[__umul24(j, S1)], w1 = Ct[__umul24(j, S1) + pwo];
-                        const double nA = jA + t1;
-                        if (nA - pA <= tcm) {
-                            jA = nA;
-                            jB = jB + w1 * t1;
-                            ++j;
-                        } else {
-                            go = false;
-                        }
+                // K or more kernels: one row at a time, never past row N (with finite
+                // inputs the pad row N stops a cursor by itself; the bound also ends the
+                // walk for unchecked inputs such as an infinite comm time)
+                while (go && j < N) {
+                    const double t1 = Ct[__umul24(j, S1)], w1 = Ct[__umul24(j, S1) + pwo];
+                    const double nA = jA + t1;
+                    if (nA - pA <= tcm) {
+                        jA = nA;
+                        jB = jB + w1 * t1;
+                        ++j;
+                    } else {
+                        go = false;
                     }
                 }
                 const int jc = cap(j, N);  // j can pass N only on a lane past its positions
@@ -277,7 +276,7 @@ __global__ void __launch_bounds__(64) eval_filter_wave_kernel(EvalArgs a, UnitOu
                     cur.c1 = C0[jc + 1];
                 }
                 if (r + 1 < R) {
-                    load_batch(cap(max(j, pp + 1), N));
+                    load_batch(cap(j, N));
                     const int pr = cap(pp, N);
                     qt = Ct[__umul24(pr, S1)];
                     qw = Ct[__umul24(pr, S1) + pwo];
