@@ -203,6 +203,8 @@ size_t kr_evaluate_and_filter_workspace(const kr_space *space);
  *   F_out        device [B]       F_P (+inf where unreachable)
  *   bp_out       device [P][B]    point index (relative to its partition) chosen for
  *                                 partition k at composite bin b of F_k; -1 if none
+ *   bp_off_out   device [P][B] or NULL: the offset of that point (-1 if none), so
+ *                                 that a walk back needs one table instead of two
  *   pt_bin_out   device [off[P]]  offset of every point
  *   info_out     device [2]       delta, tmin_sum
  *   L_out        device [1]       reachable bins 1 + sum_k M_k
@@ -217,7 +219,8 @@ size_t kr_evaluate_and_filter_workspace(const kr_space *space);
  */
 kr_status kr_compose_frontiers(int32_t n_parts, const int64_t *off, const double *T,
                                const double *E, int32_t n_bins, double delta, double *F_out,
-                               int32_t *bp_out, int32_t *pt_bin_out, double *info_out,
+                               int32_t *bp_out, int32_t *bp_off_out, int32_t *pt_bin_out,
+                               double *info_out,
                                int32_t *L_out, int32_t *stair_bin, double *stair_Tlo,
                                double *stair_E, int32_t *n_stair, int32_t *status_out,
                                void *ws, size_t ws_bytes, void *stream);
@@ -229,6 +232,9 @@ size_t kr_compose_frontiers_workspace(int32_t n_parts, int32_t n_bins);
  * back-pointers from the last partition to the first, peeling off each chosen
  * point's offset.
  *   bp, pt_bin, off, T, E   as produced / consumed by kr_compose_frontiers
+ *   bp_off        the offsets kr_compose_frontiers recorded in bp_off_out, or NULL.
+ *                 With them the walk reads one table, many rows ahead; without them it
+ *                 looks each chosen point's offset up in pt_bin (same results)
  *   bins          device [n_q] query bins
  *   cand_idx      device [off[P]] or NULL: candidate index of every frontier point
  *                 (out_idx of kr_evaluate_and_filter); when given, choice_cand_out
@@ -240,7 +246,8 @@ size_t kr_compose_frontiers_workspace(int32_t n_parts, int32_t n_bins);
  *   ok_out        device [n_q] 1 if the bin was reachable and the walk consistent
  */
 kr_status kr_extract_schedule(int32_t n_parts, int32_t n_bins, const int32_t *bp,
-                              const int32_t *pt_bin, const int64_t *off, const double *T,
+                              const int32_t *bp_off, const int32_t *pt_bin,
+                              const int64_t *off, const double *T,
                               const double *E, const int32_t *bins, int32_t n_q,
                               const int32_t *cand_idx, int32_t *choice_out,
                               int32_t *choice_cand_out, double *T_out, double *E_out,

@@ -47,10 +47,10 @@ _SIGS = {
                                       _vp, _sz, _vp]),
     "kr_evaluate_and_filter_workspace": (_sz, [_SP]),
     "kr_compose_frontiers": (_i32, [_i32, _vp, _vp, _vp, _i32, _f64, _vp, _vp, _vp, _vp, _vp, _vp,
-                                    _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+                                    _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "kr_compose_frontiers_workspace": (_sz, [_i32, _i32]),
-    "kr_extract_schedule": (_i32, [_i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
-                                   _vp, _vp, _vp, _vp]),
+    "kr_extract_schedule": (_i32, [_i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp,
+                                   _vp, _vp, _vp, _vp, _vp]),
     "kr_decode_candidates": (_i32, [_SP, _vp, _i64, _vp, _vp, _vp, _vp]),
     "kr_microbatch_frontier": (_i32, [_i32, _i32, _vp, _vp, _vp, _i64, _i32, _vp, _i32, _vp, _vp,
                                       _i32, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
@@ -286,6 +286,7 @@ def evaluate_and_filter(space, t, pw, tc, pc, cap: Optional[int] = None,
 class Composed:
     F: torch.Tensor          # float64 [B]
     bp: torch.Tensor         # int32 [P][B]
+    bp_off: torch.Tensor     # int32 [P][B]: offset of each chosen point
     pt_bin: torch.Tensor     # int32 [n_points]
     info: torch.Tensor       # float64 [2]: delta, tmin_sum
     L: torch.Tensor          # int32 [1]
@@ -312,6 +313,7 @@ def compose_frontiers(off, T, E, n_bins: int, delta: float = 0.0, out: Optional[
         f64 = dict(dtype=torch.float64, device="cuda")
         i32 = dict(dtype=torch.int32, device="cuda")
         out = Composed(torch.empty(B, **f64), torch.empty((P, B), **i32),
+                       torch.empty((P, B), **i32),
                        torch.empty(max(T.numel(), 1), **i32), torch.empty(2, **f64),
                        torch.empty(1, **i32), torch.empty(B, **i32), torch.empty(B, **f64),
                        torch.empty(B, **f64), torch.empty(1, **i32), torch.empty(1, **i32))
@@ -319,15 +321,17 @@ def compose_frontiers(off, T, E, n_bins: int, delta: float = 0.0, out: Optional[
     ws = _workspace(wsb)
     _check("kr_compose_frontiers",
            _lib.kr_compose_frontiers(P, _ptr(off), _ptr(T), _ptr(E), B, float(delta), _ptr(out.F),
-                                     _ptr(out.bp), _ptr(out.pt_bin), _ptr(out.info), _ptr(out.L),
+                                     _ptr(out.bp), _ptr(out.bp_off), _ptr(out.pt_bin),
+                                     _ptr(out.info), _ptr(out.L),
                                      _ptr(out.stair_bin), _ptr(out.stair_Tlo), _ptr(out.stair_E),
                                      _ptr(out.n_stair), _ptr(out.status), _ptr(ws), wsb,
                                      _stream()))
     return out
 
 
-def extract_schedule(comp: Composed, off, T, E, bins, cand_idx=None):
-    """Per-partition choice behind each query bin.
+def extract_schedule(comp: Composed, off, T, E, bins, cand_idx=None, use_offsets: bool = True):
+    """Per-partition choice behind each query bin (use_offsets=False walks without the
+    recorded offsets, looking each point's offset up instead).
     Returns (choice [n_q][P], choice_cand [n_q][P] or None, T [n_q], E [n_q], ok [n_q])."""
     off = _dev(off, torch.int64, "off")
     T = _dev(T, torch.float64, "T").reshape(-1)
@@ -344,7 +348,9 @@ def extract_schedule(comp: Composed, off, T, E, bins, cand_idx=None):
     Es = torch.empty(nq, dtype=torch.float64, device="cuda")
     ok = torch.empty(nq, dtype=torch.int32, device="cuda")
     _check("kr_extract_schedule",
-           _lib.kr_extract_schedule(P, B, _ptr(comp.bp), _ptr(comp.pt_bin), _ptr(off), _ptr(T),
+           _lib.kr_extract_schedule(P, B, _ptr(comp.bp),
+                                    _ptr(comp.bp_off) if use_offsets else None,
+                                    _ptr(comp.pt_bin), _ptr(off), _ptr(T),
                                     _ptr(E), _ptr(bins), nq, _ptr(cand_idx), _ptr(choice), _ptr(cc),
                                     _ptr(Ts), _ptr(Es), _ptr(ok), _stream()))
     return choice, cc, Ts, Es, ok

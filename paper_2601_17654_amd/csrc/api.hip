@@ -396,7 +396,8 @@ size_t kr_compose_frontiers_workspace(int32_t n_parts, int32_t n_bins)
 
 kr_status kr_compose_frontiers(int32_t n_parts, const int64_t *off, const double *T,
                                const double *E, int32_t n_bins, double delta, double *F_out,
-                               int32_t *bp_out, int32_t *pt_bin_out, double *info_out,
+                               int32_t *bp_out, int32_t *bp_off_out, int32_t *pt_bin_out,
+                               double *info_out,
                                int32_t *L_out, int32_t *stair_bin, double *stair_Tlo,
                                double *stair_E, int32_t *n_stair, int32_t *status_out, void *ws,
                                size_t ws_bytes, void *stream)
@@ -434,6 +435,7 @@ kr_status kr_compose_frontiers(int32_t n_parts, const int64_t *off, const double
     a.E = E;
     a.F_out = F_out;
     a.bp = bp_out;
+    a.bp_off = bp_off_out;
     a.pt_bin = pt_bin_out;
     a.info = info_out;
     a.L_out = L_out;
@@ -449,7 +451,8 @@ kr_status kr_compose_frontiers(int32_t n_parts, const int64_t *off, const double
 }
 
 kr_status kr_extract_schedule(int32_t n_parts, int32_t n_bins, const int32_t *bp,
-                              const int32_t *pt_bin, const int64_t *off, const double *T,
+                              const int32_t *bp_off, const int32_t *pt_bin,
+                              const int64_t *off, const double *T,
                               const double *E, const int32_t *bins, int32_t n_q,
                               const int32_t *cand_idx, int32_t *choice_out,
                               int32_t *choice_cand_out, double *T_out, double *E_out,
@@ -464,6 +467,7 @@ kr_status kr_extract_schedule(int32_t n_parts, int32_t n_bins, const int32_t *bp
     a.B = n_bins;
     a.n_q = n_q;
     a.bp = bp;
+    a.bp_off = bp_off;
     a.pt_bin = pt_bin;
     a.bins = bins;
     a.cand_idx = cand_idx;

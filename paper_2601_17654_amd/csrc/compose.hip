@@ -14,6 +14,8 @@
 #include "kr_device.h"
 #include "kr_wave.h"
 
+#include <utility>
+
 namespace kr {
 
 struct MinF64 {
@@ -471,6 +473,7 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
         window(1)[t] = v;
         if (b < B) {
             a.bp[b] = who;
+            if (a.bp_off) a.bp_off[b] = who >= 0 ? (int32_t)b : -1;  // its offset is b
             if (P == 1) a.F_out[b] = v;
             else publish(0, v, meta(1).x, m0.y);
         }
@@ -489,7 +492,7 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
             const int M1 = last ? 0 : meta(k + 1).x;
             const double *const wc = window(k);
             double best = INFINITY;
-            int32_t who = -1;
+            int32_t who = -1, wo = -1;  // point and its offset
             if (!loader && b0 < mc.y) {
                 for (int x = 0; x < mc.w; ++x) {
                     const int64_t src = b - w.ob2[mc.z + x];
@@ -500,6 +503,7 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
                         if (v < best) {
                             best = v;
                             who = w.oarg[mc.z + x];
+                            wo = w.ob2[mc.z + x];
                         }
                     }
                 }
@@ -511,6 +515,7 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
                 window(k + 1)[t] = v;
                 if (b < B) {
                     a.bp[(int64_t)k * B + b] = live ? who : -1;
+                    if (a.bp_off) a.bp_off[(int64_t)k * B + b] = live ? wo : -1;
                     if (last) a.F_out[b] = v;
                     else publish(k, v, M1, mc.y);
                 }
@@ -525,16 +530,23 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
         issue(1, meta(1), m0.y);
         stage(1, meta(1), m0.y);
     }
-    // The point behind bin b0 + u's least value best of step k: the part's point (sparse)
-    // or the first offset of 8-offset group idx that reaches best (dense).
-    auto point = [&](int k, double best, int idx, bool dense, int u) -> int32_t {
-        if (!dense || idx < 0) return idx;
+    // The point behind bin b0 + u's least value best of step k, and its offset: the
+    // part's record (sparse) or the first offset of 8-offset group idx that reaches best
+    // (dense).  (-1, -1) if none.
+    auto point = [&](int k, double best, int idx, bool dense, int u, int32_t &off) -> int32_t {
+        off = -1;
+        if (idx < 0) return -1;
+        if (!dense) {
+            off = sm.off8[k & 1][idx] / 8;
+            return sm.arg[k & 1][idx];
+        }
         const double *const wp = window(k);
         const double *const ep = sm.e[k & 1];
         const int i8 = 8 * idx;
         int o = 7;
 #pragma unroll
         for (int d = 7; d >= 0; --d) o = wp[u - i8 - d] + ep[i8 + d] == best ? d : o;
+        off = i8 + o;
         return sm.arg[k & 1][i8 + o];
     };
     // Least value and its part's index for bin b0 + u from the partial minima.
@@ -672,7 +684,7 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
                     best = v < best ? v : best;
                 }
                 sm.pbest[qtr][t] = best;
-                sm.pidx[qtr][t] = bx >= 0 ? sm.arg[buf][bx] : -1;
+                sm.pidx[qtr][t] = bx;  // the record; its point and offset are read at the end
             }
         }
         __syncthreads();  // every partial minimum is in LDS
@@ -687,8 +699,12 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
                 if (last) a.F_out[b] = v;
                 else publish(k, v, mn.x, mc.y);
             }
-            const int32_t who = active ? point(k, best, idx, dense, t) : -1;
-            if (b < B) a.bp[(int64_t)k * B + b] = live ? who : -1;
+            int32_t wo = -1;
+            const int32_t who = active ? point(k, best, idx, dense, t, wo) : -1;
+            if (b < B) {
+                a.bp[(int64_t)k * B + b] = live ? who : -1;
+                if (a.bp_off) a.bp_off[(int64_t)k * B + b] = live ? wo : -1;
+            }
         } else if (!last) {
             // chunk c + 1 replaces chunk c - 1 once step cMC - 1 has read its metadata
             if ((k + 1) % MC == 0) load_meta((k + 1) / MC + 1);
@@ -981,10 +997,181 @@ __global__ void __launch_bounds__(64) extract_kernel(ExtractArgs a)
     a.ok[q] = ok;
 }
 
+// Walk over the recorded offsets (bp_off): the bin of row k - 1 is b - bp_off[k][b], so a
+// step needs one table entry and no point lookup.  The wave keeps windows of the next
+// KR_XW_D rows in registers: slot d holds KR_XW_W consecutive bins of its row (lane l
+// the 8 bins from base + 8 l), loaded KR_XW_D steps before the row is walked, so the
+// loads fly meanwhile.  A window is placed where the offsets of the last KR_XW_D rows put
+// that row's bin; a bin outside its window is loaded directly.  The bins of all rows are
+// kept in LDS, and the chosen points are gathered from bp afterwards, all rows at once.
+// At most KR_EX_LP partitions and KR_XW_MAX table entries (32-bit byte offsets).
+#define KR_XW_D 16   // rows of look-ahead
+#define KR_XW_W 512  // bins per window (8 per lane)
+#define KR_XW_MAX (1 << 29)
+typedef int32_t i32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));  // 4-byte aligned
+
+// f where the wave-uniform mask m is 0, t where it is all ones (one VALU select; the
+// compiler would branch on the uniform condition instead)
+__device__ __forceinline__ int32_t kr_usel(int32_t f, int32_t t, uint64_t m)
+{
+    int32_t r;
+    asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(f), "v"(t), "s"(m));
+    return r;
+}
+
+// v with lane L set to the wave-uniform s
+template <int L>
+__device__ __forceinline__ int32_t kr_setlane(int32_t v, int32_t s)
+{
+    asm("v_writelane_b32 %0, %1, %2" : "+v"(v) : "s"(s), "I"(L));
+    return v;
+}
+
+// f(std::integral_constant<int, I>) for I = 0 .. N - 1, in order, unrolled
+template <typename F, int... I>
+__device__ __forceinline__ void kr_unroll(F &&f, std::integer_sequence<int, I...>)
+{
+    (f(std::integral_constant<int, I>{}), ...);
+}
+
+__global__ void __launch_bounds__(64) extract_walk_kernel(ExtractArgs a)
+{
+    __shared__ double sT[KR_EX_RS], sE[KR_EX_RS];
+    __shared__ int64_t s_off[KR_EX_LP + 1];
+    __shared__ int32_t s_b[KR_EX_LP];
+    __shared__ int32_t s_ch[KR_EX_LP];
+    constexpr int D = KR_XW_D, W = KR_XW_W;
+    const int P = a.P;
+    const int32_t B = a.B;
+    const int32_t total = P * B;  // at most KR_XW_MAX
+    const int q = blockIdx.x, lane = threadIdx.x;
+    int32_t *choice = a.choice + (int64_t)q * P;
+    for (int k = lane; k <= P; k += 64) s_off[k] = a.off[k];
+
+    i32x4_a4 wl[D], wh[D];  // slot d: bins base[d] + 8 lane + 0..3, + 4..7 of its row
+    int32_t base[D];
+    // window of the row starting at table index r0, placed below bin bk by the predicted
+    // drift (a guess: any value works), then moved to lie inside the table (it holds at
+    // least W entries): entries that run into a neighbouring row are never read, since a
+    // walk's bins stay in [0, B)
+    auto issue = [&](int d, int32_t r0, int32_t bk, int32_t drift) {
+        int32_t x0 = r0 + min(bk - drift - W / 2, bk - (W - 1));
+        x0 = min(max(x0, 0), total - W);
+        base[d] = x0 - r0;
+        const uint32_t x = (uint32_t)(x0 + 8 * lane);
+        wl[d] = *(const i32x4_a4 *)(a.bp_off + x);
+        wh[d] = *(const i32x4_a4 *)(a.bp_off + x + 4);
+    };
+    // the recorded offset at bin bk of the row starting at r0: from slot d when bk is in
+    // its window, else loaded
+    auto lookup = [&](int d, int32_t r0, int32_t bk) -> int32_t {
+        const int32_t pos = bk - base[d];
+        const uint64_t m2 = (pos & 4) ? ~0ull : 0ull, m1 = (pos & 2) ? ~0ull : 0ull,
+                       m0 = (pos & 1) ? ~0ull : 0ull;
+        const int32_t y0 = kr_usel(wl[d].x, wh[d].x, m2), y1 = kr_usel(wl[d].y, wh[d].y, m2);
+        const int32_t y2 = kr_usel(wl[d].z, wh[d].z, m2), y3 = kr_usel(wl[d].w, wh[d].w, m2);
+        const int32_t z0 = kr_usel(y0, y2, m1), z1 = kr_usel(y1, y3, m1);
+        int32_t o = __builtin_amdgcn_readlane(kr_usel(z0, z1, m0), (pos >> 3) & 63);
+        if (__builtin_expect((uint32_t)pos >= (uint32_t)W, 0)) o = a.bp_off[r0 + bk];
+        return o;
+    };
+
+    const int32_t b_query = a.bins[q];
+    int32_t b = b_query;
+    bool ok = b >= 0 && b < B;
+    if (!ok) b = 0;  // walked anyway (the results are discarded)
+    // drift predicted for D rows: the offsets of the last D rows (to start with, the
+    // query bin spread over all rows)
+    int32_t hist[D];  // the bin D rows back, by slot
+    const int32_t avg0 = b / max(P, 1);
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+        hist[d] = b;
+        issue(d, max(P - 1 - d, 0) * B, b, d * avg0);
+    }
+    // lane d holds the bin of row k0 - d of the current block of D rows (top row k0)
+    int32_t brow = 0;
+    int32_t neg = 0;  // sign bit set once an offset is -1 (no point) or a bin falls below 0
+    // one row: take its offset, record its bin, refill its slot with the row D below.  A
+    // failed walk goes on from bin 0 (memory-safe) and is dropped at the end.
+    auto step = [&](auto dc, int32_t r0) {
+        constexpr int d = decltype(dc)::value;
+        const int32_t o = lookup(d, r0, b);
+        brow = kr_setlane<d>(brow, b);
+        const int32_t bn = b - o;
+        neg |= o | bn;
+        b = max(bn, 0);
+        const int32_t drift = hist[d] - b;  // the offsets of the last D rows
+        hist[d] = b;
+        issue(d, r0 - D * B, b, drift);  // row k - D (clamped into the table)
+    };
+    int k = P - 1;
+    int32_t rk = k * B;
+    for (; k >= D - 1; k -= D, rk -= D * B) {
+        kr_unroll([&](auto dc) { step(dc, rk - decltype(dc)::value * B); },
+                  std::make_integer_sequence<int, D>{});  // row k - d: slot d
+        if (lane < D) s_b[k - lane] = brow;
+    }
+    if (k >= 0) {  // the last rows, fewer than D
+        kr_unroll(
+            [&](auto dc) {
+                if (decltype(dc)::value <= k) step(dc, rk - decltype(dc)::value * B);
+            },
+            std::make_integer_sequence<int, D - 1>{});
+        if (lane <= k) s_b[k - lane] = brow;
+    }
+    ok = ok && neg >= 0;
+    ok = ok && b == 0;
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    // the chosen points, all rows at once
+    for (int kk = lane; kk < P; kk += 64) {
+        const int32_t c = ok ? a.bp[(int64_t)kk * B + s_b[kk]] : -1;
+        s_ch[kk] = c;
+        choice[kk] = c;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    // exact T and E of the choice: the lanes gather the chosen points' values into LDS,
+    // one lane adds them in partition order
+    double Ts = 0.0, Es = 0.0;
+    for (int k0 = 0; k0 < P; k0 += KR_EX_RS) {
+        const int kn = min(P - k0, KR_EX_RS);
+        for (int i = lane; i < kn; i += 64) {
+            const int kk = k0 + i;
+            const int32_t c = s_ch[kk];
+            if (ok) {
+                const int64_t x = s_off[kk] + c;
+                sT[i] = a.T[x];
+                sE[i] = a.E[x];
+                if (a.cand_idx) a.choice_cand[(int64_t)q * P + kk] = a.cand_idx[x];
+            } else if (a.cand_idx) {
+                a.choice_cand[(int64_t)q * P + kk] = -1;
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        if (ok && lane == 0)
+            for (int i = 0; i < kn; ++i) {
+                Ts = Ts + sT[i];
+                Es = Es + sE[i];
+            }
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront", "local");
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+    }
+    if (lane != 0) return;
+    a.T_out[q] = ok ? Ts : NAN;
+    a.E_out[q] = ok ? Es : NAN;
+    a.ok[q] = ok;
+}
+
 hipError_t launch_extract(const ExtractArgs &a, hipStream_t st)
 {
     if (a.n_q == 0) return hipSuccess;
-    if (a.P <= KR_EX_LP)
+    if (a.bp_off && a.P <= KR_EX_LP && (int64_t)a.P * a.B >= KR_XW_W &&
+        (int64_t)a.P * a.B <= KR_XW_MAX)
+        hipLaunchKernelGGL(extract_walk_kernel, dim3(a.n_q), dim3(64), 0, st, a);
+    else if (a.P <= KR_EX_LP)
         hipLaunchKernelGGL(extract_kernel<true>, dim3(a.n_q), dim3(64), 0, st, a);
     else
         hipLaunchKernelGGL(extract_kernel<false>, dim3(a.n_q), dim3(64), 0, st, a);

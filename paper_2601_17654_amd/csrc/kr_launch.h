@@ -131,6 +131,7 @@ struct ComposeArgs {
     const double *T, *E;
     double *F_out;
     int32_t *bp, *pt_bin;
+    int32_t *bp_off;  // NULL, or [P][B]: offset of the chosen point (like bp)
     double *info;
     int32_t *L_out, *stair_bin, *n_stair, *status;
     double *stair_Tlo, *stair_E;
@@ -146,6 +147,7 @@ hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipEvent_t *
 struct ExtractArgs {
     int P, B, n_q;
     const int32_t *bp, *pt_bin, *bins, *cand_idx;
+    const int32_t *bp_off;  // NULL, or the offsets kr_compose_frontiers recorded
     const int64_t *off;
     const double *T, *E;
     int32_t *choice, *choice_cand, *ok;

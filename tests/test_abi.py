@@ -67,9 +67,9 @@ def test_host_validation_without_gpu():
     assert L.kr_compose_frontiers_workspace(0, 1024) == 0
     # too small a workspace is refused on the host
     assert L.kr_compose_frontiers(4, one, one, one, 1024, 0.0, one, one, one, one, one, one, one,
-                                  one, one, one, one, 16, null) == b.KR_ECAPACITY
+                                  one, one, one, one, one, 16, null) == b.KR_ECAPACITY
     assert L.kr_compose_frontiers(4, one, one, one, 1024, -1.0, one, one, one, one, one, one, one,
-                                  one, one, one, one, 1 << 30, null) == b.KR_EINVAL
+                                  one, one, one, one, one, 1 << 30, null) == b.KR_EINVAL
     assert b.candidates_per_partition(I.SPACES[2]["space"]) == 1148928
     # scores and selection: shapes and counts are checked before any launch
     assert L.kr_hvi_scores_workspace(0, 10) == 0 and L.kr_hvi_scores_workspace(4, 0) == 0

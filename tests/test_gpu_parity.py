@@ -315,6 +315,12 @@ def compare_composed(kr, comp, ref, off, T, E, what):
     assert_close(comp.F.cpu().numpy(), ref.F, RT_MINPLUS, what + " F")
     np.testing.assert_array_equal(comp.pt_bin.cpu().numpy()[:len(ref.pt_bin)], ref.pt_bin)
     np.testing.assert_array_equal(comp.bp.cpu().numpy(), ref.bp, err_msg=what + " bp")
+    # the recorded offsets are the chosen points' offsets in the oracle's binning
+    want = np.full(ref.bp.shape, -1, dtype=np.int64)
+    for k in range(ref.bp.shape[0]):
+        sel = ref.bp[k] >= 0
+        want[k, sel] = ref.pt_bin[off[k] + ref.bp[k, sel]]
+    np.testing.assert_array_equal(comp.bp_off.cpu().numpy(), want, err_msg=what + " bp_off")
 
 
 @pytest.fixture(scope="module")
@@ -497,6 +503,46 @@ def test_compose_edge_cases(kr, oracle_lib):
                                 delta=0.5)
     assert int(comp.status.item()) == kr.KR_ECAPACITY
     assert int(comp.n_stair.item()) == 0
+
+
+def test_extract_walks(kr, oracle_lib, config4):
+    """Both schedule walks against the oracle: over the recorded offsets with windows
+    read rows ahead (query bins spread over the whole axis, so windows both hit and
+    miss), and with each chosen point's offset looked up (Section 5.1)."""
+    rng = np.random.default_rng(23)
+    cases = [("cfg4",) + tuple(config4) + (I.COMPOSE_SPACE["bins"],)]
+    n = rng.integers(20, 60, 6)
+    n[2] = 3000
+    span = rng.uniform(1e-3, 2e-3, 6)
+    span[2] = 0.08  # offsets wider than a window
+    cases.append(("wide",) + tuple(I.frontier_batch(101, n.tolist(), span.tolist())) + (8192,))
+    cases.append(("tiny", np.array([0, 2, 5], dtype=np.int64), np.array([1e-3, 2e-3, 1e-3, 3e-3,
+                  5e-3]), np.array([2.0, 1.0, 3.0, 2.0, 1.0]), 4))
+    for what, off, T, E, B in cases:
+        print("extract walks case", what, flush=True)
+        Td, Ed, od = torch.from_numpy(T).cuda(), torch.from_numpy(E).cuda(), torch.from_numpy(off).cuda()
+        comp = kr.compose_frontiers(od, Td, Ed, B)
+        ref = oracle_lib.compose(off, T, E, B)
+        reach = np.flatnonzero(np.isfinite(ref.F))
+        rb, _, _ = oracle_lib.staircase(ref.F, ref.delta, ref.tmin_sum)
+        bins = np.concatenate([rb[:40], rb[-40:], rng.choice(reach, size=min(24, len(reach)),
+                               replace=False), [0, ref.L - 1, B - 1]]).astype(np.int32)
+        outs = [kr.extract_schedule(comp, od, Td, Ed, torch.from_numpy(bins).cuda(),
+                                    use_offsets=u) for u in (True, False)]
+        outs = [[x.cpu().numpy() for x in (o[0], o[2], o[3], o[4])] for o in outs]
+        for x, y in zip(outs[0], outs[1]):  # the two walks agree bit for bit
+            np.testing.assert_array_equal(x.view(np.uint8), y.view(np.uint8), err_msg=what)
+        ch, Ts, Es, ok = outs[0]
+        for q, bq in enumerate(bins):
+            live = bq < ref.L and np.isfinite(ref.F[bq])
+            assert ok[q] == int(live), (what, int(bq))
+            if live:
+                rc, rts, res = oracle_lib.extract(off, T, E, ref, int(bq))
+                np.testing.assert_array_equal(ch[q], rc, err_msg="%s bin %d" % (what, bq))
+                assert_close(Ts[q], rts, RT_TE, "%s extract T bin %d" % (what, bq))
+                assert_close(Es[q], res, RT_TE, "%s extract E bin %d" % (what, bq))
+            else:
+                assert (ch[q] == -1).all()
 
 
 def test_decode(kr, oracle_lib):
