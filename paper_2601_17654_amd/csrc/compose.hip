@@ -592,8 +592,9 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
                 const int j = tid % (KR_MP_W / 2);
                 const int q = __builtin_amdgcn_readfirstlane(tid / (KR_MP_W / 2));
                 const int ng = (mc.x + 8) / 8;
-                const int g0 = ng * q / KR_WF_S, g1 = ng * (q + 1) / KR_WF_S;
-                const_f64 *et = (const_f64 *)(w.ebits + mc.z);
+                const int g0 = __builtin_amdgcn_readfirstlane(ng * q / KR_WF_S);
+                const int g1 = __builtin_amdgcn_readfirstlane(ng * (q + 1) / KR_WF_S);
+                const_f64 *et = (const_f64 *)(w.ebits + __builtin_amdgcn_readfirstlane(mc.z));
                 double best0 = INFINITY, best1 = INFINITY;
                 int bg0 = -1, bg1 = -1;
                 // one group of 8 offsets: updates the two running minima
