@@ -505,19 +505,53 @@ def test_compose_edge_cases(kr, oracle_lib):
     assert int(comp.n_stair.item()) == 0
 
 
+def window_hits(bp_off, b, D=16, W=512):
+    """(hits, misses) of the offset walk's register windows for a walk from bin b: the
+    placement rules of the walk kernel (a window of W bins per row, loaded D rows
+    ahead, placed below the bin by the offsets of the last D rows), replayed on the
+    host so that a test can show it reaches both the window reads and the direct
+    loads."""
+    P, B = bp_off.shape
+    total = P * B
+    base = [0] * D
+
+    def place(d, r0, bk, drift):
+        x0 = min(max(r0 + min(bk - drift - W // 2, bk - (W - 1)), 0), total - W)
+        base[d] = x0 - r0
+
+    hist = [b] * D
+    for d in range(D):
+        place(d, max(P - 1 - d, 0) * B, b, d * (b // max(P, 1)))
+    hits = misses = 0
+    for k in range(P - 1, -1, -1):
+        d = (P - 1 - k) % D
+        if 0 <= b - base[d] < W:
+            hits += 1
+        else:
+            misses += 1
+        b = b - int(bp_off[k, b])
+        drift, hist[d] = hist[d] - b, b
+        place(d, (k - D) * B, b, drift)
+    return hits, misses
+
+
 def test_extract_walks(kr, oracle_lib, config4):
     """Both schedule walks against the oracle: over the recorded offsets with windows
     read rows ahead (query bins spread over the whole axis, so windows both hit and
     miss), and with each chosen point's offset looked up (Section 5.1)."""
     rng = np.random.default_rng(23)
     cases = [("cfg4",) + tuple(config4) + (I.COMPOSE_SPACE["bins"],)]
-    n = rng.integers(20, 60, 6)
-    n[2] = 3000
-    span = rng.uniform(1e-3, 2e-3, 6)
-    span[2] = 0.08  # offsets wider than a window
+    n = rng.integers(20, 60, 40)
+    n[[2, 25]] = 3000
+    span = rng.uniform(1e-3, 2e-3, 40)
+    span[[2, 25]] = 0.04  # offsets wider than a window
     cases.append(("wide",) + tuple(I.frontier_batch(101, n.tolist(), span.tolist())) + (8192,))
+    # one partition: the walk is the last-rows path alone (table of exactly one window)
+    cases.append(("one",) + tuple(I.frontier_batch(102, [300], [1e-3])) + (512,))
+    # a table smaller than a window: the point-lookup walk
     cases.append(("tiny", np.array([0, 2, 5], dtype=np.int64), np.array([1e-3, 2e-3, 1e-3, 3e-3,
                   5e-3]), np.array([2.0, 1.0, 3.0, 2.0, 1.0]), 4))
+    hm_all = np.zeros(2, dtype=np.int64)
     for what, off, T, E, B in cases:
         print("extract walks case", what, flush=True)
         Td, Ed, od = torch.from_numpy(T).cuda(), torch.from_numpy(E).cuda(), torch.from_numpy(off).cuda()
@@ -533,6 +567,12 @@ def test_extract_walks(kr, oracle_lib, config4):
         for x, y in zip(outs[0], outs[1]):  # the two walks agree bit for bit
             np.testing.assert_array_equal(x.view(np.uint8), y.view(np.uint8), err_msg=what)
         ch, Ts, Es, ok = outs[0]
+        if what in ("cfg4", "wide"):  # walks that read windows and load directly
+            bo = comp.bp_off.cpu().numpy()
+            hm = np.array([window_hits(bo, int(bq)) for bq in bins if bq < ref.L and
+                           np.isfinite(ref.F[bq])]).sum(axis=0)
+            print("window hits, misses:", hm, flush=True)
+            hm_all += hm
         for q, bq in enumerate(bins):
             live = bq < ref.L and np.isfinite(ref.F[bq])
             assert ok[q] == int(live), (what, int(bq))
@@ -543,6 +583,7 @@ def test_extract_walks(kr, oracle_lib, config4):
                 assert_close(Es[q], res, RT_TE, "%s extract E bin %d" % (what, bq))
             else:
                 assert (ch[q] == -1).all()
+    assert hm_all[0] > 0 and hm_all[1] > 0, hm_all
 
 
 def test_decode(kr, oracle_lib):
