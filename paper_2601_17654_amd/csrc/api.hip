@@ -314,7 +314,8 @@ kr_status kr_pareto_filter(int64_t n_total, const double *T, const double *E,
     L.unit_base = w.unit_base;
     L.n_seg = n_seg;
     L.unit_stride = KR_TILE;
-    if (n_seg > 0 && launch_tile_layout(seg_off, w.unit_base, n_seg, KR_TILE, st) != hipSuccess)
+    if (n_seg > 0 &&
+        launch_tile_layout(seg_off, w.unit_base, n_seg, KR_TILE, w.lists, st) != hipSuccess)
         return KR_EHIP;
     UnitOut o{w.buf[0].T, w.buf[0].E, w.buf[0].I, w.ucnt};
     if (n_seg > 0 && launch_pareto_tiles(T, E, L, n_units, o, st) != hipSuccess) return KR_EHIP;
@@ -349,7 +350,8 @@ kr_status kr_evaluate_and_filter(const kr_space *space, const double *t, const d
     a.pc = pc;
     Carve c(ws);
     FilterWs w = carve_filter(c, (int64_t)a.P * a.useg, a.P, (int64_t)a.P * a.uper, true);
-    if (launch_uniform_layout(w.seg_off, w.unit_base, a.P, a.useg, a.uper, st) != hipSuccess)
+    if (launch_uniform_layout(w.seg_off, w.unit_base, a.P, a.useg, a.uper, w.lists, st) !=
+        hipSuccess)
         return KR_EHIP;
     UnitOut o{w.buf[0].T, w.buf[0].E, w.buf[0].I, w.ucnt};
     a.dma16 = (a.wave || a.pair) && (a.N * (a.S + 1)) % 2 == 0 && (uintptr_t)t % 16 == 0 &&

@@ -92,13 +92,16 @@ int pair_owner_host(int p1, int NW);
 hipError_t launch_decode(const DecodeArgs &d, hipStream_t st);
 
 // pareto.hip
+// Both layouts also clear lists[0], which launch_finalize expects to be zero.
 hipError_t launch_uniform_layout(int64_t *seg_off, int64_t *unit_base, int n_seg,
-                                 int64_t seg_len, int64_t units_per_seg, hipStream_t st);
+                                 int64_t seg_len, int64_t units_per_seg, int32_t *lists,
+                                 hipStream_t st);
 hipError_t launch_tile_layout(const int64_t *seg_off, int64_t *unit_base, int n_seg, int tile,
-                              hipStream_t st);
+                              int32_t *lists, hipStream_t st);
 hipError_t launch_pareto_tiles(const double *T, const double *E, const SegLayout &L,
                                int64_t n_units_bound, const UnitOut &o, hipStream_t st);
-// lists: 2 * n_seg + 2 ints of scratch
+// lists: 2 * n_seg + 2 ints of scratch, lists[0] zero on entry (cleared by the layout
+// launches above)
 hipError_t launch_finalize(const SegLayout &L, const PointBufs &buf, const int32_t *ucnt,
                            const PointBufs &fin, int32_t *fcnt, int32_t *runcnt, uint8_t *flags,
                            int32_t *lists, hipStream_t st);

@@ -19,28 +19,35 @@
 
 namespace kr {
 
+// The layout kernels also clear lists[0], the count of segments that the first merge
+// stage passes on (so that the merge needs no launch of its own for it).
 __global__ void uniform_layout_kernel(int64_t *seg_off, int64_t *unit_base, int n_seg,
-                                      int64_t seg_len, int64_t units_per_seg)
+                                      int64_t seg_len, int64_t units_per_seg, int32_t *lists)
 {
     const int g = blockIdx.x * KR_BLOCK + threadIdx.x;
+    if (g == 0) lists[0] = 0;
     if (g > n_seg) return;
     seg_off[g] = (int64_t)g * seg_len;
     unit_base[g] = (int64_t)g * units_per_seg;
 }
 
 hipError_t launch_uniform_layout(int64_t *seg_off, int64_t *unit_base, int n_seg,
-                                 int64_t seg_len, int64_t units_per_seg, hipStream_t st)
+                                 int64_t seg_len, int64_t units_per_seg, int32_t *lists,
+                                 hipStream_t st)
 {
     hipLaunchKernelGGL(uniform_layout_kernel, dim3((n_seg + 1 + KR_BLOCK - 1) / KR_BLOCK),
-                       dim3(KR_BLOCK), 0, st, seg_off, unit_base, n_seg, seg_len, units_per_seg);
+                       dim3(KR_BLOCK), 0, st, seg_off, unit_base, n_seg, seg_len, units_per_seg,
+                       lists);
     return hipGetLastError();
 }
 
 // unit_base = exclusive prefix sum of ceil(len_g / tile); one block.
 __global__ void __launch_bounds__(KR_BLOCK)
-tile_layout_kernel(const int64_t *seg_off, int64_t *unit_base, int n_seg, int tile)
+tile_layout_kernel(const int64_t *seg_off, int64_t *unit_base, int n_seg, int tile,
+                   int32_t *lists)
 {
     __shared__ int64_t sc[KR_WAVES];
+    if (threadIdx.x == 0) lists[0] = 0;
     int64_t carry = 0;
     for (int g0 = 0; g0 < n_seg; g0 += KR_BLOCK) {
         const int g = g0 + threadIdx.x;
@@ -58,10 +65,10 @@ tile_layout_kernel(const int64_t *seg_off, int64_t *unit_base, int n_seg, int ti
 }
 
 hipError_t launch_tile_layout(const int64_t *seg_off, int64_t *unit_base, int n_seg, int tile,
-                              hipStream_t st)
+                              int32_t *lists, hipStream_t st)
 {
     hipLaunchKernelGGL(tile_layout_kernel, dim3(1), dim3(KR_BLOCK), 0, st, seg_off, unit_base,
-                       n_seg, tile);
+                       n_seg, tile, lists);
     return hipGetLastError();
 }
 
@@ -467,11 +474,6 @@ finalize_large_kernel(SegLayout L, PointBufs buf, const int32_t *ucnt, PointBufs
     }
 }
 
-__global__ void finalize_lists_init_kernel(int32_t *lists)
-{
-    if (threadIdx.x == 0) lists[0] = 0;
-}
-
 // Stage 3, the segments on the second list: one block per segment (blocks loop over
 // the list).  The union is sorted in LDS when it fits; otherwise it is cut into
 // LDS-sized chunks whose frontiers are merged pairwise in device memory.
@@ -603,7 +605,6 @@ hipError_t launch_finalize(const SegLayout &L, const PointBufs &buf, const int32
 {
     if (L.n_seg == 0) return hipSuccess;
     const dim3 loop_grid(min(L.n_seg, 256));
-    hipLaunchKernelGGL(finalize_lists_init_kernel, dim3(1), dim3(64), 0, st, lists);
     hipLaunchKernelGGL(finalize_small_kernel, dim3(L.n_seg), dim3(KR_FM_SMALL_NT), 0, st, L, buf,
                        ucnt, fin, fcnt, lists);
     hipLaunchKernelGGL(finalize_large_kernel, loop_grid, dim3(KR_FM_LARGE_NT), 0, st, L, buf,
@@ -646,10 +647,43 @@ copy_out_kernel(SegLayout L, PointBufs fin, const int64_t *out_off, int64_t cap,
     }
 }
 
+// Up to KR_OUT_SCAN segments: each block forms its segment's output offset itself (the
+// sum of the counts before it, in integers, so equal to the scan's) and copies the
+// segment, with no separate scan launch.
+#define KR_OUT_SCAN 4096
+__global__ void __launch_bounds__(KR_BLOCK)
+copy_out_scan_kernel(SegLayout L, PointBufs fin, const int32_t *fcnt, int64_t *out_off,
+                     int64_t cap, int32_t *out_idx, double *out_T, double *out_E)
+{
+    __shared__ int64_t sc[KR_WAVES];
+    const int g = blockIdx.x;
+    int64_t part = 0;
+    for (int h = threadIdx.x; h < g; h += KR_BLOCK) part += fcnt[h];
+    const int64_t dst0 = block_reduce(part, (int64_t)0, SumI64(), sc);
+    const int64_t n = fcnt[g];
+    if (threadIdx.x == 0) {
+        out_off[g] = dst0;
+        if (g == L.n_seg - 1) out_off[L.n_seg] = dst0 + n;
+    }
+    const int64_t src0 = L.seg_off[g];
+    for (int64_t x = threadIdx.x; x < n; x += KR_BLOCK) {
+        const int64_t d = dst0 + x;
+        if (d >= cap) break;
+        out_idx[d] = fin.I[src0 + x];
+        out_T[d] = fin.T[src0 + x];
+        out_E[d] = fin.E[src0 + x];
+    }
+}
+
 hipError_t launch_output(const SegLayout &L, const PointBufs &fin, const int32_t *fcnt,
                          int64_t cap, int64_t *out_off, int32_t *out_idx, double *out_T,
                          double *out_E, hipStream_t st)
 {
+    if (L.n_seg > 0 && L.n_seg <= KR_OUT_SCAN) {
+        hipLaunchKernelGGL(copy_out_scan_kernel, dim3(L.n_seg), dim3(KR_BLOCK), 0, st, L, fin,
+                           fcnt, out_off, cap, out_idx, out_T, out_E);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL(count_scan_kernel, dim3(1), dim3(KR_BLOCK), 0, st, L.n_seg, fcnt, out_off);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || L.n_seg == 0) return e;

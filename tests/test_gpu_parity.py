@@ -232,10 +232,14 @@ def _tied(rng, n):
     return T, E
 
 
-@pytest.mark.parametrize("kind", ["tied", "continuous", "staircase", "mixed-lengths"])
+@pytest.mark.parametrize("kind", ["tied", "continuous", "staircase", "mixed-lengths",
+                                  "many-segments"])
 def test_pareto_filter(kr, oracle_lib, kind):
-    rng = np.random.default_rng({"tied": 1, "continuous": 2, "staircase": 3}.get(kind, 4))
-    if kind == "tied":
+    rng = np.random.default_rng({"tied": 1, "continuous": 2, "staircase": 3,
+                                 "many-segments": 5}.get(kind, 4))
+    if kind == "many-segments":  # more segments than one output block scans for itself
+        lens = list(rng.integers(0, 24, size=5000))
+    elif kind == "tied":
         lens = [0, 1, 2, 7, 2047, 2048, 2049, 5000, 0, 12345]
     elif kind == "continuous":
         lens = [100000, 3, 65536, 1]
@@ -305,6 +309,15 @@ def test_pareto_filter_capacity(kr):
     assert torch.equal(fr.idx[:100].cpu(), torch.arange(100, dtype=torch.int32))
     fr = kr.pareto_filter(T, E, seg)  # grows its capacity and retries
     assert fr.idx.numel() == 5000
+    # several segments, the capacity ending inside the second: the entries up to it match
+    # the uncapped output and the offsets are complete
+    seg = np.array([0, 2000, 3000, 5000], dtype=np.int64)
+    full = kr.pareto_filter(T, E, seg)
+    part = kr.pareto_filter(T, E, seg, cap=2500, sync=False)
+    torch.cuda.synchronize()
+    assert torch.equal(part.off.cpu(), full.off.cpu())
+    for x, y in ((part.idx, full.idx), (part.T, full.T), (part.E, full.E)):
+        assert torch.equal(x[:2500].cpu(), y[:2500].cpu())
 
 
 def compare_composed(kr, comp, ref, off, T, E, what):
