@@ -848,12 +848,8 @@ __global__ void __launch_bounds__(KR_ST_NT) staircase_write_kernel(ComposeArgs a
             a.stair_E[pos] = v[q];
             ++pos;
         }
-    if (blockIdx.x == 0 && threadIdx.x == 0) *a.n_stair = ta;
-}
-
-__global__ void staircase_skip_kernel(ComposeArgs a)
-{
-    if (*a.status != KR_OK) *a.n_stair = 0;
+    // a composition that failed (status set by an earlier kernel) has no staircase
+    if (blockIdx.x == 0 && threadIdx.x == 0) *a.n_stair = *a.status == KR_OK ? ta : 0;
 }
 
 hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipEvent_t *minplus_ev,
@@ -874,7 +870,6 @@ hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipEvent_t *
         hipLaunchKernelGGL(staircase_min_kernel, dim3(nb), dim3(KR_ST_NT), 0, st, a, w);
         hipLaunchKernelGGL(staircase_count_kernel, dim3(nb), dim3(KR_ST_NT), 0, st, a, w);
         hipLaunchKernelGGL(staircase_write_kernel, dim3(nb), dim3(KR_ST_NT), 0, st, a, w);
-        hipLaunchKernelGGL(staircase_skip_kernel, dim3(1), dim3(1), 0, st, a);
     }
     return hipGetLastError();
 }
