@@ -237,18 +237,6 @@ __device__ __forceinline__ void bin_partition(const ComposeArgs &a, const Compos
     }
 }
 
-__global__ void __launch_bounds__(KR_BLOCK) compose_bin_kernel(ComposeArgs a, ComposeWs w)
-{
-    __shared__ uint64_t seb[KR_BIN_CAP];
-    __shared__ int32_t sea[KR_BIN_CAP];
-    __shared__ int32_t sc[KR_WAVES];
-    if (*a.status != KR_OK) return;
-    const int k = blockIdx.x;
-    if (w.Mk[k] < KR_BIN_CAP)
-        bin_partition(a, w, k, seb, sea, sc);
-    else
-        bin_partition(a, w, k, w.ebits + w.eoff[k], w.earg + w.eoff[k], sc);
-}
 
 // All min-plus steps in one launch, as a wavefront over (tile, step).  Block g owns
 // the KR_MP_W bins of tile g for every step: F_k of its own bins stays in LDS from one
@@ -280,16 +268,28 @@ __device__ __forceinline__ bool exported(int64_t x, int64_t M1, int64_t L)
     return x < L && (x % KR_MP_W) >= KR_MP_W - M1;
 }
 
-// Marks every entry of the step history that some tile will publish as unwritten.
-// One block per row k = 0 .. P-2.
-__global__ void __launch_bounds__(KR_BLOCK) wavefront_fill_kernel(ComposeArgs a, ComposeWs w)
+// Blocks 0 .. P-1 bin partition k = blockIdx.x.  Blocks P .. 2P-2 mark every entry of
+// step-history row k = blockIdx.x - P that some tile will publish as unwritten.  The
+// two are independent (both need only the setup), so they share one launch.
+__global__ void __launch_bounds__(KR_BLOCK) compose_bin_fill_kernel(ComposeArgs a, ComposeWs w)
 {
+    __shared__ uint64_t seb[KR_BIN_CAP];
+    __shared__ int32_t sea[KR_BIN_CAP];
+    __shared__ int32_t sc[KR_WAVES];
     if (*a.status != KR_OK) return;
+    if ((int)blockIdx.x >= a.P) {
+        const int k = blockIdx.x - a.P;
+        const int64_t L = min(w.Lk[k], (int64_t)a.B), M1 = w.Mk[k + 1];
+        uint64_t *row = (uint64_t *)w.Fh + (int64_t)k * a.B;
+        for (int64_t x = threadIdx.x; x < L; x += KR_BLOCK)
+            if (exported(x, M1, L)) row[x] = KR_UNSET;
+        return;
+    }
     const int k = blockIdx.x;
-    const int64_t L = min(w.Lk[k], (int64_t)a.B), M1 = w.Mk[k + 1];
-    uint64_t *row = (uint64_t *)w.Fh + (int64_t)k * a.B;
-    for (int64_t x = threadIdx.x; x < L; x += KR_BLOCK)
-        if (exported(x, M1, L)) row[x] = KR_UNSET;
+    if (w.Mk[k] < KR_BIN_CAP)
+        bin_partition(a, w, k, seb, sea, sc);
+    else
+        bin_partition(a, w, k, w.ebits + w.eoff[k], w.earg + w.eoff[k], sc);
 }
 
 #define KR_WF_MC 512  // steps per chunk of the block's step-metadata ring
@@ -558,15 +558,26 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
             pv[q] = sm.pbest[q][u];
             pi[q] = sm.pidx[q][u];
         }
-        best = INFINITY;
-        idx = -1;
+        // the first part (in offset order) with the least value, as a tree: a later part
+        // replaces an earlier one only if strictly less.  A part with no candidate holds
+        // (INFINITY, -1), so with none at all the result is (INFINITY, -1).
+        if (!dense) {
 #pragma unroll
-        for (int q = 0; q < KR_WF_S; ++q) {  // the first part (in offset order) with the least
-            if ((dense || q < KR_MP_Q) && pv[q] < best) {
-                best = pv[q];
-                idx = pi[q];
+            for (int q = KR_MP_Q; q < KR_WF_S; ++q) {
+                pv[q] = INFINITY;
+                pi[q] = -1;
             }
         }
+#pragma unroll
+        for (int d = 1; d < KR_WF_S; d *= 2)
+#pragma unroll
+            for (int q = 0; q + d < KR_WF_S; q += 2 * d)
+                if (pv[q + d] < pv[q]) {
+                    pv[q] = pv[q + d];
+                    pi[q] = pi[q + d];
+                }
+        best = pv[0];
+        idx = pi[0];
     };
     for (int k = 1; k < P; ++k) {
         __syncthreads();  // window and records of step k are in LDS
@@ -858,10 +869,8 @@ hipError_t launch_compose(const ComposeArgs &a, const ComposeWs &w, hipEvent_t *
     hipLaunchKernelGGL(compose_init_kernel, dim3(1), dim3(64), 0, st, a, w);
     hipLaunchKernelGGL(compose_range_kernel, dim3(a.P), dim3(KR_BLOCK), 0, st, a, w);
     hipLaunchKernelGGL(compose_setup_kernel, dim3(1), dim3(KR_BLOCK), 0, st, a, w);
-    hipLaunchKernelGGL(compose_bin_kernel, dim3(a.P), dim3(KR_BLOCK), 0, st, a, w);
+    hipLaunchKernelGGL(compose_bin_fill_kernel, dim3(2 * a.P - 1), dim3(KR_BLOCK), 0, st, a, w);
     const int G = (a.B + KR_MP_W - 1) / KR_MP_W;
-    if (a.P > 1)
-        hipLaunchKernelGGL(wavefront_fill_kernel, dim3(a.P - 1), dim3(KR_BLOCK), 0, st, a, w);
     if (minplus_ev) (void)hipEventRecord(minplus_ev[0], st);
     hipLaunchKernelGGL(minplus_wavefront_kernel, dim3(G), dim3(KR_MP_W * KR_MP_Q), 0, st, a, w);
     if (minplus_ev) (void)hipEventRecord(minplus_ev[1], st);
