@@ -450,6 +450,10 @@ def test_compose_wavefront_modes(kr, oracle_lib):
     cases.append(("wide", n, span, 8192))
     n = rng.integers(10, 31, 1300)
     cases.append(("long", n, rng.uniform(0.5e-3, 1.5e-3, 1300), 32768))
+    # more partitions than the extraction keeps in LDS (the walk that reads offsets and
+    # choices from memory)
+    n = rng.integers(1, 4, 2100)
+    cases.append(("many", n, rng.uniform(1e-5, 2e-5, 2100), 8192))
     for i, (what, n, span, B) in enumerate(cases):
         off, T, E = I.frontier_batch(100 + i, n.tolist(), span.tolist())
         print("compose wavefront case", what, flush=True)
@@ -464,6 +468,10 @@ def test_compose_wavefront_modes(kr, oracle_lib):
                                [B - 1]]).astype(np.int32)
         ch, _, Ts, Es, ok = kr.extract_schedule(comp, off, T, E, torch.from_numpy(bins).cuda())
         ch, Ts, Es, ok = ch.cpu().numpy(), Ts.cpu().numpy(), Es.cpu().numpy(), ok.cpu().numpy()
+        alt = kr.extract_schedule(comp, off, T, E, torch.from_numpy(bins).cuda(),
+                                  use_offsets=False)  # the point-lookup walk: the same
+        for x, y in zip((ch, Ts, Es, ok), (alt[0], alt[2], alt[3], alt[4])):
+            np.testing.assert_array_equal(x.view(np.uint8), y.cpu().numpy().view(np.uint8))
         for q, bq in enumerate(bins):
             if bq >= ref.L or not np.isfinite(ref.F[bq]):
                 assert ok[q] == 0
