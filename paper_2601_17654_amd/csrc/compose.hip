@@ -587,7 +587,12 @@ __global__ void __launch_bounds__(KR_MP_W *KR_MP_Q) minplus_wavefront_kernel(Com
         const bool dense = dense_step(mc);
         const int4 mn = meta(last ? k : k + 1);
         const bool moves = loader && !last && busy(mn);
-        if (moves) issue(k + 1, mn, mc.y);
+        if (moves) {
+            // ahead of the SIMD's other waves: the loads then fly during their scans
+            __builtin_amdgcn_s_setprio(2);
+            issue(k + 1, mn, mc.y);
+            __builtin_amdgcn_s_setprio(0);
+        }
         const int buf = k & 1;
         const double *const wc = window(k);
         if (active) {
